@@ -1,0 +1,327 @@
+/*
+ * CPU oracle for MEC, the memory-efficient convolution of Cho & Brand,
+ * "MEC: Memory-efficient Convolution for Deep Neural Network" (ICML 2017).
+ *
+ * TEST INFRASTRUCTURE ONLY. This file is the plain, slow reference against
+ * which the GPU library is checked. Only the test suite, the smoke check and
+ * the CPU-baseline leg of the benchmark may load it. It shares no code,
+ * header, table or helper with the GPU library, and the GPU library must
+ * never call it.
+ *
+ * Notation follows Table 1 of the paper: input I is i_n x i_h x i_w x i_c
+ * (n-h-w-c, row-major), kernel K is k_h x k_w x i_c x k_c, output O is
+ * i_n x o_h x o_w x k_c, lowered tensor L is i_n x o_w x i_h x k_w x i_c,
+ * and s_h, s_w are the kernel strides. Padding is assumed to have been
+ * applied to I already (Section 2.1).
+ *
+ * Element types of I, K and L: dtype 0 is IEEE fp32, dtype 1 is bfloat16
+ * stored as its 16-bit pattern. Every product and sum here is done in fp64;
+ * bf16 and fp32 values widen to fp64 exactly, so each output is the exact
+ * dot product up to one fp64 rounding per addition.
+ *
+ * Readings of the paper taken here:
+ *  - Eq. (1) gives no rounding rule when s does not divide i - k; the
+ *    output size is floor((i - k) / s) + 1.
+ *  - Eqs. (2)-(4) write k_c where the lowered row length is i_c; the sizes
+ *    use i_c, as Algorithm 2 (its allocation of L) and the shape of K do.
+ *  - The operation is cross-correlation: kernel element (a, b) multiplies
+ *    input pixel (y*s_h + a, x*s_w + b), with no kernel flip (Section 3.1:
+ *    each output is the dot product of K with a sliding sub-matrix of I).
+ *  - L spans all i_h input rows (Algorithm 2 allocates and fills
+ *    i_n*o_w*i_h*k_w*i_c elements).
+ *
+ * Build: gcc -O2 -fopenmp -shared -fPIC (see build.py beside this file).
+ */
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define DT_F32 0
+#define DT_BF16 1
+
+/* Widen one element of a dtype-tagged array to fp64. Both conversions are
+ * exact: a bf16 pattern is the top half of an fp32 pattern. */
+static double elem(const void* base, int64_t idx, int dtype)
+{
+    if (dtype == DT_F32) {
+        return (double)((const float*)base)[idx];
+    } else {
+        uint32_t bits = (uint32_t)((const uint16_t*)base)[idx] << 16;
+        float f;
+        memcpy(&f, &bits, sizeof f);
+        return (double)f;
+    }
+}
+
+static int64_t elem_bytes(int dtype) { return dtype == DT_F32 ? 4 : 2; }
+
+/* Eq. (1): o = (i - k) / s + 1, read with floor division. Callers keep
+ * i >= k >= 1 and s >= 1, so C's truncating division is the floor. */
+int64_t oracle_out_dim(int64_t i, int64_t k, int64_t s)
+{
+    return (i - k) / s + 1;
+}
+
+/* Size of MEC's lowered tensor L, in elements: Algorithm 2 allocates
+ * i_n*o_w*i_h*k_w*i_c elements (Eq. (3) with the i_c reading). */
+int64_t oracle_lowered_elems(int64_t i_n, int64_t i_h, int64_t i_w, int64_t i_c,
+                             int64_t k_h, int64_t k_w, int64_t k_c,
+                             int64_t s_h, int64_t s_w)
+{
+    (void)k_h; (void)k_c; (void)s_h;
+    int64_t o_w = oracle_out_dim(i_w, k_w, s_w);
+    return i_n * o_w * i_h * k_w * i_c;
+}
+
+/* Size of the im2col lowered matrix of Section 3.1, in elements:
+ * (i_n*o_h*o_w) rows by (k_h*k_w*i_c) columns (Eq. (2), i_c reading). */
+int64_t oracle_im2col_elems(int64_t i_n, int64_t i_h, int64_t i_w, int64_t i_c,
+                            int64_t k_h, int64_t k_w, int64_t k_c,
+                            int64_t s_h, int64_t s_w)
+{
+    (void)k_c;
+    int64_t o_h = oracle_out_dim(i_h, k_h, s_h);
+    int64_t o_w = oracle_out_dim(i_w, k_w, s_w);
+    return i_n * o_h * o_w * k_h * k_w * i_c;
+}
+
+/* Eq. (4), second form: R = i_n*i_c*o_w*k_w*(o_h*k_h - i_h), the number of
+ * elements MEC's L saves over im2col. Negative when s_h > k_h. */
+int64_t oracle_saving_R(int64_t i_n, int64_t i_h, int64_t i_w, int64_t i_c,
+                        int64_t k_h, int64_t k_w, int64_t k_c,
+                        int64_t s_h, int64_t s_w)
+{
+    (void)k_c;
+    int64_t o_h = oracle_out_dim(i_h, k_h, s_h);
+    int64_t o_w = oracle_out_dim(i_w, k_w, s_w);
+    return i_n * i_c * o_w * k_w * (o_h * k_h - i_h);
+}
+
+/* Direct convolution, Section 3.1 and Fig. 1(a): each output element is the
+ * dot product of K with the sub-matrix of I whose top-left corner is
+ * (y*s_h, x*s_w):
+ *   O[n,y,x,m] = sum_{a<k_h} sum_{b<k_w} sum_{c<i_c}
+ *                I[n, y*s_h + a, x*s_w + b, c] * K[a, b, c, m].
+ * O is written in fp64, n-h-w-c. */
+void oracle_conv2d_direct(const void* I, const void* K, double* O,
+                          int64_t i_n, int64_t i_h, int64_t i_w, int64_t i_c,
+                          int64_t k_h, int64_t k_w, int64_t k_c,
+                          int64_t s_h, int64_t s_w, int dtype)
+{
+    int64_t o_h = oracle_out_dim(i_h, k_h, s_h);
+    int64_t o_w = oracle_out_dim(i_w, k_w, s_w);
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t n = 0; n < i_n; ++n)
+        for (int64_t y = 0; y < o_h; ++y)
+            for (int64_t x = 0; x < o_w; ++x)
+                for (int64_t m = 0; m < k_c; ++m) {
+                    double acc = 0.0;
+                    for (int64_t a = 0; a < k_h; ++a)
+                        for (int64_t b = 0; b < k_w; ++b)
+                            for (int64_t c = 0; c < i_c; ++c) {
+                                int64_t ii = ((n * i_h + (y * s_h + a)) * i_w + (x * s_w + b)) * i_c + c;
+                                int64_t kk = ((a * k_w + b) * i_c + c) * k_c + m;
+                                acc += elem(I, ii, dtype) * elem(K, kk, dtype);
+                            }
+                    O[((n * o_h + y) * o_w + x) * k_c + m] = acc;
+                }
+}
+
+/* The same definition evaluated at chosen output positions only, for
+ * sampled checks of outputs too large to compute whole. idx holds npts
+ * rows of (n, y, x, m); out[p] receives O[n,y,x,m] in fp64. */
+void oracle_conv2d_points(const void* I, const void* K, const int64_t* idx, int64_t npts,
+                          double* out,
+                          int64_t i_n, int64_t i_h, int64_t i_w, int64_t i_c,
+                          int64_t k_h, int64_t k_w, int64_t k_c,
+                          int64_t s_h, int64_t s_w, int dtype)
+{
+    (void)i_n;
+#pragma omp parallel for schedule(static)
+    for (int64_t p = 0; p < npts; ++p) {
+        int64_t n = idx[4 * p + 0], y = idx[4 * p + 1], x = idx[4 * p + 2], m = idx[4 * p + 3];
+        double acc = 0.0;
+        for (int64_t a = 0; a < k_h; ++a)
+            for (int64_t b = 0; b < k_w; ++b)
+                for (int64_t c = 0; c < i_c; ++c) {
+                    int64_t ii = ((n * i_h + (y * s_h + a)) * i_w + (x * s_w + b)) * i_c + c;
+                    int64_t kk = ((a * k_w + b) * i_c + c) * k_c + m;
+                    acc += elem(I, ii, dtype) * elem(K, kk, dtype);
+                }
+        out[p] = acc;
+    }
+}
+
+/* MEC compact lowering, Algorithm 2 (its first parallel loop): for every
+ * image n, output column w and input row h, copy the k_w*i_c contiguous
+ * elements I[n, h, s_w*w : s_w*w + k_w, 0 : i_c] into L[n, w, h, 0:k_w, 0:i_c].
+ * A pure bit copy; works for any element size. */
+void oracle_mec_lower(const void* I, void* L,
+                      int64_t i_n, int64_t i_h, int64_t i_w, int64_t i_c,
+                      int64_t k_h, int64_t k_w, int64_t k_c,
+                      int64_t s_h, int64_t s_w, int dtype)
+{
+    (void)k_h; (void)k_c; (void)s_h;
+    int64_t o_w = oracle_out_dim(i_w, k_w, s_w);
+    int64_t es = elem_bytes(dtype);
+    int64_t run = k_w * i_c; /* elements copied per (n, w, h) */
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t n = 0; n < i_n; ++n)
+        for (int64_t w = 0; w < o_w; ++w)
+            for (int64_t h = 0; h < i_h; ++h) {
+                int64_t dst = (((n * o_w + w) * i_h + h) * k_w) * i_c;  /* L[n, w, h, 0, 0] */
+                int64_t src = ((n * i_h + h) * i_w + s_w * w) * i_c;    /* I[n, h, s_w*w, 0] */
+                memcpy((char*)L + dst * es, (const char*)I + src * es, (size_t)(run * es));
+            }
+}
+
+/* Algorithm 1 (VanillaMEC), the single-image, single-channel case
+ * i_n = i_c = k_c = 1. L is o_w x i_h x k_w; then output row h is
+ * L[0:o_w, s_h*k_w*h : s_h*k_w*h + k_h*k_w] times K viewed as a
+ * (k_h*k_w) x 1 matrix, the sub-matrix taken with leading dimension i_h*k_w.
+ * I is i_h x i_w fp32, K is k_h x k_w fp32, O is o_h x o_w fp64;
+ * Lout (o_w*i_h*k_w fp32) receives the lowered matrix. */
+void oracle_vanilla_mec(const float* I, const float* K, double* O, float* Lout,
+                        int64_t i_h, int64_t i_w, int64_t k_h, int64_t k_w,
+                        int64_t s_h, int64_t s_w)
+{
+    int64_t o_h = oracle_out_dim(i_h, k_h, s_h);
+    int64_t o_w = oracle_out_dim(i_w, k_w, s_w);
+    /* lowering: L[w, h, 0:k_w] = I[h, s_w*w : s_w*w + k_w] */
+    for (int64_t w = 0; w < o_w; ++w)
+        for (int64_t h = 0; h < i_h; ++h)
+            for (int64_t b = 0; b < k_w; ++b)
+                Lout[(w * i_h + h) * k_w + b] = I[h * i_w + s_w * w + b];
+    /* o_h small matrix products over shifted column windows of L */
+    int64_t ld = i_h * k_w;
+    for (int64_t h = 0; h < o_h; ++h)
+        for (int64_t w = 0; w < o_w; ++w) {
+            double acc = 0.0;
+            for (int64_t j = 0; j < k_h * k_w; ++j)
+                acc += (double)Lout[w * ld + s_h * k_w * h + j] * (double)K[j];
+            O[h * o_w + w] = acc;
+        }
+}
+
+/* MEC's matrix-multiplication phase on an already lowered L (Algorithm 2,
+ * from the point where K is viewed as a (k_h*k_w*i_c) x k_c matrix).
+ * Let R = k_w*i_c, KD = k_h*R and LD = i_h*R (one row of L viewed as an
+ * (i_n*o_w) x (i_h*k_w*i_c) matrix). The sub-matrix for output row h
+ * starts at column s_h*R*h and is KD wide.
+ *
+ * solution 'A': o_h products over all i_n*o_w rows at once, giving O in
+ *   h-n-w-c order; then the n-h-w-c order is recovered by copying the
+ *   intermediate out and writing O[n,h,:] = tmp[h,n,:]. The paper reuses
+ *   the storage of L for that intermediate; a separate fp64 buffer is used
+ *   here, which changes no value.
+ * solution 'B': i_n*o_h products, one per image and output row, each over
+ *   o_w rows, giving n-h-w-c directly.
+ * O receives fp64 n-h-w-c. Returns 0, or -1 if the scratch allocation fails
+ * or solution is neither 'A' nor 'B'. */
+int oracle_mec_gemm(const void* L, const void* K, double* O,
+                    int64_t i_n, int64_t i_h, int64_t i_w, int64_t i_c,
+                    int64_t k_h, int64_t k_w, int64_t k_c,
+                    int64_t s_h, int64_t s_w, int dtype, int solution)
+{
+    int64_t o_h = oracle_out_dim(i_h, k_h, s_h);
+    int64_t o_w = oracle_out_dim(i_w, k_w, s_w);
+    int64_t R = k_w * i_c, KD = k_h * R, LD = i_h * R;
+
+    if (solution == 'A') {
+        int64_t rows = i_n * o_w; /* the (i_n*o_w) x KD sub-matrix */
+        double* tmp = (double*)malloc((size_t)(o_h * rows * k_c) * sizeof(double));
+        if (!tmp) return -1;
+        /* O viewed as o_h x (i_n*o_w*k_c): row h = L[0:rows, s_h*R*h : +KD] x K */
+#pragma omp parallel for schedule(static)
+        for (int64_t h = 0; h < o_h; ++h)
+            for (int64_t r = 0; r < rows; ++r)
+                for (int64_t m = 0; m < k_c; ++m) {
+                    double acc = 0.0;
+                    for (int64_t j = 0; j < KD; ++j)
+                        acc += elem(L, r * LD + s_h * R * h + j, dtype) * elem(K, j * k_c + m, dtype);
+                    tmp[(h * rows + r) * k_c + m] = acc;
+                }
+        /* h-n-w-c to n-h-w-c: O[n, h, 0:o_w*k_c] = tmp[h, n, 0:o_w*k_c] */
+        int64_t chunk = o_w * k_c;
+#pragma omp parallel for collapse(2) schedule(static)
+        for (int64_t n = 0; n < i_n; ++n)
+            for (int64_t h = 0; h < o_h; ++h)
+                memcpy(O + (n * o_h + h) * chunk, tmp + (h * i_n + n) * chunk,
+                       (size_t)chunk * sizeof(double));
+        free(tmp);
+        return 0;
+    }
+    if (solution == 'B') {
+        /* L viewed as i_n matrices of o_w x LD; O as i_n matrices of o_h x (o_w*k_c) */
+#pragma omp parallel for collapse(2) schedule(static)
+        for (int64_t n = 0; n < i_n; ++n)
+            for (int64_t h = 0; h < o_h; ++h)
+                for (int64_t w = 0; w < o_w; ++w)
+                    for (int64_t m = 0; m < k_c; ++m) {
+                        double acc = 0.0;
+                        for (int64_t j = 0; j < KD; ++j)
+                            acc += elem(L, (n * o_w + w) * LD + s_h * R * h + j, dtype) *
+                                   elem(K, j * k_c + m, dtype);
+                        O[((n * o_h + h) * o_w + w) * k_c + m] = acc;
+                    }
+        return 0;
+    }
+    return -1;
+}
+
+/* The whole of Algorithm 2: allocate L, lower, then take Solution A when
+ * o_w <= T and |O| <= |L|, else Solution B. O receives fp64 n-h-w-c.
+ * Returns 0, or -1 on allocation failure. */
+int oracle_mec_conv2d(const void* I, const void* K, double* O,
+                      int64_t i_n, int64_t i_h, int64_t i_w, int64_t i_c,
+                      int64_t k_h, int64_t k_w, int64_t k_c,
+                      int64_t s_h, int64_t s_w, int dtype, int64_t T)
+{
+    int64_t o_h = oracle_out_dim(i_h, k_h, s_h);
+    int64_t o_w = oracle_out_dim(i_w, k_w, s_w);
+    int64_t nL = oracle_lowered_elems(i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w);
+    int64_t nO = i_n * o_h * o_w * k_c;
+    void* L = malloc((size_t)(nL * elem_bytes(dtype)));
+    if (!L) return -1;
+    oracle_mec_lower(I, L, i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w, dtype);
+    int sol = (o_w <= T && nO <= nL) ? 'A' : 'B';
+    int rc = oracle_mec_gemm(L, K, O, i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w, dtype, sol);
+    free(L);
+    return rc;
+}
+
+/* im2col lowering of Section 3.1 / Fig. 1(b), the comparison point for
+ * MEC's memory saving: row (n, y, x) of the (i_n*o_h*o_w) x (k_h*k_w*i_c)
+ * matrix holds the sub-matrix I[n, y*s_h : y*s_h + k_h, x*s_w : x*s_w + k_w,
+ * 0:i_c] linearised in (a, b, c) order. A bit copy. */
+void oracle_im2col(const void* I, void* M,
+                   int64_t i_n, int64_t i_h, int64_t i_w, int64_t i_c,
+                   int64_t k_h, int64_t k_w, int64_t k_c,
+                   int64_t s_h, int64_t s_w, int dtype)
+{
+    (void)k_c;
+    int64_t o_h = oracle_out_dim(i_h, k_h, s_h);
+    int64_t o_w = oracle_out_dim(i_w, k_w, s_w);
+    int64_t es = elem_bytes(dtype);
+    int64_t cols = k_h * k_w * i_c;
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t n = 0; n < i_n; ++n)
+        for (int64_t y = 0; y < o_h; ++y)
+            for (int64_t x = 0; x < o_w; ++x)
+                for (int64_t a = 0; a < k_h; ++a)
+                    for (int64_t b = 0; b < k_w; ++b)
+                        for (int64_t c = 0; c < i_c; ++c) {
+                            int64_t dst = ((n * o_h + y) * o_w + x) * cols + (a * k_w + b) * i_c + c;
+                            int64_t src = ((n * i_h + (y * s_h + a)) * i_w + (x * s_w + b)) * i_c + c;
+                            memcpy((char*)M + dst * es, (const char*)I + src * es, (size_t)es);
+                        }
+}
+
+/* Number of OpenMP threads a parallel region here would use (0 when built
+ * without OpenMP), for reporting the core count of timed runs. */
+#ifdef _OPENMP
+#include <omp.h>
+int oracle_num_threads(void) { return omp_get_max_threads(); }
+#else
+int oracle_num_threads(void) { return 0; }
+#endif

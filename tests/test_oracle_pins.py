@@ -1,0 +1,392 @@
+"""Pins for the CPU oracle: checks against what the paper and mathematics fix.
+
+None of these re-types the oracle's own formula. Each compares it with
+something independent: values the paper prints (tests/golden), hand-derived
+closed forms of a worked example, an independently written pure-Python brute
+force, a library routine a special case reduces to (torch's conv2d in fp64,
+numpy matmul), or an invariant (delta kernels, linearity, multiplicities).
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from conftest import GOLDEN
+from paper_1706_06873_amd import workloads
+
+F32 = np.float32
+
+
+def golden(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def rand_case(rng, i_n, i_h, i_w, i_c, k_h, k_w, k_c, ints=False):
+    if ints:
+        I = rng.integers(-3, 4, size=(i_n, i_h, i_w, i_c)).astype(F32)
+        K = rng.integers(-3, 4, size=(k_h, k_w, i_c, k_c)).astype(F32)
+    else:
+        I = rng.uniform(-1, 1, size=(i_n, i_h, i_w, i_c)).astype(F32)
+        K = rng.uniform(-1, 1, size=(k_h, k_w, i_c, k_c)).astype(F32)
+    return I, K
+
+
+def torch_conv_f64(I, K, s_h, s_w):
+    """torch's CPU conv2d in fp64 (NCHW / OIHW), returned n-h-w-c."""
+    x = torch.from_numpy(I.astype(np.float64)).permute(0, 3, 1, 2)
+    w = torch.from_numpy(K.astype(np.float64)).permute(3, 2, 0, 1)
+    y = torch.nn.functional.conv2d(x, w, stride=(s_h, s_w))
+    return y.permute(0, 2, 3, 1).contiguous().numpy()
+
+
+# ---------------------------------------------------------------- worked example
+
+def fig_example_input():
+    h = np.arange(7).reshape(7, 1)
+    w = np.arange(7).reshape(1, 7)
+    return (7 * h + w).astype(F32)  # I[h, w] = 7h + w
+
+
+def test_example_dimensions_match_paper(orc):
+    g = golden("fig1_fig2_example.json")
+    I = fig_example_input().reshape(1, 7, 7, 1)
+    K = np.ones((3, 3, 1, 1), F32)
+    O = orc.conv2d_direct(I, K, 1, 1)
+    assert O.shape[1:3] == (g["o_h"], g["o_w"])
+    dims = (1, 7, 7, 1, 3, 3, 1, 1, 1)
+    L = orc.mec_lower(I, 3, 3, 1, 1, 1)
+    # MEC's L viewed as o_w x (i_h*k_w*i_c) is the 5 x 21 matrix of Fig. 2
+    assert L.reshape(L.shape[0] * L.shape[1], -1).shape == tuple(g["mec_L_shape"])
+    assert orc.lowered_elems(*dims) == g["mec_L_shape"][0] * g["mec_L_shape"][1]
+    M = orc.im2col(I, 3, 3, 1, 1)
+    assert M.shape == tuple(g["im2col_shape"])
+    assert orc.im2col_elems(*dims) == g["im2col_shape"][0] * g["im2col_shape"][1]
+    assert g["ld"] == 7 * 3  # ld = i_h * k_w
+
+
+def test_example_lowered_matrix_closed_form(orc):
+    """L[w, 3h + b] = I[h, w + b] = 7h + w + b (hand-derived from the lowering)."""
+    I = fig_example_input().reshape(1, 7, 7, 1)
+    L = orc.mec_lower(I, 3, 3, 1, 1, 1).reshape(5, 21)
+    for w in range(5):
+        for h in range(7):
+            for b in range(3):
+                assert L[w, 3 * h + b] == 7 * h + w + b
+    assert L[0].tolist()[:6] == [0, 1, 2, 7, 8, 9]
+    assert L[0].tolist()[-3:] == [42, 43, 44]
+    assert L[4].tolist()[-3:] == [46, 47, 48]
+    assert int(L.sum()) == 2520
+    # each horizontal partition (A, B, ...) is the 7 x 3 window I[0:7, w:w+3]
+    g = golden("fig1_fig2_example.json")
+    Iv = fig_example_input()
+    for w in range(g["horizontal_partitions"]):
+        assert np.array_equal(L[w].reshape(g["horizontal_partition_shape"]), Iv[:, w:w + 3])
+
+
+def test_example_outputs_closed_form_and_no_flip(orc):
+    I = fig_example_input().reshape(1, 7, 7, 1)
+    y = np.arange(5).reshape(5, 1)
+    x = np.arange(5).reshape(1, 5)
+    base = 7 * y + x
+    # all-ones kernel: O[y, x] = 9(7y + x) + 72
+    O1 = orc.conv2d_direct(I, np.ones((3, 3, 1, 1), F32), 1, 1)[0, :, :, 0]
+    assert np.array_equal(O1, 9 * base + 72)
+    assert O1[0].tolist() == [72, 81, 90, 99, 108] and O1[4, 4] == 360
+    # asymmetric kernel K[a, b] = 3a + b + 1: O = 45(7y + x) + 492;
+    # a flipped kernel would give 45(7y + x) + 228 instead
+    a = np.arange(3).reshape(3, 1)
+    b = np.arange(3).reshape(1, 3)
+    Ka = (3 * a + b + 1).astype(F32)
+    O2 = orc.conv2d_direct(I, Ka.reshape(3, 3, 1, 1), 1, 1)[0, :, :, 0]
+    assert np.array_equal(O2, 45 * base + 492)
+    assert O2[0].tolist() == [492, 537, 582, 627, 672] and O2[4, 4] == 1932
+    assert not np.array_equal(O2, 45 * base + 228)
+
+
+def test_example_vertical_partitions(orc):
+    """Algorithm 1: O row h = L[0:5, 3h : 3h + 9] x vec(K); P and Q shift by s_h*k_w = 3."""
+    g = golden("fig1_fig2_example.json")
+    I = fig_example_input()
+    a = np.arange(3).reshape(3, 1)
+    b = np.arange(3).reshape(1, 3)
+    Ka = (3 * a + b + 1).astype(F32)
+    O, L = orc.vanilla_mec(I, Ka, 1, 1)
+    assert L.shape == tuple(g["mec_L_shape"])
+    P = L[:, g["P_cols"][0]:g["P_cols"][1]]
+    Q = L[:, g["Q_cols"][0]:g["Q_cols"][1]]
+    assert P.shape == Q.shape == tuple(g["vertical_partition_shape"])
+    shift = g["vertical_partition_shift"]
+    assert np.array_equal(Q[:, :9 - shift], P[:, shift:])
+    kvec = Ka.reshape(-1).astype(np.float64)
+    assert np.array_equal(O[0], P.astype(np.float64) @ kvec)
+    assert np.array_equal(O[1], Q.astype(np.float64) @ kvec)
+    y = np.arange(5).reshape(5, 1)
+    x = np.arange(5).reshape(1, 5)
+    assert np.array_equal(O, 45 * (7 * y + x) + 492)
+
+
+# ---------------------------------------------------------------- brute force
+
+TINY_SHAPES = [
+    # i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w
+    (1, 5, 5, 1, 3, 3, 1, 1, 1),
+    (2, 7, 6, 2, 3, 2, 3, 2, 1),
+    (1, 9, 8, 3, 4, 3, 2, 3, 2),   # (i - k) not divisible by s
+    (2, 6, 9, 1, 2, 4, 2, 1, 3),
+    (1, 4, 4, 3, 4, 4, 2, 1, 1),   # kernel covers the whole input
+    (1, 8, 7, 2, 1, 1, 3, 2, 2),   # 1x1 kernel with stride
+    (2, 9, 9, 3, 3, 3, 3, 3, 3),   # s == k: no overlap
+    (1, 9, 9, 2, 2, 2, 1, 3, 3),   # s > k: gaps between windows
+]
+
+
+@pytest.mark.parametrize("shape", TINY_SHAPES)
+def test_brute_force_integers_exact(orc, shape):
+    i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w = shape
+    rng = np.random.default_rng(sum(shape))
+    I, K = rand_case(rng, i_n, i_h, i_w, i_c, k_h, k_w, k_c, ints=True)
+    Ib = I.astype(int).tolist()
+    Kb = K.astype(int).tolist()
+    Ob = np.array(orc.brute.conv2d(Ib, Kb, s_h, s_w), dtype=np.float64)
+    assert np.array_equal(orc.conv2d_direct(I, K, s_h, s_w), Ob)
+    Lb = np.array(orc.brute.mec_lower(Ib, k_w, s_w), dtype=F32)
+    L = orc.mec_lower(I, k_h, k_w, k_c, s_h, s_w)
+    assert L.shape == Lb.shape and np.array_equal(L, Lb)
+    for sol in "AB":
+        assert np.array_equal(orc.mec_gemm(L, K, i_h, i_w, s_h, s_w, sol), Ob)
+    for T in (0, 10 ** 6):
+        assert np.array_equal(orc.mec_conv2d(I, K, s_h, s_w, T=T), Ob)
+
+
+@pytest.mark.parametrize("shape", TINY_SHAPES[:4])
+def test_brute_force_floats(orc, shape):
+    i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w = shape
+    rng = np.random.default_rng(1000 + sum(shape))
+    I, K = rand_case(rng, i_n, i_h, i_w, i_c, k_h, k_w, k_c)
+    Ob = np.array(orc.brute.conv2d(I.astype(float).tolist(), K.astype(float).tolist(), s_h, s_w))
+    np.testing.assert_allclose(orc.conv2d_direct(I, K, s_h, s_w), Ob, rtol=0, atol=1e-12)
+
+
+# ---------------------------------------------------------------- invariants
+
+@pytest.mark.parametrize("s", [(1, 1), (2, 3), (3, 1)])
+@pytest.mark.parametrize("kk", [(1, 1), (3, 3), (2, 4)])
+def test_delta_kernel_reproduces_shifted_input(orc, s, kk):
+    """A delta at (a0, b0) mapping channel c to c gives
+    O[n, y, x, c] = I[n, y*s_h + a0, x*s_w + b0, c] bit for bit."""
+    s_h, s_w = s
+    k_h, k_w = kk
+    rng = np.random.default_rng(7)
+    i_n, i_h, i_w, i_c = 2, 11, 10, 3
+    I = rng.uniform(-1, 1, size=(i_n, i_h, i_w, i_c)).astype(F32)
+    for a0 in range(k_h):
+        for b0 in range(k_w):
+            K = np.zeros((k_h, k_w, i_c, i_c), F32)
+            for c in range(i_c):
+                K[a0, b0, c, c] = 1
+            O = orc.conv2d_direct(I, K, s_h, s_w)
+            o_h = (i_h - k_h) // s_h + 1
+            o_w = (i_w - k_w) // s_w + 1
+            ref = I[:, a0:a0 + s_h * (o_h - 1) + 1:s_h, b0:b0 + s_w * (o_w - 1) + 1:s_w, :]
+            assert O.shape == ref.shape
+            assert np.array_equal(O, ref.astype(np.float64))
+
+
+def test_identity_1x1(orc):
+    rng = np.random.default_rng(3)
+    I = rng.uniform(-1, 1, size=(2, 6, 5, 4)).astype(F32)
+    K = np.eye(4, dtype=F32).reshape(1, 1, 4, 4)
+    O = orc.conv2d_direct(I, K, 1, 1)
+    assert np.array_equal(O, I.astype(np.float64))
+
+
+def test_linearity(orc):
+    rng = np.random.default_rng(11)
+    shape = (2, 9, 8, 3, 3, 2, 4)
+    I1, K1 = rand_case(rng, *shape)
+    I2, K2 = rand_case(rng, *shape)
+    al, be = F32(0.75), F32(-1.5)
+    lhs = orc.conv2d_direct((al * I1 + be * I2).astype(F32), K1, 2, 1)
+    rhs = float(al) * orc.conv2d_direct(I1, K1, 2, 1) + float(be) * orc.conv2d_direct(I2, K1, 2, 1)
+    np.testing.assert_allclose(lhs, rhs, rtol=0, atol=1e-5)
+    lhs = orc.conv2d_direct(I1, (al * K1 + be * K2).astype(F32), 2, 1)
+    rhs = float(al) * orc.conv2d_direct(I1, K1, 2, 1) + float(be) * orc.conv2d_direct(I1, K2, 2, 1)
+    np.testing.assert_allclose(lhs, rhs, rtol=0, atol=1e-5)
+
+
+def test_lowered_multiplicity_sum(orc):
+    """Each I[n, h, x, c] appears in L once for every (w, b) with s_w*w + b = x."""
+    rng = np.random.default_rng(5)
+    for (i_w, k_w, s_w) in [(9, 3, 1), (11, 4, 2), (10, 2, 3), (13, 5, 4)]:
+        I = rng.integers(-50, 50, size=(2, 4, i_w, 3)).astype(F32)
+        L = orc.mec_lower(I, 1, k_w, 1, 1, s_w)
+        o_w = (i_w - k_w) // s_w + 1
+        mult = np.zeros(i_w)
+        for w in range(o_w):
+            for b in range(k_w):
+                mult[s_w * w + b] += 1
+        expect = (I.astype(np.float64) * mult.reshape(1, 1, i_w, 1)).sum()
+        assert L.astype(np.float64).sum() == expect
+        assert L.size == mult.sum() * I.shape[0] * I.shape[1] * I.shape[3]
+
+
+# ---------------------------------------------------------------- library routines
+
+TORCH_SHAPES = [
+    (2, 12, 10, 3, 3, 3, 5, 1, 1),
+    (1, 15, 17, 4, 5, 3, 6, 2, 3),
+    (3, 20, 20, 8, 7, 7, 4, 2, 2),
+    (1, 27, 27, 3, 11, 11, 8, 4, 4),
+    (2, 10, 9, 16, 3, 3, 16, 1, 1),
+]
+
+
+@pytest.mark.parametrize("shape", TORCH_SHAPES)
+def test_against_torch_conv2d_f64(orc, shape):
+    i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w = shape
+    rng = np.random.default_rng(sum(shape) * 3)
+    I, K = rand_case(rng, i_n, i_h, i_w, i_c, k_h, k_w, k_c)
+    ref = torch_conv_f64(I, K, s_h, s_w)
+    np.testing.assert_allclose(orc.conv2d_direct(I, K, s_h, s_w), ref, rtol=0, atol=1e-12)
+    L = orc.mec_lower(I, k_h, k_w, k_c, s_h, s_w)
+    for sol in "AB":
+        np.testing.assert_allclose(orc.mec_gemm(L, K, i_h, i_w, s_h, s_w, sol), ref,
+                                   rtol=0, atol=1e-12)
+
+
+def test_1x1_reduces_to_matmul(orc):
+    rng = np.random.default_rng(9)
+    I, K = rand_case(rng, 3, 5, 7, 6, 1, 1, 4)
+    ref = I.reshape(-1, 6).astype(np.float64) @ K.reshape(6, 4).astype(np.float64)
+    O = orc.conv2d_direct(I, K, 1, 1)
+    np.testing.assert_allclose(O.reshape(-1, 4), ref, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("shape", TORCH_SHAPES[:3])
+def test_mec_equals_im2col(orc, shape):
+    """Slab row (n, w) of output row h is im2col row (n, h, w): same products."""
+    i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w = shape
+    rng = np.random.default_rng(sum(shape) * 5)
+    I, K = rand_case(rng, i_n, i_h, i_w, i_c, k_h, k_w, k_c)
+    M = orc.im2col(I, k_h, k_w, s_h, s_w).astype(np.float64)
+    ref = M @ K.reshape(-1, k_c).astype(np.float64)
+    O = orc.mec_conv2d(I, K, s_h, s_w)
+    np.testing.assert_allclose(O.reshape(-1, k_c), ref, rtol=0, atol=1e-12)
+    # explicit slab view: L as (i_n*o_w) x (i_h*k_w*i_c), columns s_h*k_w*i_c*h : +k_h*k_w*i_c
+    L = orc.mec_lower(I, k_h, k_w, k_c, s_h, s_w)
+    o_h, o_w = O.shape[1:3]
+    Lm = L.reshape(i_n * o_w, i_h * k_w * i_c).astype(np.float64)
+    R = k_w * i_c
+    for h in range(o_h):
+        slab = Lm[:, s_h * R * h: s_h * R * h + k_h * R]
+        rows = M.reshape(i_n, o_h, o_w, -1)[:, h].reshape(i_n * o_w, -1)
+        assert np.array_equal(slab, rows)
+
+
+def test_bf16_inputs_widen_exactly(orc):
+    rng = np.random.default_rng(21)
+    I, K = rand_case(rng, 2, 9, 9, 8, 3, 3, 5)
+    Ib = torch.from_numpy(I).to(torch.bfloat16)
+    Kb = torch.from_numpy(K).to(torch.bfloat16)
+    Ia, Ka = workloads.to_oracle_array(Ib), workloads.to_oracle_array(Kb)
+    assert Ia.dtype == np.uint16
+    ref = torch_conv_f64(Ib.to(torch.float64).numpy(), Kb.to(torch.float64).numpy(), 1, 2)
+    np.testing.assert_allclose(orc.conv2d_direct(Ia, Ka, 1, 2), ref, rtol=0, atol=1e-12)
+    L = orc.mec_lower(Ia, 3, 3, 5, 1, 2)
+    Lf = orc.mec_lower(Ib.to(torch.float32).numpy(), 3, 3, 5, 1, 2)
+    assert np.array_equal(torch.from_numpy(L.view(np.int16)).view(torch.bfloat16).float().numpy(), Lf)
+
+
+def test_points_match_full(orc):
+    rng = np.random.default_rng(4)
+    I, K = rand_case(rng, 2, 13, 11, 3, 3, 4, 5)
+    O = orc.conv2d_direct(I, K, 2, 3)
+    idx = np.stack([rng.integers(0, d, 40) for d in O.shape], axis=1)
+    vals = orc.conv2d_points(I, K, 2, 3, idx)
+    assert np.array_equal(vals, O[tuple(idx.T)])
+
+
+def test_vanilla_is_algorithm2_special_case(orc):
+    rng = np.random.default_rng(8)
+    I = rng.uniform(-1, 1, size=(11, 9)).astype(F32)
+    K = rng.uniform(-1, 1, size=(4, 3)).astype(F32)
+    for s in [(1, 1), (2, 3), (3, 2)]:
+        O1, L1 = orc.vanilla_mec(I, K, *s)
+        O2 = orc.mec_conv2d(I.reshape(1, 11, 9, 1), K.reshape(4, 3, 1, 1), *s)
+        np.testing.assert_allclose(O1, O2[0, :, :, 0], rtol=0, atol=1e-12)
+        L2 = orc.mec_lower(I.reshape(1, 11, 9, 1), 4, 3, 1, *s)
+        assert np.array_equal(L1.reshape(-1), L2.reshape(-1))
+
+
+# ---------------------------------------------------------------- closed forms
+
+def test_lowered_sizes_against_arrays_and_eq4(orc):
+    for shape in TINY_SHAPES + TORCH_SHAPES:
+        i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w = shape
+        I = np.zeros((i_n, i_h, i_w, i_c), F32)
+        nL = orc.mec_lower(I, k_h, k_w, k_c, s_h, s_w).size
+        nM = orc.im2col(I, k_h, k_w, s_h, s_w).size
+        assert orc.lowered_elems(*shape) == nL
+        assert orc.im2col_elems(*shape) == nM
+        # Eq. (4): R is im2col's size minus MEC's
+        assert orc.saving_R(*shape) == nM - nL
+        # Eq. (4), last form, holds when s_h divides i_h - k_h; MEC saves iff k_h > s_h
+        o_w = (i_w - k_w) // s_w + 1
+        if (i_h - k_h) % s_h == 0:
+            last = i_n * i_c * o_w * k_w * (i_h - k_h) * (k_h / s_h - 1)
+            assert math.isclose(orc.saving_R(*shape), last, abs_tol=1e-9)
+            if i_h > k_h:
+                assert (nM > nL) == (k_h > s_h)
+
+
+def test_table3_memory_cells(orc):
+    """Table 3's MEM columns reproduce from the closed forms (MiB, fp32, batch 1,
+    times the layer weight). The MEC cell of cv9 is printed 6.7 where the closed
+    form gives 6.645: the one cell off, by under 0.06."""
+    t2 = golden("table2_benchmarks.json")["layers"]
+    t3 = golden("table3_resnet101_mem.json")
+    off = []
+    for row in t3["rows"]:
+        i_h, i_w, i_c, k_h, k_w, k_c, s = t2[row["name"]]
+        dims = (1, i_h, i_w, i_c, k_h, k_w, k_c, s, s)
+        conv = orc.im2col_elems(*dims) * 4 * row["weight"] / 2 ** 20
+        mec = orc.lowered_elems(*dims) * 4 * row["weight"] / 2 ** 20
+        for got, printed, what in ((conv, row["conv_mem"], "conv"), (mec, row["mec_mem"], "mec")):
+            if abs(got - printed) > 0.05 + 1e-9:
+                off.append((row["name"], what, got, printed))
+    assert len(off) == 1 and off[0][:2] == ("cv9", "mec") and abs(off[0][2] - off[0][3]) < 0.06
+    # the SUM row adds the printed cells, and RATIO divides them
+    assert math.isclose(sum(r["conv_mem"] for r in t3["rows"]), t3["sum"]["conv_mem"], abs_tol=1e-9)
+    assert math.isclose(sum(r["mec_mem"] for r in t3["rows"]), t3["sum"]["mec_mem"], abs_tol=1e-9)
+    assert round(t3["sum"]["conv_mem"] / t3["sum"]["mec_mem"], 1) == t3["ratio"]["conv_mem"]
+
+
+def test_eq1_floor_reading_pinned_by_table3(orc):
+    """cv4 (224, k 7, s 2) has a non-integer (i - k)/s; only the floor reading
+    (o = 109) reproduces Table 3's 142.1 / 41.7."""
+    assert orc.out_dim(224, 7, 2) == 109
+    ceil_o = 110
+    im2col_ceil = ceil_o * ceil_o * 7 * 7 * 64 * 4 / 2 ** 20
+    assert abs(im2col_ceil - 142.1) > 2
+    dims = (1, 224, 224, 64, 7, 7, 64, 2, 2)
+    assert round(orc.im2col_elems(*dims) * 4 / 2 ** 20, 1) == 142.1
+    assert round(orc.lowered_elems(*dims) * 4 / 2 ** 20, 1) == 41.7
+
+
+def test_workload_sizes(orc):
+    """|L| and |im2col| of the five synthetic layers (elements)."""
+    expect = {
+        "tiny": (105, 225),
+        "resnet_mid": (19_955_712, 57_802_752),
+        "vgg_first": (7_289_856, 21_676_032),
+        "alexnet_conv1": (52_736_640, 140_553_600),
+        "deep_bf16": (88_080_384, 231_211_008),
+    }
+    for name, (nl, nm) in expect.items():
+        d = workloads.LAYERS[name].dims
+        assert orc.lowered_elems(*d) == nl
+        assert orc.im2col_elems(*d) == nm
