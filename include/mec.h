@@ -1,0 +1,147 @@
+/*
+ * mec.h -- C ABI of the MI355X (gfx950) library for MEC, the memory-efficient
+ * convolution of Cho & Brand, "MEC: Memory-efficient Convolution for Deep
+ * Neural Network" (ICML 2017).
+ *
+ * The operation is the 2-D convolution O = I * K with strides s_h, s_w of
+ * Section 2.1, on an input that the caller has already padded:
+ *
+ *   O[n, y, x, m] = sum_{a < k_h} sum_{b < k_w} sum_{c < i_c}
+ *                   I[n, y*s_h + a, x*s_w + b, c] * K[a, b, c, m]
+ *
+ * (cross-correlation: the kernel is not flipped). MEC computes it in two
+ * steps (Section 3.3, Algorithm 2): a compact lowering of I into L, then o_h
+ * small matrix products over overlapping column windows ("slabs") of L.
+ *
+ * Dimensions use the paper's notation (Table 1):
+ *   I  input    i_n x i_h x i_w x i_c     (n-h-w-c, row-major)
+ *   K  kernel   k_h x k_w x i_c x k_c     (h-w-i-o, row-major)
+ *   O  output   i_n x o_h x o_w x k_c     (n-h-w-c, row-major)
+ *   L  lowered  i_n x o_w x i_h x k_w x i_c
+ * with o_h = floor((i_h - k_h) / s_h) + 1 and o_w likewise (Eq. (1); the
+ * floor is this library's reading when s does not divide i - k).
+ *
+ * Conventions shared by every entry point:
+ *  - All tensor pointers are DEVICE pointers to dense row-major memory owned
+ *    by the caller. The library never allocates, frees or synchronises.
+ *  - Each pointer must be aligned to its element size (4 bytes for fp32,
+ *    2 bytes for bf16); otherwise MEC_ERR_ALIGNMENT.
+ *  - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL means
+ *    the default stream). Results are visible after the stream is
+ *    synchronised.
+ *  - Every argument is checked on the host before anything is enqueued; on
+ *    any error nothing is launched and no memory is written.
+ *  - No global state: calls are thread-safe. Calls on different streams that
+ *    write the same memory race, as with any asynchronous device work.
+ *  - Status codes are returned; negative values are errors. No C++ exception
+ *    crosses this interface.
+ */
+#ifndef MEC_H
+#define MEC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Element type of I, K and L. O is always fp32 (products are accumulated in
+ * fp32). MEC_BF16 means bfloat16 bit patterns; it is an extension: the paper
+ * works in fp32 only (Section 4). */
+enum mec_dtype { MEC_F32 = 0, MEC_BF16 = 1 };
+
+/* MEC_ALGO_LOWERED: Algorithm 2 as two kernels -- the lowering writes L into
+ *   the caller's workspace, then the slab products read it.
+ * MEC_ALGO_FUSED: one kernel forms each slab of L in on-chip memory straight
+ *   from I; L is never written to device memory and no workspace is used. */
+enum mec_algo { MEC_ALGO_LOWERED = 0, MEC_ALGO_FUSED = 1 };
+
+enum mec_status {
+    MEC_OK = 0,
+    MEC_ERR_INVALID_ARG = -1, /* a dimension or stride < 1, k > i, unknown enum,
+                                 NULL tensor pointer, or a size too large    */
+    MEC_ERR_WORKSPACE = -2,   /* workspace NULL or smaller than required      */
+    MEC_ERR_ALIGNMENT = -3,   /* a pointer not aligned to its element size    */
+    MEC_ERR_HIP = -4,         /* the HIP runtime reported a launch error      */
+    MEC_ERR_UNSUPPORTED = -5  /* valid but beyond this build's kernel limits
+                                 (k_h larger than the on-chip tile allows)    */
+};
+
+/* Output size, Eq. (1) with the floor reading: o_h = (i_h - k_h) / s_h + 1,
+ * o_w = (i_w - k_w) / s_w + 1. Writes *o_h and *o_w (either may be NULL).
+ * Returns MEC_OK, or MEC_ERR_INVALID_ARG for a size or stride < 1 or k > i. */
+int mec_output_dims(int i_h, int i_w, int k_h, int k_w, int s_h, int s_w,
+                    int* o_h, int* o_w);
+
+/* Workspace needed by mec_conv2d, in bytes.
+ * MEC_ALGO_LOWERED: exactly |L| * sizeof(element), with
+ *   |L| = i_n * o_w * i_h * k_w * i_c -- the size of the lowered tensor that
+ *   Algorithm 2 allocates (Section 3.4, Eq. (3), read with i_c where the
+ *   printed equation has k_c). No rounding up.
+ * MEC_ALGO_FUSED: 0.
+ * Returns the byte count (>= 0) or a negative status. */
+int64_t mec_workspace_bytes(int i_n, int i_h, int i_w, int i_c,
+                            int k_h, int k_w, int k_c, int s_h, int s_w,
+                            int dtype, int algo);
+
+/* Size of the im2col lowered matrix that MEC's L replaces, in bytes:
+ * (i_n*o_h*o_w) x (k_h*k_w*i_c) elements (Section 3.1, Eq. (2), i_c reading).
+ * Provided so callers can report MEC's saving; no kernel uses it.
+ * Returns the byte count (>= 0) or a negative status. */
+int64_t mec_im2col_bytes(int i_n, int i_h, int i_w, int i_c,
+                         int k_h, int k_w, int k_c, int s_h, int s_w, int dtype);
+
+/* MEC compact lowering (Section 3.3, Algorithm 2, first loop):
+ *   L[n, w, h, 0:k_w, 0:i_c] = I[n, h, s_w*w : s_w*w + k_w, 0:i_c]
+ * for all n < i_n, w < o_w, h < i_h. A bit copy in the element type `dtype`;
+ * L must hold |L| = i_n*o_w*i_h*k_w*i_c elements and must not overlap I.
+ * k_h, k_c and s_h do not change L but are validated (o_h >= 1) so every
+ * entry point takes the same shape contract.
+ * Returns MEC_OK or a negative status. */
+int mec_lower(const void* I, void* L,
+              int i_n, int i_h, int i_w, int i_c,
+              int k_h, int k_w, int k_c, int s_h, int s_w,
+              int dtype, void* stream);
+
+/* MEC's product phase on an already lowered L (Section 3.3, Algorithm 2,
+ * from viewing K as a (k_h*k_w*i_c) x k_c matrix on). For every output row
+ * h < o_h, with R = k_w*i_c:
+ *   O[n, h, w, 0:k_c] = L[n, w][s_h*R*h : s_h*R*h + k_h*R] x K
+ * where L[n, w] is row (n, w) of L viewed as an (i_n*o_w) x (i_h*R) matrix.
+ * The result is written straight in n-h-w-c order, so neither Solution A's
+ * final transposition nor the |O| <= |L| condition applies. L must hold the
+ * output of mec_lower for the same arguments. O must not overlap L or K.
+ * Returns MEC_OK or a negative status. */
+int mec_gemm(const void* L, const void* K, float* O,
+             int i_n, int i_h, int i_w, int i_c,
+             int k_h, int k_w, int k_c, int s_h, int s_w,
+             int dtype, void* stream);
+
+/* The convolution O = I * K by MEC (Algorithm 2).
+ * MEC_ALGO_LOWERED: mec_lower into `workspace`, then mec_gemm from it;
+ *   workspace_bytes must be >= mec_workspace_bytes(..., MEC_ALGO_LOWERED) and
+ *   the workspace must be aligned to the element size. On return (after the
+ *   stream completes) the workspace holds L exactly as mec_lower writes it.
+ * MEC_ALGO_FUSED: one kernel; workspace may be NULL and is not touched.
+ * O must not overlap I, K or the workspace.
+ * Returns MEC_OK or a negative status. */
+int mec_conv2d(const void* I, const void* K, float* O,
+               void* workspace, size_t workspace_bytes,
+               int i_n, int i_h, int i_w, int i_c,
+               int k_h, int k_w, int k_c, int s_h, int s_w,
+               int dtype, int algo, void* stream);
+
+/* Static, NUL-terminated description of a status code (never NULL). */
+const char* mec_strerror(int status);
+
+/* Detail of the most recent MEC_ERR_HIP returned on the calling thread: the
+ * kernel that failed to launch and the HIP error name and text. Empty string
+ * when none. The pointer is valid until the next call on the same thread. */
+const char* mec_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MEC_H */

@@ -1,0 +1,212 @@
+"""MI355X (gfx950) MEC convolution: thin Python binding of ``include/mec.h``.
+
+MEC is the memory-efficient convolution of Cho & Brand (ICML 2017): a compact
+lowering of the input I into L (i_n x o_w x i_h x k_w x i_c), then o_h small
+matrix products over overlapping slabs of L. Every step runs in the HIP kernels
+of ``libmec.so``; this module only marshals arguments. PyTorch supplies device
+memory and streams: tensors passed here must be contiguous tensors on a HIP
+device. There is no CPU fallback: if the library is missing, importing this
+package raises.
+
+Layouts (paper notation): I is i_n x i_h x i_w x i_c, K is k_h x k_w x i_c x
+k_c, O is i_n x o_h x o_w x k_c (fp32). I and K are both fp32 or both bf16.
+"""
+import ctypes
+import os
+
+# torch first: importing it loads its HIP runtime, and libmec.so then binds to
+# that same runtime. Loaded the other way round, the process would map a
+# second HIP runtime (the system one) beside torch's, and device memory and
+# streams from one are not valid in the other.
+import torch  # noqa: E402,F401
+
+__all__ = [
+    "MecError", "F32", "BF16", "LOWERED", "FUSED", "lib", "output_dims", "workspace_bytes",
+    "im2col_bytes", "lower", "gemm", "conv2d", "strerror",
+]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmec.so")
+
+F32, BF16 = 0, 1
+LOWERED, FUSED = 0, 1
+_ALGOS = {"lowered": LOWERED, "fused": FUSED, LOWERED: LOWERED, FUSED: FUSED}
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError("%s is not built; run `python paper_1706_06873_amd/build.py`" % LIB_PATH)
+
+_i = ctypes.c_int
+_vp = ctypes.c_void_p
+_DIMS = [_i] * 9
+
+
+def _load(path):
+    L = ctypes.CDLL(path)
+    L.mec_output_dims.argtypes = [_i] * 6 + [ctypes.POINTER(_i), ctypes.POINTER(_i)]
+    L.mec_output_dims.restype = _i
+    L.mec_workspace_bytes.argtypes = _DIMS + [_i, _i]
+    L.mec_workspace_bytes.restype = ctypes.c_int64
+    L.mec_im2col_bytes.argtypes = _DIMS + [_i]
+    L.mec_im2col_bytes.restype = ctypes.c_int64
+    L.mec_lower.argtypes = [_vp, _vp] + _DIMS + [_i, _vp]
+    L.mec_lower.restype = _i
+    L.mec_gemm.argtypes = [_vp, _vp, _vp] + _DIMS + [_i, _vp]
+    L.mec_gemm.restype = _i
+    L.mec_conv2d.argtypes = [_vp, _vp, _vp, _vp, ctypes.c_size_t] + _DIMS + [_i, _i, _vp]
+    L.mec_conv2d.restype = _i
+    L.mec_strerror.argtypes = [_i]
+    L.mec_strerror.restype = ctypes.c_char_p
+    L.mec_last_error.argtypes = []
+    L.mec_last_error.restype = ctypes.c_char_p
+    return L
+
+
+def _hip_runtimes():
+    """Distinct HIP runtime libraries mapped into this process."""
+    try:
+        with open("/proc/self/maps") as f:
+            paths = {line.split()[-1] for line in f if "libamdhip64" in line}
+    except OSError:
+        return []
+    return sorted(os.path.realpath(p) for p in paths)
+
+
+lib = _load(LIB_PATH)
+if len(_hip_runtimes()) > 1:
+    raise ImportError("two HIP runtimes are loaded in this process (%s): libmec.so must bind to "
+                      "the one torch uses" % ", ".join(_hip_runtimes()))
+
+
+class MecError(RuntimeError):
+    """A negative status from the library."""
+
+    def __init__(self, status, what):
+        self.status = status
+        detail = lib.mec_last_error().decode() if status == -4 else ""
+        super().__init__("%s: %s (status %d)%s" % (what, strerror(status), status,
+                                                    " -- " + detail if detail else ""))
+
+
+def strerror(status):
+    return lib.mec_strerror(status).decode()
+
+
+def _check(status, what):
+    if status < 0:
+        raise MecError(int(status), what)
+    return status
+
+
+def output_dims(i_h, i_w, k_h, k_w, s_h, s_w):
+    """(o_h, o_w) by Eq. (1), floor reading."""
+    o_h, o_w = _i(), _i()
+    _check(lib.mec_output_dims(i_h, i_w, k_h, k_w, s_h, s_w, ctypes.byref(o_h), ctypes.byref(o_w)),
+           "mec_output_dims")
+    return o_h.value, o_w.value
+
+
+def _dtype_code(t):
+    import torch
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError("I and K must be float32 or bfloat16, got %s" % t.dtype)
+
+
+def workspace_bytes(i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w, dtype=F32, algo=LOWERED):
+    return _check(lib.mec_workspace_bytes(i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w, dtype,
+                                          _ALGOS[algo]), "mec_workspace_bytes")
+
+
+def im2col_bytes(i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w, dtype=F32):
+    return _check(lib.mec_im2col_bytes(i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w, dtype),
+                  "mec_im2col_bytes")
+
+
+def _stream_handle(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dev_ptr(t, name):
+    if not t.is_cuda:
+        raise ValueError("%s must be a device tensor" % name)
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _dims(I, K, s_h, s_w):
+    if I.dim() != 4 or K.dim() != 4:
+        raise ValueError("I must be i_n x i_h x i_w x i_c and K k_h x k_w x i_c x k_c")
+    i_n, i_h, i_w, i_c = I.shape
+    k_h, k_w, k_ic, k_c = K.shape
+    if k_ic != i_c:
+        raise ValueError("K's third dimension (%d) must equal i_c (%d)" % (k_ic, i_c))
+    if I.dtype != K.dtype:
+        raise TypeError("I and K must have the same dtype")
+    return (i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w)
+
+
+def lower(I, k_h, k_w, k_c, s_h, s_w, L=None, stream=None):
+    """MEC lowering of I into L (i_n x o_w x i_h x k_w x i_c); returns L."""
+    import torch
+    i_n, i_h, i_w, i_c = I.shape
+    _, o_w = output_dims(i_h, i_w, k_h, k_w, s_h, s_w)
+    if L is None:
+        L = torch.empty((i_n, o_w, i_h, k_w, i_c), dtype=I.dtype, device=I.device)
+    if L.numel() != i_n * o_w * i_h * k_w * i_c or L.dtype != I.dtype:
+        raise ValueError("L has the wrong size or dtype")
+    _check(lib.mec_lower(_dev_ptr(I, "I"), _dev_ptr(L, "L"), i_n, i_h, i_w, i_c, k_h, k_w, k_c,
+                         s_h, s_w, _dtype_code(I), _stream_handle(stream)), "mec_lower")
+    return L
+
+
+def _out(I, K, s_h, s_w, O):
+    import torch
+    d = _dims(I, K, s_h, s_w)
+    o_h, o_w = output_dims(d[1], d[2], d[4], d[5], s_h, s_w)
+    shape = (d[0], o_h, o_w, d[6])
+    if O is None:
+        O = torch.empty(shape, dtype=torch.float32, device=I.device)
+    if tuple(O.shape) != shape or O.dtype != torch.float32:
+        raise ValueError("O must be float32 of shape %s" % (shape,))
+    return d, O
+
+
+def gemm(L, K, i_h, i_w, s_h, s_w, O=None, stream=None):
+    """MEC's slab products on a lowered L (i_n x o_w x i_h x k_w x i_c); returns O."""
+    import torch
+    i_n, o_w, _, k_w, i_c = L.shape
+    k_h, _, _, k_c = K.shape
+    o_h, o_w2 = output_dims(i_h, i_w, k_h, k_w, s_h, s_w)
+    if o_w2 != o_w:
+        raise ValueError("L's o_w does not match i_w, k_w, s_w")
+    if O is None:
+        O = torch.empty((i_n, o_h, o_w, k_c), dtype=torch.float32, device=L.device)
+    _check(lib.mec_gemm(_dev_ptr(L, "L"), _dev_ptr(K, "K"), _dev_ptr(O, "O"), i_n, i_h, i_w, i_c,
+                        k_h, k_w, k_c, s_h, s_w, _dtype_code(L), _stream_handle(stream)),
+           "mec_gemm")
+    return O
+
+
+def conv2d(I, K, s_h=1, s_w=1, algo="lowered", workspace=None, O=None, stream=None):
+    """O = I * K by MEC. With algo="lowered" a workspace of
+    workspace_bytes(...) bytes is allocated unless given (a uint8 device
+    tensor); after the call it holds L. Returns O."""
+    import torch
+    d, O = _out(I, K, s_h, s_w, O)
+    a = _ALGOS[algo]
+    ws_ptr, ws_bytes = None, 0
+    if a == LOWERED:
+        need = workspace_bytes(*d, dtype=_dtype_code(I), algo=a)
+        if workspace is None:
+            workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=I.device)
+        ws_ptr = _dev_ptr(workspace, "workspace")
+        ws_bytes = workspace.numel() * workspace.element_size()
+    _check(lib.mec_conv2d(_dev_ptr(I, "I"), _dev_ptr(K, "K"), _dev_ptr(O, "O"), ws_ptr, ws_bytes,
+                          *d, _dtype_code(I), a, _stream_handle(stream)), "mec_conv2d")
+    return O

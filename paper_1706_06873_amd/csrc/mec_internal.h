@@ -1,0 +1,104 @@
+// Internal declarations shared by the host API (mec_api.cpp) and the HIP
+// kernels (mec_lower.hip, mec_gemm.hip). Not part of the public ABI.
+#pragma once
+
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifndef MEC_HD
+#if defined(__HIPCC__)
+#define MEC_HD __host__ __device__
+#else
+#define MEC_HD
+#endif
+#endif
+
+namespace mec {
+
+// Unsigned division by a runtime constant d >= 1 for dividends below 2^31,
+// by one 64-bit multiply and a shift. With l = ceil(log2 d) and
+// m = floor(2^(31+l) / d) + 1 (which is below 2^32), floor(x*m / 2^(31+l))
+// equals floor(x / d) for every x < 2^31 (Granlund and Montgomery, "Division
+// by invariant integers using multiplication", PLDI 1994, round-up method).
+struct FastDiv {
+    uint32_t d;
+    uint32_t shift;  // 31 + l
+    uint64_t m;
+
+    FastDiv() = default;
+    explicit FastDiv(uint32_t divisor) : d(divisor) {
+        uint32_t l = 0;
+        while ((uint64_t(1) << l) < divisor) ++l;
+        shift = 31 + l;
+        m = ((uint64_t(1) << shift) / divisor) + 1;
+    }
+    MEC_HD inline uint32_t div(uint32_t x) const {
+        return (uint32_t)(((uint64_t)x * m) >> shift);
+    }
+};
+
+// Shape of one convolution in the paper's notation, plus derived sizes.
+struct Shape {
+    int64_t i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w;
+    int64_t o_h, o_w;
+    int64_t R;      // k_w * i_c: elements copied per (n, w, h) by the lowering
+    int64_t pairs;  // i_n * o_w: rows of L viewed as a matrix
+};
+
+// ---------------------------------------------------------------- lowering
+struct LowerParams {
+    const void* I;
+    void* L;
+    int64_t rows;          // i_n * o_w * i_h rows of R elements in L
+    int64_t R;             // k_w * i_c
+    int64_t i_h, o_w, i_w, i_c, s_w;
+    int32_t rows_per_block;
+    uint32_t nblocks;
+    FastDiv divR;          // division by R (elements) or by R / VEC (vectors)
+};
+
+// Enqueue the lowering. elem_bytes is 4 (fp32) or 2 (bf16). Returns a
+// hipError_t from the launch.
+hipError_t launch_lower(const Shape& s, const void* I, void* L, int elem_bytes,
+                        hipStream_t stream);
+
+// ---------------------------------------------------------------- slab products
+struct GemmParams {
+    const void* A;     // L (lowered) or I (fused)
+    const void* K;     // k_h x k_w x i_c x k_c
+    float* O;          // i_n x o_h x o_w x k_c
+    int64_t i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w, o_h, o_w;
+    int64_t R;         // k_w * i_c
+    int64_t pairs;     // i_n * o_w
+    int64_t a_xstride; // elements between rows x and x+1 of one pair's source
+    int32_t hrows;     // input rows staged per tile: (HT - 1) * s_h + k_h
+    int32_t nchunks;   // r-chunks of KT covering R
+    int32_t pair_tiles, h_tiles, n_tiles;
+    uint32_t ntiles;
+};
+
+// Enqueue the slab products. fused selects the I-sourced variant.
+// Returns hipErrorInvalidValue when the shape exceeds the kernels' on-chip
+// limits (see gemm_supported), else the launch status.
+hipError_t launch_gemm(const Shape& s, const void* A, const void* K, float* O, int dtype,
+                       bool fused, hipStream_t stream);
+
+// Whether the slab-product kernels can run this shape (LDS limits).
+bool gemm_supported(const Shape& s, int dtype);
+
+}  // namespace mec
+
+#if defined(__HIP__)
+namespace mec {
+// Block index remapped so that each of the 8 XCDs of the MI355X, which
+// receive workgroups round-robin (block b runs on XCD b % 8), processes one
+// contiguous range of logical blocks. Neighbouring tiles then share an XCD's
+// L2 cache. A bijection on [0, G).
+__device__ inline uint32_t xcd_remap(uint32_t b, uint32_t G) {
+    const uint32_t xcd = b & 7u, slot = b >> 3;
+    const uint32_t base = G >> 3, rem = G & 7u;
+    return xcd * base + (xcd < rem ? xcd : rem) + slot;
+}
+}  // namespace mec
+#endif

@@ -79,10 +79,11 @@ def _draw(gen, shape, dist):
     raise ValueError("unknown distribution %r" % dist)
 
 
-def make_inputs(layer: Layer, i_n: int = None):
+def make_inputs(layer: Layer, i_n: int = None, round_bf16: bool = True):
     """Draw (I, K) for a layer on the CPU. ``i_n`` overrides the batch size
     (the first i_n images of the full draw are NOT reproduced; a smaller batch
-    is a separate draw with the same seed)."""
+    is a separate draw with the same seed). With ``round_bf16=False`` a bf16
+    layer is returned as the fp32 values before rounding."""
     n = layer.i_n if i_n is None else i_n
     gen = torch.Generator(device="cpu")
     gen.manual_seed(layer.seed)
@@ -94,7 +95,7 @@ def make_inputs(layer: Layer, i_n: int = None):
         I[:, p:p + layer.ih_int, p:p + layer.iw_int, :] = interior
     else:
         I = interior.contiguous()
-    if layer.dtype == "bf16":
+    if layer.dtype == "bf16" and round_bf16:
         I = I.to(torch.bfloat16)
         K = K.to(torch.bfloat16)
     return I.contiguous(), K.contiguous()

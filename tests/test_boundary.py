@@ -1,0 +1,235 @@
+"""The C-ABI library on the CPU: it loads, exports every declared symbol, and
+its host-side logic (Eq. (1), workspace sizes, argument validation) is right.
+
+No test here launches a kernel: every call either is pure host arithmetic or
+fails validation before anything is enqueued (tensor pointers are fake,
+never dereferenced).
+"""
+import ctypes
+import os
+import re
+import subprocess
+import sys
+
+import numpy as np
+import pytest
+
+import paper_1706_06873_amd as mec
+from conftest import REPO
+
+HEADER = os.path.join(REPO, "include", "mec.h")
+FAKE = ctypes.c_void_p(0x100000)      # 4 KiB aligned, never dereferenced
+ODD = ctypes.c_void_p(0x100002)       # 2-byte aligned only
+NULL = ctypes.c_void_p(0)
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mec_\w+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    names = declared_functions()
+    assert len(names) >= 7
+    for name in names:
+        assert hasattr(mec.lib, name), name
+
+
+def test_single_hip_runtime_in_fresh_process():
+    """Importing the package first (before torch) still maps one HIP runtime."""
+    code = ("import paper_1706_06873_amd as m, torch; torch.cuda.is_available(); "
+            "print(len(m._hip_runtimes()))")
+    out = subprocess.run([sys.executable, "-c", code], cwd=REPO, capture_output=True, text=True)
+    assert out.returncode == 0, out.stderr
+    assert out.stdout.strip().splitlines()[-1] == "1"
+
+
+def test_status_codes_match_header():
+    text = open(HEADER).read()
+    codes = dict((k, int(v)) for k, v in re.findall(r"(MEC_\w+)\s*=\s*(-?\d+)", text))
+    assert codes["MEC_F32"] == mec.F32 and codes["MEC_BF16"] == mec.BF16
+    assert codes["MEC_ALGO_LOWERED"] == mec.LOWERED and codes["MEC_ALGO_FUSED"] == mec.FUSED
+    for name in ("MEC_OK", "MEC_ERR_INVALID_ARG", "MEC_ERR_WORKSPACE", "MEC_ERR_ALIGNMENT",
+                 "MEC_ERR_HIP", "MEC_ERR_UNSUPPORTED"):
+        msg = mec.strerror(codes[name])
+        assert msg and msg != "unknown status"
+    assert mec.strerror(12345) == "unknown status"
+
+
+SHAPES = [
+    (1, 7, 7, 1, 3, 3, 1, 1, 1),
+    (32, 58, 58, 64, 3, 3, 64, 1, 1),
+    (16, 226, 226, 3, 3, 3, 64, 1, 1),
+    (128, 227, 227, 3, 11, 11, 96, 4, 4),
+    (256, 16, 16, 512, 3, 3, 512, 1, 1),
+    (2, 9, 8, 3, 4, 3, 2, 3, 2),
+    (1, 224, 224, 64, 7, 7, 64, 2, 2),
+    (3, 10, 10, 5, 10, 10, 7, 3, 3),
+]
+
+
+@pytest.mark.parametrize("shape", SHAPES)
+def test_sizes_agree_with_oracle(orc, shape):
+    nL = orc.lowered_elems(*shape)
+    nM = orc.im2col_elems(*shape)
+    for dt, es in ((mec.F32, 4), (mec.BF16, 2)):
+        assert mec.workspace_bytes(*shape, dtype=dt, algo=mec.LOWERED) == nL * es
+        assert mec.workspace_bytes(*shape, dtype=dt, algo=mec.FUSED) == 0
+        assert mec.im2col_bytes(*shape, dtype=dt) == nM * es
+    o = mec.output_dims(shape[1], shape[2], shape[4], shape[5], shape[7], shape[8])
+    assert o == (orc.out_dim(shape[1], shape[4], shape[7]), orc.out_dim(shape[2], shape[5], shape[8]))
+
+
+def test_table3_cv4_bytes():
+    # cv4 of Table 2 at batch 1: 41.7 / 142.1 MiB in Table 3
+    dims = (1, 224, 224, 64, 7, 7, 64, 2, 2)
+    assert mec.workspace_bytes(*dims) == 43_753_472
+    assert mec.im2col_bytes(*dims) == 149_035_264
+
+
+def test_workspace_is_exact_for_tiny():
+    # no rounding: 105 fp32 elements
+    assert mec.workspace_bytes(1, 7, 7, 1, 3, 3, 1, 1, 1) == 420
+    assert mec.im2col_bytes(1, 7, 7, 1, 3, 3, 1, 1, 1) == 900
+
+
+BAD_DIMS = [
+    (0, 7, 7, 1, 3, 3, 1, 1, 1),
+    (1, 7, 7, 0, 3, 3, 1, 1, 1),
+    (1, 7, 7, 1, 8, 3, 1, 1, 1),    # k_h > i_h
+    (1, 7, 7, 1, 3, 8, 1, 1, 1),    # k_w > i_w
+    (1, 7, 7, 1, 3, 3, 0, 1, 1),
+    (1, 7, 7, 1, 3, 3, 1, 0, 1),
+    (1, 7, 7, 1, 3, 3, 1, 1, -2),
+    (1 << 20, 1 << 11, 1 << 11, 1 << 9, 3, 3, 64, 1, 1),  # too large
+]
+
+
+@pytest.mark.parametrize("dims", BAD_DIMS)
+def test_invalid_dims_rejected_everywhere(dims):
+    E = -1
+    L = mec.lib
+    assert L.mec_workspace_bytes(*dims, 0, 0) == E
+    assert L.mec_im2col_bytes(*dims, 0) == E
+    assert L.mec_lower(FAKE, FAKE, *dims, 0, NULL) == E
+    assert L.mec_gemm(FAKE, FAKE, FAKE, *dims, 0, NULL) == E
+    assert L.mec_conv2d(FAKE, FAKE, FAKE, FAKE, 1 << 40, *dims, 0, 0, NULL) == E
+    assert L.mec_conv2d(FAKE, FAKE, FAKE, NULL, 0, *dims, 0, 1, NULL) == E
+
+
+def test_output_dims_errors_and_floor():
+    o_h, o_w = ctypes.c_int(-7), ctypes.c_int(-7)
+    assert mec.lib.mec_output_dims(7, 7, 8, 3, 1, 1, ctypes.byref(o_h), ctypes.byref(o_w)) == -1
+    assert o_h.value == -7  # nothing written on error
+    assert mec.lib.mec_output_dims(7, 7, 3, 3, 0, 1, None, None) == -1
+    assert mec.lib.mec_output_dims(7, 7, 3, 3, 1, 1, None, None) == 0
+    assert mec.output_dims(224, 227, 7, 11, 2, 4) == (109, 55)
+    assert mec.output_dims(10, 10, 10, 10, 3, 3) == (1, 1)
+
+
+GOOD = (2, 9, 8, 4, 3, 3, 5, 1, 2)
+
+
+def test_bad_enums_and_null_pointers():
+    L = mec.lib
+    assert L.mec_workspace_bytes(*GOOD, 2, 0) == -1
+    assert L.mec_workspace_bytes(*GOOD, 0, 2) == -1
+    assert L.mec_im2col_bytes(*GOOD, -1) == -1
+    assert L.mec_lower(NULL, FAKE, *GOOD, 0, NULL) == -1
+    assert L.mec_lower(FAKE, NULL, *GOOD, 0, NULL) == -1
+    assert L.mec_lower(FAKE, FAKE, *GOOD, 3, NULL) == -1
+    assert L.mec_gemm(NULL, FAKE, FAKE, *GOOD, 0, NULL) == -1
+    assert L.mec_gemm(FAKE, NULL, FAKE, *GOOD, 0, NULL) == -1
+    assert L.mec_gemm(FAKE, FAKE, NULL, *GOOD, 0, NULL) == -1
+    for bad in ((NULL, FAKE, FAKE), (FAKE, NULL, FAKE), (FAKE, FAKE, NULL)):
+        assert L.mec_conv2d(*bad, FAKE, 1 << 30, *GOOD, 0, 0, NULL) == -1
+    assert L.mec_conv2d(FAKE, FAKE, FAKE, FAKE, 1 << 30, *GOOD, 0, 7, NULL) == -1
+    assert L.mec_conv2d(FAKE, FAKE, FAKE, FAKE, 1 << 30, *GOOD, 5, 0, NULL) == -1
+
+
+def test_alignment_rejected():
+    L = mec.lib
+    # fp32 needs 4-byte alignment, bf16 2-byte; O is always fp32
+    assert L.mec_lower(ODD, FAKE, *GOOD, 0, NULL) == -3
+    assert L.mec_lower(FAKE, ODD, *GOOD, 0, NULL) == -3
+    assert L.mec_gemm(FAKE, FAKE, ODD, *GOOD, 1, NULL) == -3
+    assert L.mec_gemm(ODD, FAKE, FAKE, *GOOD, 0, NULL) == -3
+    assert L.mec_conv2d(ODD, FAKE, FAKE, FAKE, 1 << 30, *GOOD, 0, 0, NULL) == -3
+    assert L.mec_conv2d(FAKE, FAKE, ODD, NULL, 0, *GOOD, 1, 1, NULL) == -3
+    assert L.mec_conv2d(FAKE, FAKE, FAKE, ODD, 1 << 30, *GOOD, 0, 0, NULL) == -3
+
+
+def test_workspace_rejected():
+    L = mec.lib
+    need = mec.workspace_bytes(*GOOD)
+    assert L.mec_conv2d(FAKE, FAKE, FAKE, NULL, need, *GOOD, 0, 0, NULL) == -2
+    assert L.mec_conv2d(FAKE, FAKE, FAKE, FAKE, need - 1, *GOOD, 0, 0, NULL) == -2
+    need16 = mec.workspace_bytes(*GOOD, dtype=mec.BF16)
+    assert need16 * 2 == need
+    assert L.mec_conv2d(FAKE, FAKE, FAKE, FAKE, need16 - 2, *GOOD, 1, 0, NULL) == -2
+
+
+def test_unsupported_kernel_height():
+    # far taller than the on-chip tile holds: refused before any launch
+    dims = (1, 300, 8, 1, 300, 3, 1, 1, 1)
+    assert mec.lib.mec_gemm(FAKE, FAKE, FAKE, *dims, 0, NULL) == -5
+    assert mec.lib.mec_conv2d(FAKE, FAKE, FAKE, NULL, 0, *dims, 0, 1, NULL) == -5
+    assert mec.workspace_bytes(*dims) == 1 * 6 * 300 * 3 * 4
+
+
+def test_python_binding_raises():
+    with pytest.raises(mec.MecError) as ei:
+        mec.workspace_bytes(1, 7, 7, 1, 8, 3, 1, 1, 1)
+    assert ei.value.status == -1
+
+
+def test_fastdiv_exhaustive_cpu(tmp_path):
+    """The kernels' division by invariant integers, checked on the host against
+    '/' for many divisors and dividends up to 2^31 - 1."""
+    src = tmp_path / "fd.cpp"
+    src.write_text(r'''
+#include <cstdio>
+#include <cstdint>
+#include <random>
+#define MEC_HD
+#include "mec_internal.h"
+int main() {
+    std::mt19937_64 rng(1);
+    uint64_t bad = 0, n = 0;
+    auto check = [&](uint32_t d, uint32_t x) {
+        mec::FastDiv f(d);
+        ++n;
+        if (f.div(x) != x / d) { if (bad < 5) printf("d=%u x=%u\n", d, x); ++bad; }
+    };
+    const uint32_t top = 0x7fffffffu;
+    for (uint32_t d = 1; d < 70000; ++d) {
+        for (uint32_t x : {0u, 1u, d - 1, d, d + 1, 2 * d - 1, 2 * d, top, top - 1, top - d})
+            if (x <= top) check(d, x);
+        for (int k = 0; k < 16; ++k) check(d, (uint32_t)(rng() & top));
+        uint32_t q = top / d;
+        check(d, q * d); check(d, q * d - 1 < top ? q * d - 1 : 0);
+    }
+    for (int k = 0; k < 2000000; ++k) {
+        uint32_t d = (uint32_t)(rng() % top) + 1, x = (uint32_t)(rng() & top);
+        check(d, x);
+        if (x >= d) check(d, (x / d) * d);
+    }
+    for (int b = 0; b < 31; ++b) {
+        for (uint32_t d : {1u << b, (1u << b) + 1, (1u << b) - 1}) {
+            if (!d) continue;
+            for (int k = 0; k < 2000; ++k) check(d, (uint32_t)(rng() & top));
+            check(d, top);
+        }
+    }
+    printf("%llu checks, %llu wrong\n", (unsigned long long)n, (unsigned long long)bad);
+    return bad != 0;
+}
+''')
+    exe = tmp_path / "fd"
+    subprocess.run(["g++", "-O2", "-std=c++17", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include",
+                    "-I", os.path.join(REPO, "paper_1706_06873_amd", "csrc"), str(src), "-o",
+                    str(exe)], check=True)
+    out = subprocess.run([str(exe)], capture_output=True, text=True)
+    assert out.returncode == 0, out.stdout
+    assert " 0 wrong" in out.stdout

@@ -1,0 +1,279 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Bars: L bit for bit; O within relative L2 error 1e-5 for fp32 inputs, and for
+bf16 inputs within 1e-5 of the oracle fed the same bf16 values (the GPU
+accumulates in fp32) and within 1e-2 of the oracle fed the fp32 values before
+rounding. With small-integer inputs every partial sum is exact in fp32, so O
+must then match bit for bit.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_1706_06873_amd as mec
+from paper_1706_06873_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+TOL_F32 = 1e-5
+TOL_BF16_VS_F32 = 1e-2
+
+
+def say(*a):
+    print("[case]", *a, flush=True)
+
+
+def rel_l2(got, ref):
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    den = np.linalg.norm(ref)
+    return np.linalg.norm(got - ref) / (den if den > 0 else 1.0)
+
+
+def to_dev(t):
+    return t.to(DEV)
+
+
+def host(t):
+    return wl.to_oracle_array(t)
+
+
+def case(seed, dims, dtype="f32", dist="u11"):
+    return wl.random_case(seed, *dims, dtype=dtype, dist=dist)
+
+
+# Shapes that reach every kernel configuration and the ragged edges: pairs not
+# a multiple of 32, o_h not a multiple of the h tile, k_c not a multiple of 32,
+# R not a multiple of the r-chunk, s not dividing i - k, s >= k, k = i.
+SWEEP = [
+    # i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w
+    (1, 7, 7, 1, 3, 3, 1, 1, 1),
+    (2, 19, 17, 64, 3, 3, 64, 1, 1),     # f32 wide
+    (3, 20, 21, 16, 3, 3, 40, 1, 2),     # wide, ragged channels
+    (2, 23, 25, 3, 3, 3, 64, 1, 1),      # narrow (R = 9)
+    (3, 31, 30, 3, 11, 11, 96, 4, 4),    # tall (11x11 s4)
+    (1, 35, 33, 3, 11, 11, 100, 4, 3),   # tall, ragged channels and strides
+    (2, 13, 12, 5, 5, 5, 33, 2, 2),
+    (1, 30, 9, 2, 20, 3, 7, 1, 1),       # generic HT=4 (tall k_h)
+    (1, 40, 9, 1, 13, 3, 130, 9, 1),     # generic HT=4, large s_h
+    (1, 60, 9, 1, 20, 3, 130, 16, 1),    # generic HT=1 (hrows of HT=4 too many)
+    (2, 9, 9, 4, 3, 3, 8, 3, 3),         # s == k
+    (1, 11, 10, 3, 2, 2, 5, 4, 3),       # s > k
+    (2, 6, 5, 7, 6, 5, 3, 1, 1),         # k == i: o = 1 x 1
+    (4, 8, 8, 8, 1, 1, 16, 1, 1),        # 1x1
+    (1, 3, 70, 2, 3, 1, 1, 1, 1),        # o_h = 1, many pairs
+    (33, 4, 4, 4, 2, 2, 33, 1, 1),       # pairs = 99
+]
+
+SWEEP_BF16 = [
+    (2, 19, 17, 64, 3, 3, 64, 1, 1),     # bf16 8-wide loads
+    (2, 10, 10, 16, 3, 3, 96, 1, 1),
+    (3, 17, 15, 3, 3, 3, 40, 1, 2),      # bf16 generic
+    (2, 31, 30, 3, 11, 11, 64, 4, 4),    # bf16 tall -> HT=1
+    (1, 12, 12, 8, 5, 3, 130, 2, 1),
+    (2, 6, 5, 7, 6, 5, 3, 1, 1),
+]
+
+
+def run_conv(I, K, s_h, s_w, algo):
+    O = mec.conv2d(to_dev(I), to_dev(K), s_h, s_w, algo=algo)
+    torch.cuda.synchronize()
+    return O.cpu().numpy()
+
+
+@pytest.mark.parametrize("dims", SWEEP)
+@pytest.mark.parametrize("algo", ["lowered", "fused"])
+def test_conv_f32_sweep(orc, dims, algo):
+    say("conv f32", algo, dims)
+    I, K = case(sum(dims), dims)
+    s_h, s_w = dims[7], dims[8]
+    ref = orc.conv2d_direct(host(I), host(K), s_h, s_w)
+    got = run_conv(I, K, s_h, s_w, algo)
+    assert got.shape == ref.shape
+    assert rel_l2(got, ref) <= TOL_F32
+
+
+@pytest.mark.parametrize("dims", SWEEP)
+@pytest.mark.parametrize("algo", ["lowered", "fused"])
+def test_conv_f32_integer_inputs_bitwise(orc, dims, algo):
+    say("conv f32 int", algo, dims)
+    I, K = case(7 + sum(dims), dims, dist="int")
+    s_h, s_w = dims[7], dims[8]
+    ref = orc.conv2d_direct(host(I), host(K), s_h, s_w)
+    assert np.abs(ref).max() < 2 ** 24
+    got = run_conv(I, K, s_h, s_w, algo)
+    assert np.array_equal(got, ref.astype(np.float32))
+
+
+@pytest.mark.parametrize("dims", SWEEP_BF16)
+@pytest.mark.parametrize("algo", ["lowered", "fused"])
+def test_conv_bf16_sweep(orc, dims, algo):
+    say("conv bf16", algo, dims)
+    I32, K32 = case(3 * sum(dims), dims, dtype="f32")
+    I, K = I32.to(torch.bfloat16), K32.to(torch.bfloat16)
+    s_h, s_w = dims[7], dims[8]
+    ref_bf = orc.conv2d_direct(host(I), host(K), s_h, s_w)
+    ref_32 = orc.conv2d_direct(host(I32), host(K32), s_h, s_w)
+    got = run_conv(I, K, s_h, s_w, algo)
+    assert rel_l2(got, ref_bf) <= TOL_F32
+    assert rel_l2(got, ref_32) <= TOL_BF16_VS_F32
+
+
+@pytest.mark.parametrize("dims", SWEEP_BF16)
+def test_conv_bf16_integer_inputs_bitwise(orc, dims):
+    say("conv bf16 int", dims)
+    I, K = case(11 + sum(dims), dims, dtype="bf16", dist="int")
+    s_h, s_w = dims[7], dims[8]
+    ref = orc.conv2d_direct(host(I), host(K), s_h, s_w)
+    for algo in ("lowered", "fused"):
+        assert np.array_equal(run_conv(I, K, s_h, s_w, algo), ref.astype(np.float32))
+
+
+@pytest.mark.parametrize("dims", SWEEP + SWEEP_BF16)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_lower_bitwise_sweep(orc, dims, dtype):
+    say("lower", dtype, dims)
+    I, _ = case(5 * sum(dims), dims, dtype=dtype)
+    k_h, k_w, k_c, s_h, s_w = dims[4:]
+    ref = orc.mec_lower(host(I), k_h, k_w, k_c, s_h, s_w)
+    L = mec.lower(to_dev(I), k_h, k_w, k_c, s_h, s_w)
+    torch.cuda.synchronize()
+    got = host(L.cpu())
+    assert got.shape == ref.shape and np.array_equal(got, ref)
+
+
+@pytest.mark.parametrize("shift", [1, 2, 3])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_unaligned_tensors(orc, shift, dtype):
+    """Tensors that start off a 16-byte boundary take the element-wise paths."""
+    dims = (2, 19, 17, 64, 3, 3, 64, 1, 1)
+    say("unaligned", dtype, shift, dims)
+    I, K = case(99, dims, dtype=dtype, dist="int")
+    k_h, k_w, k_c, s_h, s_w = dims[4:]
+    tdt = I.dtype
+
+    def offset_copy(t):
+        buf = torch.zeros(t.numel() + 8, dtype=tdt, device=DEV)
+        v = buf[shift:shift + t.numel()].view(t.shape)
+        v.copy_(t.to(DEV))
+        return v
+
+    Id, Kd = offset_copy(I), offset_copy(K)
+    assert Id.data_ptr() % 16 != 0
+    Lbuf = torch.zeros(orc.lowered_elems(*dims) + 8, dtype=tdt, device=DEV)
+    Ld = Lbuf[shift:shift + orc.lowered_elems(*dims)]
+    mec.lower(Id, k_h, k_w, k_c, s_h, s_w, L=Ld)
+    ref_L = orc.mec_lower(host(I), k_h, k_w, k_c, s_h, s_w)
+    ref = orc.conv2d_direct(host(I), host(K), s_h, s_w).astype(np.float32)
+    Obuf = torch.zeros(ref.size + 8, dtype=torch.float32, device=DEV)
+    Od = Obuf[shift:shift + ref.size].view(ref.shape)
+    es = 2 if dtype == "bf16" else 4
+    ws = torch.zeros(mec.workspace_bytes(*dims, dtype=mec.BF16 if dtype == "bf16" else mec.F32)
+                     + 64, dtype=torch.uint8, device=DEV)[es * shift:]
+    torch.cuda.synchronize()
+    assert np.array_equal(host(Ld.cpu()).reshape(ref_L.shape), ref_L)
+    for algo in ("lowered", "fused"):
+        Od.zero_()
+        mec.conv2d(Id, Kd, s_h, s_w, algo=algo, O=Od, workspace=ws)
+        torch.cuda.synchronize()
+        assert np.array_equal(Od.cpu().numpy(), ref), algo
+
+
+@pytest.mark.parametrize("dims", SWEEP[:8])
+def test_workspace_holds_L_and_gemm_alone(orc, dims):
+    say("workspace/gemm", dims)
+    I, K = case(2 * sum(dims), dims)
+    k_h, k_w, k_c, s_h, s_w = dims[4:]
+    ws = torch.empty(mec.workspace_bytes(*dims), dtype=torch.uint8, device=DEV)
+    O = mec.conv2d(to_dev(I), to_dev(K), s_h, s_w, algo="lowered", workspace=ws)
+    ref_L = orc.mec_lower(host(I), k_h, k_w, k_c, s_h, s_w)
+    torch.cuda.synchronize()
+    assert np.array_equal(ws.cpu().numpy().view(np.float32).reshape(ref_L.shape), ref_L)
+    # the product phase alone, on the oracle's L
+    O2 = mec.gemm(to_dev(torch.from_numpy(ref_L)), to_dev(K), dims[1], dims[2], s_h, s_w)
+    ref = orc.mec_gemm(ref_L, host(K), dims[1], dims[2], s_h, s_w, "B")
+    torch.cuda.synchronize()
+    assert rel_l2(O2.cpu().numpy(), ref) <= TOL_F32
+    assert np.array_equal(O2.cpu().numpy(), O.cpu().numpy())
+
+
+def test_output_not_written_outside(orc):
+    """O of a ragged shape written exactly in place: a guard band stays intact."""
+    dims = (3, 31, 30, 3, 11, 11, 100, 4, 3)
+    say("guard", dims)
+    I, K = case(5, dims)
+    ref = orc.conv2d_direct(host(I), host(K), dims[7], dims[8]).astype(np.float32)
+    buf = torch.full((ref.size + 4096,), 7.0, dtype=torch.float32, device=DEV)
+    O = buf[1024:1024 + ref.size].view(ref.shape)
+    for algo in ("lowered", "fused"):
+        mec.conv2d(to_dev(I), to_dev(K), dims[7], dims[8], algo=algo, O=O)
+        torch.cuda.synchronize()
+        b = buf.cpu().numpy()
+        assert np.all(b[:1024] == 7.0) and np.all(b[1024 + ref.size:] == 7.0)
+        assert rel_l2(O.cpu().numpy(), ref) <= TOL_F32
+
+
+# ---------------------------------------------------------------- the five layers
+
+LAYERS = wl.LAYER_ORDER
+
+
+@pytest.mark.parametrize("name", LAYERS)
+def test_layer_lower_full_bitwise(orc, name):
+    layer = wl.LAYERS[name]
+    say("layer lower full", name)
+    I, _ = wl.make_inputs(layer)
+    k_h, k_w, k_c, s_h, s_w = layer.dims[4:]
+    Ld = mec.lower(to_dev(I), k_h, k_w, k_c, s_h, s_w)
+    ref = orc.mec_lower(host(I), k_h, k_w, k_c, s_h, s_w)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(Ld.cpu()), ref)
+
+
+@pytest.mark.parametrize("name", LAYERS)
+def test_layer_reduced_batch_full_compare(orc, name):
+    """Full output compared at a batch of 2 (all spatial tiles, ragged edges)."""
+    layer = wl.LAYERS[name]
+    say("layer reduced batch", name)
+    I, K = wl.make_inputs(layer, i_n=min(2, layer.i_n))
+    s_h, s_w = layer.s_h, layer.s_w
+    ref = orc.conv2d_direct(host(I), host(K), s_h, s_w)
+    ref32 = None
+    if layer.dtype == "bf16":
+        # the 1e-2 bar is sized for the fp32 values before rounding to bf16
+        I32, K32 = wl.make_inputs(layer, i_n=min(2, layer.i_n), round_bf16=False)
+        assert torch.equal(I32.to(torch.bfloat16), I)
+        ref32 = orc.conv2d_direct(host(I32), host(K32), s_h, s_w)
+    for algo in ("lowered", "fused"):
+        got = run_conv(I, K, s_h, s_w, algo)
+        assert rel_l2(got, ref) <= TOL_F32, algo
+        if ref32 is not None:
+            assert rel_l2(got, ref32) <= TOL_BF16_VS_F32, algo
+
+
+@pytest.mark.parametrize("name", LAYERS)
+def test_layer_full_size_sampled(orc, name):
+    """Full-size layers in the benchmark's launch configuration, checked on
+    sampled outputs the oracle computes one by one (corners included), and
+    LOWERED == FUSED bit for bit (same staged values, same reduction order)."""
+    layer = wl.LAYERS[name]
+    say("layer full sampled", name)
+    I, K = wl.make_inputs(layer)
+    s_h, s_w = layer.s_h, layer.s_w
+    Id, Kd = to_dev(I), to_dev(K)
+    O1 = mec.conv2d(Id, Kd, s_h, s_w, algo="lowered")
+    O2 = mec.conv2d(Id, Kd, s_h, s_w, algo="fused")
+    torch.cuda.synchronize()
+    shape = tuple(O1.shape)
+    rng = np.random.default_rng(layer.seed)
+    idx = np.stack([rng.integers(0, d, 3000) for d in shape], axis=1)
+    corners = np.array([[n, y, x, m] for n in (0, shape[0] - 1) for y in (0, shape[1] - 1)
+                        for x in (0, shape[2] - 1) for m in (0, shape[3] - 1)])
+    idx = np.concatenate([idx, corners])
+    ref = orc.conv2d_points(host(I), host(K), s_h, s_w, idx)
+    g1 = O1.cpu().numpy()
+    assert rel_l2(g1[tuple(idx.T)], ref) <= TOL_F32
+    assert torch.equal(O1, O2)
+    assert np.isfinite(g1).all()
