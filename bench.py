@@ -87,7 +87,7 @@ def main():
         if j:
             I = I.clone()
         sets.append(dict(I=I, K=K0.to(dev),
-                         L=torch.empty(size_L, dtype=I0.dtype, device=dev),
+                         L=torch.empty((i_n, o_w, i_h, k_w, i_c), dtype=I0.dtype, device=dev),
                          O=torch.empty((i_n, o_h, o_w, k_c), dtype=torch.float32, device=dev)))
     stream = torch.cuda.Stream(device=dev)  # default priority
     torch.cuda.synchronize()

@@ -23,42 +23,10 @@
 // k); bf16 uses v_mfma_f32_32x32x16_bf16 (8 consecutive k per lane) with fp32
 // accumulation. The epilogue stores each accumulator straight into n-h-w-c O,
 // which replaces Solution A's h-n-w-c result and its transposition.
-#include <hip/hip_runtime.h>
-
-#include "mec_internal.h"
+#include "mec_mfma.h"
 
 namespace mec {
 namespace {
-
-typedef float floatx16 __attribute__((ext_vector_type(16)));
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-
-constexpr int kThreads = 256;
-constexpr int kPairs = 32;  // pairs per tile = MFMA block rows
-
-struct TraitsF32 {
-    using E = uint32_t;              // fp32 bits in LDS and registers
-    static constexpr int KS = 2;     // reduction length of one MFMA
-    static constexpr int KL = 1;     // k values each lane supplies
-    using Frag = float;
-    static __device__ inline Frag frag(const E* p) { return __builtin_bit_cast(float, *p); }
-    static __device__ inline floatx16 mfma(Frag a, Frag b, floatx16 c) {
-        return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
-    }
-};
-
-struct TraitsBF16 {
-    using E = uint16_t;              // bf16 bits
-    static constexpr int KS = 16;
-    static constexpr int KL = 8;
-    using Frag = bf16x8;
-    static __device__ inline Frag frag(const E* p) {
-        return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(p));
-    }
-    static __device__ inline floatx16 mfma(Frag a, Frag b, floatx16 c) {
-        return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
-    }
-};
 
 // Launch-time layout of the LDS stages (elements of E).
 struct Lds {
@@ -96,24 +64,6 @@ struct Cfg {
     // elements of one stage each thread moves (A in vectors of VA, B singly)
     static constexpr int AVEC = PF ? (kPairs * HROWS_MAX * KT / VA + kThreads - 1) / kThreads : 1;
     static constexpr int BREG = PF ? (KH_MAX * NT * KT + kThreads - 1) / kThreads : 1;
-};
-
-// VA consecutive elements moved as one load: 16 bytes when VA*sizeof(E) == 16.
-template <int VA, typename E, bool WIDE = (VA * sizeof(E) == 16)>
-struct VecA {
-    E e[VA];
-    __device__ inline void load(const E* src) {
-#pragma unroll
-        for (int k = 0; k < VA; ++k) e[k] = src[k];
-    }
-};
-template <int VA, typename E>
-struct VecA<VA, E, true> {
-    union {
-        uint4 v;
-        E e[VA];
-    };
-    __device__ inline void load(const E* src) { v = *reinterpret_cast<const uint4*>(src); }
 };
 
 template <class C>
@@ -187,7 +137,7 @@ __global__ __launch_bounds__(kThreads) void slab_gemm_kernel(Args args) {
         return nullptr;
     };
 
-    VecA<VA, E> areg[C::AVEC];
+    VecN<VA, E> areg[C::AVEC];
     E breg[C::BREG];
 
     // PF: global -> registers for r-chunk rc
@@ -197,9 +147,8 @@ __global__ __launch_bounds__(kThreads) void slab_gemm_kernel(Args args) {
 #pragma unroll
         for (int j = 0; j < C::AVEC; ++j) {
             const int e = (tid + j * kThreads) * VA;
-            VecA<VA, E> v;
-#pragma unroll
-            for (int k = 0; k < VA; ++k) v.e[k] = 0;
+            VecN<VA, E> v;
+            v.zero();
             if (e < a_count) {
                 const E* src = a_map(e, r0, off);
                 if (src) v.load(src);
@@ -246,9 +195,8 @@ __global__ __launch_bounds__(kThreads) void slab_gemm_kernel(Args args) {
         int off;
 #pragma unroll 2
         for (int e = tid * VA; e < a_count; e += kThreads * VA) {
-            VecA<VA, E> v;
-#pragma unroll
-            for (int k = 0; k < VA; ++k) v.e[k] = 0;
+            VecN<VA, E> v;
+            v.zero();
             const E* src = a_map(e, r0, off);
             if (src) v.load(src);
 #pragma unroll
@@ -334,8 +282,7 @@ __global__ __launch_bounds__(kThreads) void slab_gemm_kernel(Args args) {
             if (c >= p.k_c) continue;
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
-                const int i = (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
-                const int64_t ob = obase[i];
+                const int64_t ob = obase[acc_row(v, lane)];
                 if (ob >= 0) p.O[ob + h * ostride_h + c] = acc[hw][nb][v];
             }
         }
@@ -461,11 +408,16 @@ hipError_t dispatch(const Shape& s, const void* A, const void* K, float* O, int 
 }  // namespace
 
 bool gemm_supported(const Shape& s, int dtype) {
+    if (launch_gemm_fixed(s, nullptr, nullptr, nullptr, dtype, false, nullptr, true) == hipSuccess)
+        return true;
     return dispatch<false>(s, nullptr, nullptr, nullptr, dtype, nullptr, true) == hipSuccess;
 }
 
 hipError_t launch_gemm(const Shape& s, const void* A, const void* K, float* O, int dtype,
                        bool fused, hipStream_t stream) {
+    // kernels specialised for this kernel height and stride first
+    const hipError_t e = launch_gemm_fixed(s, A, K, O, dtype, fused, stream, false);
+    if (e != hipErrorNotSupported) return e;
     if (fused) return dispatch<true>(s, A, K, O, dtype, stream, false);
     return dispatch<false>(s, A, K, O, dtype, stream, false);
 }

@@ -87,6 +87,12 @@ hipError_t launch_gemm(const Shape& s, const void* A, const void* K, float* O, i
 // Whether the slab-product kernels can run this shape (LDS limits).
 bool gemm_supported(const Shape& s, int dtype);
 
+// The kernels specialised for a compile-time kernel height and stride.
+// Returns hipErrorNotSupported when none matches the shape (or the pointers'
+// alignment); with dry_run, only reports whether one matches.
+hipError_t launch_gemm_fixed(const Shape& s, const void* A, const void* K, float* O, int dtype,
+                             bool fused, hipStream_t stream, bool dry_run);
+
 }  // namespace mec
 
 #if defined(__HIP__)
