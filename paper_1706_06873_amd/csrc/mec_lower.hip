@@ -3,12 +3,27 @@
 // L viewed as (i_n*o_w*i_h) rows of R = k_w*i_c elements: row q = (n*o_w + w)*i_h + h
 // is the contiguous run of R elements of I that starts at ((n*i_h + h)*i_w + s_w*w)*i_c.
 //
-// A pure copy, bound by HBM bandwidth. Each workgroup owns a contiguous range of
-// L rows, so its stores form one contiguous, 16-byte-vectorised stream. The
-// source offset of each of its rows is computed once into LDS. Reads of I are
-// contiguous inside each run; the k_w/s_w-fold re-reads of I by neighbouring
-// w hit in L2 because workgroups are remapped so that each XCD walks one
-// contiguous range of L.
+// A pure copy, bound by HBM bandwidth, and write-heavy: |L| is about
+// k_w/s_w times |I|. Three kernels, chosen per shape on the host:
+//
+//  rows   Every run starts on a 16-byte boundary (R, s_w*i_c and i_w*i_c are
+//         multiples of the 16-byte vector). A workgroup reads one input row
+//         (n, h) into LDS once -- a contiguous, fully coalesced read, so I is
+//         read from HBM exactly once -- and writes its o_w runs
+//         L[n, w, h, :] as 16-byte non-temporal stores. The runs are
+//         scattered through L (stride i_h*R); streaming them past the caches
+//         is what lets the write stream run near copy speed.
+//  strip  Short or unaligned runs (e.g. R = 33 fp32 for 11x11x3 kernels). A
+//         workgroup reads Hb consecutive input rows of one image (again one
+//         contiguous span of I) and, for every w, writes the chunk
+//         L[n, w, h0:h0+Hb, :] -- contiguous in L, Hb*R elements -- with
+//         aligned 16-byte non-temporal stores and element stores at the
+//         chunk's unaligned head and tail.
+//  gather Fallback when an input row does not fit in LDS: each thread
+//         gathers 16 bytes of L straight from I.
+//
+// Workgroups are remapped so that each XCD (which receives workgroups
+// round-robin) walks one contiguous range of the work.
 #include <hip/hip_runtime.h>
 
 #include "mec_internal.h"
@@ -16,24 +31,136 @@
 namespace mec {
 namespace {
 
-constexpr int kThreads = 256;
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kRowsThreads = 256;
+constexpr int kStripThreads = 512;
+constexpr int kGatherThreads = 256;
 constexpr int kMaxRowsPerBlock = 1024;
 constexpr int64_t kTargetElemsPerBlock = 8192;
+constexpr int64_t kRowsLdsLimit = 64 * 1024;   // one input row, rows kernel
+constexpr int64_t kStripLdsLimit = 48 * 1024;  // Hb input rows, strip kernel
 
 // E is a 32-bit (fp32) or 16-bit (bf16) payload; VEC elements make 16 bytes.
 template <typename E>
 struct Vec16 {
     static constexpr int N = 16 / sizeof(E);
     union {
-        uint4 v;
+        u32x4 v;
         E e[N];
     };
 };
 
-// Source offset (elements of I) of the first element of each L row of the block.
-__device__ inline void fill_row_sources(int64_t* src, const LowerParams& p, int64_t row0,
-                                        int nrows) {
-    for (int i = threadIdx.x; i < nrows; i += kThreads) {
+inline bool aligned16(const void* ptr) { return ((uintptr_t)ptr & 15u) == 0; }
+
+// ---------------------------------------------------------------- rows
+struct RowsParams {
+    const void* I;
+    void* L;
+    uint32_t nrows_in;  // i_n * i_h
+    uint32_t i_h, o_w;
+    uint32_t rowv;      // vectors per input row: i_w*i_c / VEC
+    uint32_t RV;        // vectors per run: R / VEC
+    uint32_t swv;       // vectors between consecutive runs in a row: s_w*i_c / VEC
+    FastDiv div_ih, div_RV;
+};
+
+template <typename E>
+__global__ __launch_bounds__(kRowsThreads) void lower_rows_kernel(RowsParams p) {
+    extern __shared__ u32x4 row[];
+    const uint32_t blk = xcd_remap(blockIdx.x, p.nrows_in);  // input row n*i_h + h
+    const uint32_t n = p.div_ih.div(blk), h = blk - n * p.i_h;
+    const u32x4* __restrict__ I = reinterpret_cast<const u32x4*>(p.I) + (size_t)blk * p.rowv;
+    for (uint32_t i = threadIdx.x; i < p.rowv; i += kRowsThreads) row[i] = I[i];
+    __syncthreads();
+    u32x4* __restrict__ L = reinterpret_cast<u32x4*>(p.L);
+    const uint32_t total = p.o_w * p.RV;
+    for (uint32_t f = threadIdx.x; f < total; f += kRowsThreads) {
+        const uint32_t w = p.div_RV.div(f);
+        const uint32_t c = f - w * p.RV;
+        __builtin_nontemporal_store(row[w * p.swv + c],
+                                    L + (((size_t)n * p.o_w + w) * p.i_h + h) * p.RV + c);
+    }
+}
+
+// ---------------------------------------------------------------- strip
+struct StripParams {
+    const void* I;
+    void* L;
+    uint32_t i_h, o_w, rowlen, R, swic, Hb, hblocks, vpw, nblocks;
+    FastDiv div_hblocks, div_R, div_vpw;
+};
+
+// VECIN: input rows are 16-byte vectors; VECOUT: L is 16-byte aligned.
+template <typename E, bool VECIN, bool VECOUT>
+__global__ __launch_bounds__(kStripThreads) void lower_strip_kernel(StripParams p) {
+    constexpr int VEC = Vec16<E>::N;
+    extern __shared__ u32x4 strip4[];
+    E* rows = reinterpret_cast<E*>(strip4);
+    const uint32_t blk = xcd_remap(blockIdx.x, p.nblocks);
+    const uint32_t n = p.div_hblocks.div(blk), h0 = (blk - n * p.hblocks) * p.Hb;
+    const uint32_t hb = min(p.Hb, p.i_h - h0);
+    const uint32_t nin = hb * p.rowlen;
+    const E* __restrict__ I = reinterpret_cast<const E*>(p.I) + ((size_t)n * p.i_h + h0) * p.rowlen;
+    if (VECIN) {
+        for (uint32_t i = threadIdx.x; i < nin / VEC; i += kStripThreads)
+            strip4[i] = reinterpret_cast<const u32x4*>(I)[i];
+    } else {
+        for (uint32_t i = threadIdx.x; i < nin; i += kStripThreads) rows[i] = I[i];
+    }
+    __syncthreads();
+
+    const uint32_t len = hb * p.R;  // elements of the chunk L[n, w, h0:h0+hb, :]
+    E* __restrict__ L = reinterpret_cast<E*>(p.L);
+    const uint32_t total = p.o_w * p.vpw;
+    for (uint32_t f = threadIdx.x; f < total; f += kStripThreads) {
+        const uint32_t w = p.div_vpw.div(f);
+        const uint32_t v = f - w * p.vpw;
+        const size_t g0 = (((size_t)n * p.o_w + w) * p.i_h + h0) * p.R;  // chunk start in L
+        // the chunk is covered by the 16-byte-aligned vectors starting at a0
+        const size_t a0 = VECOUT ? g0 & ~(size_t)(VEC - 1) : g0;
+        const size_t gv = a0 + (size_t)v * VEC;
+        if (gv >= g0 + len) continue;
+        const int e0 = (int)((long long)gv - (long long)g0);  // chunk index of the vector's first element
+        uint32_t ee = e0 < 0 ? 0u : (uint32_t)e0;
+        uint32_t r = p.div_R.div(ee), c = ee - r * p.R;
+        const E* src = rows + w * p.swic;
+        Vec16<E> val;
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) {
+            const int e = e0 + k;
+            val.e[k] = E(0);
+            if (e >= 0 && e < (int)len) {
+                val.e[k] = src[r * p.rowlen + c];
+                if (++c == p.R) {
+                    c = 0;
+                    ++r;
+                }
+            }
+        }
+        if (VECOUT && e0 >= 0 && e0 + VEC <= (int)len) {
+            __builtin_nontemporal_store(val.v, reinterpret_cast<u32x4*>(L + gv));
+        } else {
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) {
+                const int e = e0 + k;
+                if (e >= 0 && e < (int)len) L[gv + k] = val.e[k];
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------- gather
+// Each workgroup owns a contiguous range of L rows; the source offset of each
+// of its rows is computed once into LDS.
+template <typename E, bool VECDST>
+__global__ __launch_bounds__(kGatherThreads) void lower_gather_kernel(LowerParams p) {
+    constexpr int VEC = Vec16<E>::N;
+    __shared__ int64_t src[kMaxRowsPerBlock];
+    const uint32_t blk = xcd_remap(blockIdx.x, p.nblocks);
+    const int64_t row0 = (int64_t)blk * p.rows_per_block;
+    const int nrows = (int)min((int64_t)p.rows_per_block, p.rows - row0);
+    for (int i = threadIdx.x; i < nrows; i += kGatherThreads) {
         const int64_t q = row0 + i;
         const int64_t h = q % p.i_h;
         const int64_t nw = q / p.i_h;
@@ -41,49 +168,13 @@ __device__ inline void fill_row_sources(int64_t* src, const LowerParams& p, int6
         const int64_t n = nw / p.o_w;
         src[i] = ((n * p.i_h + h) * p.i_w + p.s_w * w) * p.i_c;
     }
-}
-
-// Every run start is a multiple of VEC elements and both tensors are 16-byte
-// aligned: one 16-byte load and one 16-byte store per vector.
-template <typename E>
-__global__ __launch_bounds__(kThreads) void lower_vec_kernel(LowerParams p) {
-    constexpr int VEC = Vec16<E>::N;
-    __shared__ int64_t src[kMaxRowsPerBlock];
-    const uint32_t blk = xcd_remap(blockIdx.x, p.nblocks);
-    const int64_t row0 = (int64_t)blk * p.rows_per_block;
-    const int nrows = (int)min((int64_t)p.rows_per_block, p.rows - row0);
-    fill_row_sources(src, p, row0, nrows);
-    __syncthreads();
-
-    const uint32_t RV = (uint32_t)(p.R / VEC);  // vectors per row
-    const uint32_t total = (uint32_t)nrows * RV;
-    const uint4* __restrict__ I = reinterpret_cast<const uint4*>(p.I);
-    uint4* __restrict__ L = reinterpret_cast<uint4*>(p.L) + row0 * (int64_t)RV;
-    for (uint32_t f = threadIdx.x; f < total; f += kThreads) {
-        const uint32_t r = p.divR.div(f);
-        const uint32_t c = f - r * RV;
-        L[f] = I[src[r] / VEC + c];
-    }
-}
-
-// General runs (any R, any alignment of the run starts). Each thread gathers
-// VEC consecutive L elements and writes them with one 16-byte store when the
-// block's slice of L is 16-byte aligned (VECDST), element by element otherwise.
-template <typename E, bool VECDST>
-__global__ __launch_bounds__(kThreads) void lower_gather_kernel(LowerParams p) {
-    constexpr int VEC = Vec16<E>::N;
-    __shared__ int64_t src[kMaxRowsPerBlock];
-    const uint32_t blk = xcd_remap(blockIdx.x, p.nblocks);
-    const int64_t row0 = (int64_t)blk * p.rows_per_block;
-    const int nrows = (int)min((int64_t)p.rows_per_block, p.rows - row0);
-    fill_row_sources(src, p, row0, nrows);
     __syncthreads();
 
     const uint32_t R = (uint32_t)p.R;
     const uint32_t count = (uint32_t)nrows * R;  // elements of L this block writes
     const E* __restrict__ I = reinterpret_cast<const E*>(p.I);
     E* __restrict__ L = reinterpret_cast<E*>(p.L) + row0 * p.R;
-    for (uint32_t e0 = threadIdx.x * VEC; e0 < count; e0 += kThreads * VEC) {
+    for (uint32_t e0 = threadIdx.x * VEC; e0 < count; e0 += kGatherThreads * VEC) {
         uint32_t r = p.divR.div(e0);
         uint32_t c = e0 - r * R;
         Vec16<E> v;
@@ -96,7 +187,7 @@ __global__ __launch_bounds__(kThreads) void lower_gather_kernel(LowerParams p) {
             }
         }
         if (VECDST && e0 + VEC <= count) {
-            *reinterpret_cast<uint4*>(L + e0) = v.v;
+            *reinterpret_cast<u32x4*>(L + e0) = v.v;
         } else {
 #pragma unroll
             for (int k = 0; k < VEC; ++k)
@@ -105,10 +196,71 @@ __global__ __launch_bounds__(kThreads) void lower_gather_kernel(LowerParams p) {
     }
 }
 
-inline bool aligned16(const void* ptr) { return ((uintptr_t)ptr & 15u) == 0; }
+// ---------------------------------------------------------------- host side
 
 template <typename E>
-hipError_t launch_typed(const Shape& s, const void* I, void* L, hipStream_t stream) {
+hipError_t launch_rows(const Shape& s, const void* I, void* L, hipStream_t stream) {
+    constexpr int VEC = Vec16<E>::N;
+    RowsParams p{};
+    p.I = I;
+    p.L = L;
+    p.nrows_in = (uint32_t)(s.i_n * s.i_h);
+    p.i_h = (uint32_t)s.i_h;
+    p.o_w = (uint32_t)s.o_w;
+    p.rowv = (uint32_t)(s.i_w * s.i_c / VEC);
+    p.RV = (uint32_t)(s.R / VEC);
+    p.swv = (uint32_t)(s.s_w * s.i_c / VEC);
+    p.div_ih = FastDiv(p.i_h);
+    p.div_RV = FastDiv(p.RV);
+    hipLaunchKernelGGL(lower_rows_kernel<E>, dim3(p.nrows_in), dim3(kRowsThreads),
+                       (size_t)p.rowv * 16, stream, p);
+    return hipGetLastError();
+}
+
+template <typename E>
+hipError_t launch_strip(const Shape& s, const void* I, void* L, hipStream_t stream) {
+    constexpr int VEC = Vec16<E>::N;
+    const int64_t es = sizeof(E);
+    const int64_t row_bytes = s.i_w * s.i_c * es;
+    // Hb rows per workgroup: chunks of about 1 KB of L, enough workgroups to
+    // fill the chip (about 1024), and Hb rows within the LDS limit.
+    int64_t hb = (1024 + s.R * es - 1) / (s.R * es);
+    const int64_t by_count = (s.i_n * s.i_h) / 1024;
+    if (hb > by_count) hb = by_count;
+    if (hb > kStripLdsLimit / row_bytes) hb = kStripLdsLimit / row_bytes;
+    if (hb > s.i_h) hb = s.i_h;
+    if (hb < 1) hb = 1;
+    StripParams p{};
+    p.I = I;
+    p.L = L;
+    p.i_h = (uint32_t)s.i_h;
+    p.o_w = (uint32_t)s.o_w;
+    p.rowlen = (uint32_t)(s.i_w * s.i_c);
+    p.R = (uint32_t)s.R;
+    p.swic = (uint32_t)(s.s_w * s.i_c);
+    p.Hb = (uint32_t)hb;
+    p.hblocks = (uint32_t)((s.i_h + hb - 1) / hb);
+    p.vpw = (uint32_t)((hb * s.R + VEC - 1) / VEC + 1);
+    p.nblocks = (uint32_t)(s.i_n * p.hblocks);
+    p.div_hblocks = FastDiv(p.hblocks);
+    p.div_R = FastDiv(p.R);
+    p.div_vpw = FastDiv(p.vpw);
+    const size_t lds = (size_t)hb * row_bytes;
+    const bool vin = (s.i_w * s.i_c) % VEC == 0 && aligned16(I);
+    const bool vout = aligned16(L);
+#define MEC_STRIP(VI, VO)                                                                      \
+    hipLaunchKernelGGL((lower_strip_kernel<E, VI, VO>), dim3(p.nblocks), dim3(kStripThreads), \
+                       lds, stream, p)
+    if (vin && vout) MEC_STRIP(true, true);
+    else if (vin) MEC_STRIP(true, false);
+    else if (vout) MEC_STRIP(false, true);
+    else MEC_STRIP(false, false);
+#undef MEC_STRIP
+    return hipGetLastError();
+}
+
+template <typename E>
+hipError_t launch_gather(const Shape& s, const void* I, void* L, hipStream_t stream) {
     constexpr int VEC = Vec16<E>::N;
     LowerParams p{};
     p.I = I;
@@ -120,30 +272,35 @@ hipError_t launch_typed(const Shape& s, const void* I, void* L, hipStream_t stre
     p.i_w = s.i_w;
     p.i_c = s.i_c;
     p.s_w = s.s_w;
-    // Rows per block: about kTargetElemsPerBlock elements, a multiple of VEC so
-    // every block's slice of L starts 16-byte aligned when L does.
+    // rows per block: about kTargetElemsPerBlock elements, a multiple of VEC so
+    // every block's slice of L starts 16-byte aligned when L does
     int64_t rpb = (kTargetElemsPerBlock + s.R - 1) / s.R;
     rpb = (rpb + VEC - 1) / VEC * VEC;
     if (rpb > kMaxRowsPerBlock) rpb = kMaxRowsPerBlock;
     p.rows_per_block = (int32_t)rpb;
-    const int64_t nblocks = (p.rows + rpb - 1) / rpb;
-    p.nblocks = (uint32_t)nblocks;
-
-    const bool vec_runs = (s.R % VEC == 0) && ((s.s_w * s.i_c) % VEC == 0) &&
-                          ((s.i_w * s.i_c) % VEC == 0) && aligned16(I) && aligned16(L);
-    if (vec_runs) {
-        p.divR = FastDiv((uint32_t)(s.R / VEC));
-        hipLaunchKernelGGL(lower_vec_kernel<E>, dim3(p.nblocks), dim3(kThreads), 0, stream, p);
-    } else {
-        p.divR = FastDiv((uint32_t)s.R);
-        if (aligned16(L))
-            hipLaunchKernelGGL((lower_gather_kernel<E, true>), dim3(p.nblocks), dim3(kThreads), 0,
-                               stream, p);
-        else
-            hipLaunchKernelGGL((lower_gather_kernel<E, false>), dim3(p.nblocks), dim3(kThreads), 0,
-                               stream, p);
-    }
+    p.nblocks = (uint32_t)((p.rows + rpb - 1) / rpb);
+    p.divR = FastDiv((uint32_t)s.R);
+    if (aligned16(L))
+        hipLaunchKernelGGL((lower_gather_kernel<E, true>), dim3(p.nblocks), dim3(kGatherThreads),
+                           0, stream, p);
+    else
+        hipLaunchKernelGGL((lower_gather_kernel<E, false>), dim3(p.nblocks), dim3(kGatherThreads),
+                           0, stream, p);
     return hipGetLastError();
+}
+
+template <typename E>
+hipError_t launch_typed(const Shape& s, const void* I, void* L, hipStream_t stream) {
+    constexpr int VEC = Vec16<E>::N;
+    const int64_t row_bytes = s.i_w * s.i_c * (int64_t)sizeof(E);
+    const bool vec_runs = s.R % VEC == 0 && (s.s_w * s.i_c) % VEC == 0 &&
+                          (s.i_w * s.i_c) % VEC == 0 && aligned16(I) && aligned16(L);
+    // 32-bit indices inside the row-based kernels
+    const bool small = s.i_n * s.i_h < (int64_t(1) << 31) && s.i_h * s.R < (int64_t(1) << 31) &&
+                       s.o_w * (s.R / VEC + 2) < (int64_t(1) << 31);
+    if (small && vec_runs && row_bytes <= kRowsLdsLimit) return launch_rows<E>(s, I, L, stream);
+    if (small && row_bytes <= kStripLdsLimit) return launch_strip<E>(s, I, L, stream);
+    return launch_gather<E>(s, I, L, stream);
 }
 
 }  // namespace

@@ -65,6 +65,8 @@ SWEEP = [
     (4, 8, 8, 8, 1, 1, 16, 1, 1),        # 1x1
     (1, 3, 70, 2, 3, 1, 1, 1, 1),        # o_h = 1, many pairs
     (33, 4, 4, 4, 2, 2, 33, 1, 1),       # pairs = 99
+    (1, 5, 200, 64, 3, 3, 8, 1, 1),      # input rows wider than the lowering's LDS stage
+    (2, 6, 130, 33, 3, 2, 5, 1, 3),      # wide odd rows
 ]
 
 SWEEP_BF16 = [
@@ -74,6 +76,7 @@ SWEEP_BF16 = [
     (2, 31, 30, 3, 11, 11, 64, 4, 4),    # bf16 tall -> HT=1
     (1, 12, 12, 8, 5, 3, 130, 2, 1),
     (2, 6, 5, 7, 6, 5, 3, 1, 1),
+    (1, 4, 400, 64, 3, 3, 16, 1, 1),     # wide rows (gather lowering)
 ]
 
 
