@@ -38,8 +38,13 @@ def parse():
     ap.add_argument("--layer", default=DEFAULT_LAYER)
     ap.add_argument("--algo", default="lowered", choices=["lowered", "fused"])
     ap.add_argument("--sets", type=int, default=4, help="rotating buffer sets")
+    ap.add_argument("--batch", type=int, default=0,
+                    help="override the layer's batch size i_n (0 keeps the layer's own)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="approximate CPU time for the oracle baseline (0 skips it)")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="after timing, run one plain device-to-device copy of this many MiB "
+                         "(a known-size reference for rocprofv3 byte counters)")
     ap.add_argument("--traffic", default=None,
                     help="JSON file with per-launch HBM bytes of the slab-product kernel "
                          "from rocprofv3 counters")
@@ -65,6 +70,9 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     layer = wl.LAYERS[args.layer]
+    if args.batch > 0:
+        import dataclasses
+        layer = dataclasses.replace(layer, i_n=args.batch)
     dims = layer.dims
     i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w = dims
     o_h, o_w = mec.output_dims(i_h, i_w, k_h, k_w, s_h, s_w)
@@ -200,6 +208,19 @@ def main():
                                  "peak": PEAK_HBM_GBS, "unit": "GB/s",
                                  "frac": round(lbytes / (lavg * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
                                  "alg_bytes": lbytes}
+    if args.copy_mib > 0:
+        # A plain copy of known size through the library's own row-copy
+        # kernel: with i_w = k_w = 1 the lowering is L = I element for element.
+        rows = args.copy_mib * (1 << 20) // 4096
+        src = torch.ones((1, rows, 1, 1024), dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        mec.lower(src, 1, 1, 1, 1, 1, L=dst, stream=stream)
+        torch.cuda.synchronize()
+        if not torch.equal(src, dst):
+            raise RuntimeError("reference copy mismatch")
+        out["copy_reference_bytes"] = {"read": src.numel() * 4, "write": dst.numel() * 4}
+        del src, dst
     out["cpu_baseline"] = cpu_baseline(layer, I0, K0, macs, args.cpu_seconds)
     print(json.dumps(out), flush=True)
 

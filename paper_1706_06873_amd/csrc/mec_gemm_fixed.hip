@@ -6,42 +6,16 @@
 // known the reduction over the kernel rows is fully unrolled: each wave loads
 // every staged row fragment it needs once per MFMA k-step and feeds it to all
 // (h, a) pairs with h*s_h + a equal to that row, so the slab overlap is reused
-// in registers as well as in LDS. Staging offsets are computed once per tile.
+// in registers as well as in LDS. Staging offsets are computed once per tile,
+// relative to the tile's first pair so they fit 32-bit registers; the next
+// r-chunk's global loads are issued after the first MFMA k-step of the current
+// one, and their LDS stores go to the other of two stage buffers.
+#include <type_traits>
+
 #include "mec_mfma.h"
 
 namespace mec {
 namespace {
-
-template <class Tr, int HT, int NB, int WAVES_H, int KT, int KH, int SH, int VA, int VB,
-          bool FUSED>
-struct FCfg {
-    using T = Tr;
-    using E = typename Tr::E;
-    static constexpr int kHT = HT, kKT = KT, kKH = KH, kSH = SH, kVA = VA, kVB = VB;
-    static constexpr bool kFused = FUSED;
-    static constexpr int NT = 32 * NB;
-    static constexpr int WAVES_N = 4 / WAVES_H;
-    static constexpr int HW = HT / WAVES_H;    // output rows per wave
-    static constexpr int NBW = NB / WAVES_N;   // 32-channel blocks per wave
-    static constexpr int HROWS = (HT - 1) * SH + KH;  // staged input rows per tile
-    static constexpr int XW = (HW - 1) * SH + KH;     // staged rows one wave reads
-    static constexpr bool kF32 = sizeof(E) == 4;
-    // LDS strides: fp32 fragments are single dwords, so odd strides put the 32
-    // rows of a fragment in 32 different banks; bf16 fragments are 16-byte
-    // reads, so strides stay multiples of 8 elements and are offset by 16 bytes.
-    static constexpr int PS = kF32 ? ((HROWS * KT) | 1) : HROWS * KT + 8;
-    static constexpr int KTB = kF32 ? (KT | 1) : KT + 8;
-    static constexpr int A_ELEMS = kPairs * PS;
-    static constexpr int STAGE = (A_ELEMS + KH * NT * KTB + 7) / 8 * 8;
-    static constexpr int A_VECS = kPairs * HROWS * KT / VA;
-    static constexpr int AJ = (A_VECS + kThreads - 1) / kThreads;
-    static constexpr int B_VECS = KH * NT * KT / VB;
-    static constexpr int BJ = (B_VECS + kThreads - 1) / kThreads;
-    static constexpr size_t LDS_BYTES = 2 * STAGE * sizeof(E);
-    static_assert(4 % WAVES_H == 0 && HT % WAVES_H == 0 && NB % WAVES_N == 0, "wave split");
-    static_assert(KT % Tr::KS == 0 && KT % VA == 0 && NT % VB == 0, "chunk");
-    static_assert(LDS_BYTES + 512 <= 160 * 1024, "LDS");
-};
 
 struct FixedParams {
     const void* A;     // L (lowered) or I (fused)
@@ -53,22 +27,57 @@ struct FixedParams {
     uint32_t ntiles;
 };
 
-template <class C>
-__global__ __launch_bounds__(kThreads) void slab_gemm_fixed_kernel(FixedParams p) {
-    using Tr = typename C::T;
-    using E = typename C::E;
-    using Frag = typename Tr::Frag;
-    constexpr int KT = C::kKT, NT = C::NT, HW = C::HW, NBW = C::NBW, VA = C::kVA, VB = C::kVB;
-    constexpr int KH = C::kKH, SH = C::kSH, HROWS = C::HROWS, XW = C::XW;
-    constexpr int PS = C::PS, KTB = C::KTB, STAGE = C::STAGE, A_ELEMS = C::A_ELEMS;
-    constexpr int AJ = C::AJ, BJ = C::BJ;
+// ---------------------------------------------------------------- fp32 kernel
+// The fp32 variant lays both stages out so that MFMA fragment reads are
+// consecutive across lanes (conflict-free) and stage writes are 16-byte:
+//   A stage [x][r][pair]   (the 32 pairs innermost: lane l of a fragment
+//                           reads pair l % 32)
+//   B stage [a][r][channel]
+// Each thread loads 4 pairs x VA consecutive r (global reads keep their runs
+// along r) and transposes them in registers into VA 16-byte LDS writes of 4
+// consecutive pairs.
+template <int HT, int NB, int WAVES_H, int KT, int KH, int SH, int VA, int VB, bool FUSED,
+          int WAVES = 4>
+struct F32Cfg {
+    using T = TraitsF32;
+    using E = uint32_t;
+    static constexpr int kHT = HT, kKT = KT, kKH = KH, kSH = SH, kVA = VA, kVB = VB;
+    static constexpr bool kFused = FUSED;
+    static constexpr int NT = 32 * NB;
+    static constexpr int kWaves = WAVES;
+    static constexpr int THREADS = 64 * WAVES;
+    static constexpr int WAVES_N = WAVES / WAVES_H;
+    static constexpr int HW = HT / WAVES_H;
+    static constexpr int NBW = NB / WAVES_N;
+    static constexpr int HROWS = (HT - 1) * SH + KH;
+    static constexpr int XW = (HW - 1) * SH + KH;
+    static constexpr int A_SIZE = HROWS * KT * kPairs;
+    static constexpr int B_SIZE = KH * KT * NT;
+    static constexpr int STAGE = A_SIZE + B_SIZE;
+    static constexpr int RG = KT / VA;                  // r-groups per staged row
+    static constexpr int A_ITEMS = HROWS * RG * 8;      // (x, r-group, 4-pair group)
+    static constexpr int AJ = (A_ITEMS + THREADS - 1) / THREADS;
+    static constexpr int NG = NT / 4;                   // 4-channel groups
+    static constexpr int B_ITEMS = KH * KT * NG;        // (a, r, 4-channel group)
+    static constexpr int BJ = (B_ITEMS + THREADS - 1) / THREADS;
+    static constexpr size_t LDS_BYTES = 2 * STAGE * sizeof(E);
+    static_assert(WAVES % WAVES_H == 0 && HT % WAVES_H == 0 && NB % WAVES_N == 0, "wave split");
+    static_assert(KT % 2 == 0 && KT % VA == 0 && (VB == 1 || VB == 4), "chunk");
+    static_assert(LDS_BYTES + 1024 <= 160 * 1024, "LDS");
+};
 
-    __shared__ __align__(16) E lds[2 * STAGE];
-    __shared__ int64_t abase_s[kPairs];  // source element of (pair, row 0), or -1
-    __shared__ int64_t obase_s[kPairs];  // O element of (n, 0, w, 0), or -1
+template <class C>
+__global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_kernel(FixedParams p) {
+    constexpr int KT = C::kKT, NT = C::NT, HW = C::HW, NBW = C::NBW, VA = C::kVA, VB = C::kVB;
+    constexpr int KH = C::kKH, SH = C::kSH, HROWS = C::HROWS, XW = C::XW, RG = C::RG, NG = C::NG;
+    constexpr int A_SIZE = C::A_SIZE, STAGE = C::STAGE, AJ = C::AJ, BJ = C::BJ;
+
+    __shared__ __align__(16) uint32_t lds[2 * STAGE];
+    __shared__ int64_t abase_s[kPairs];
+    __shared__ int64_t obase_s[kPairs];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wh = wave % (4 / C::WAVES_N), wn = wave / (4 / C::WAVES_N);
+    const int wh = wave % (C::kWaves / C::WAVES_N), wn = wave / (C::kWaves / C::WAVES_N);
 
     const uint32_t t = xcd_remap(blockIdx.x, p.ntiles);
     const int n_tile = (int)(t % (uint32_t)p.n_tiles);
@@ -92,72 +101,380 @@ __global__ __launch_bounds__(kThreads) void slab_gemm_fixed_kernel(FixedParams p
     }
     __syncthreads();
 
-    // Per-thread staging entries, fixed for the whole tile. A entry j covers VA
-    // consecutive r of (pair pp, staged row x); B entry j covers VB consecutive
-    // channels of (kernel row a, r). g: element offset from the tile's source
-    // base (or from K) at r-chunk 0, -1 when the entry stages zeros; l: LDS
-    // offset | r << 24, -1 when the entry does not exist.
-    const int64_t abase0 = abase_s[0];
-    const E* __restrict__ Atile = reinterpret_cast<const E*>(p.A) + abase0;
-    const E* __restrict__ Kg = reinterpret_cast<const E*>(p.K);
-    int ag[AJ], al[AJ], bg[BJ], bl[BJ];
+    // The tile's source base, computed from uniform values so it stays in
+    // scalar registers and every staging load is base + 32-bit offset.
+    int64_t abase0;
+    {
+        const int64_t n_first = pair0 / p.o_w, w_first = pair0 % p.o_w;
+        abase0 = C::kFused ? ((n_first * p.i_h) * p.i_w + p.s_w * w_first) * p.i_c : pair0 * p.i_h * p.R;
+    }
+    const uint32_t* __restrict__ Atile = reinterpret_cast<const uint32_t*>(p.A) + abase0;
+    const uint32_t* __restrict__ Kg = reinterpret_cast<const uint32_t*>(p.K);
+    // An interior tile (all pairs, staged rows, r-chunks and channels in range)
+    // stages without any predication.
+    const bool full = pair0 + kPairs <= p.pairs && x0 + HROWS <= p.i_h && p.R % KT == 0 &&
+                      n0 + NT <= p.k_c && (VB == 4 || p.k_c % 4 == 0);
+
+    // staging entries, fixed for the tile: element offsets at r-chunk 0 (-1 =
+    // stage zeros), LDS offsets (-1 = no such entry) and the entry's first r
+    uint32_t ag[AJ][4];
+    int al[AJ], ar[AJ];
 #pragma unroll
     for (int j = 0; j < AJ; ++j) {
-        const int e = (tid + j * kThreads) * VA;
-        ag[j] = -1;
+        const int it = tid + j * C::THREADS;
         al[j] = -1;
-        if (e < kPairs * HROWS * KT) {
-            const int r = e % KT, pr = e / KT;
-            const int pp = pr / HROWS, x = pr - pp * HROWS;
-            al[j] = (pp * PS + x * KT + r) | (r << 24);
-            const int64_t ab = abase_s[pp];
-            if (ab >= 0 && x0 + x < p.i_h) ag[j] = (int)(ab - abase0 + (x0 + x) * p.a_xstride + r);
+        ar[j] = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) ag[j][q] = 0xffffffffu;
+        if (it < C::A_ITEMS) {
+            const int pg = it % 8, t2 = it / 8;
+            const int rg = t2 % RG, x = t2 / RG;
+            al[j] = (x * KT + rg * VA) * kPairs + 4 * pg;
+            ar[j] = rg * VA;
+            if (x0 + x < p.i_h) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int64_t ab = abase_s[4 * pg + q];
+                    if (ab >= 0) ag[j][q] = (uint32_t)(ab - abase0 + (x0 + x) * p.a_xstride + rg * VA);
+                }
+            }
         }
     }
+    uint32_t bg[BJ];
+    int bl[BJ], br[BJ], bn[BJ];
 #pragma unroll
     for (int j = 0; j < BJ; ++j) {
-        const int e = (tid + j * kThreads) * VB;
-        bg[j] = -1;
+        const int it = tid + j * C::THREADS;
+        bg[j] = 0xffffffffu;
         bl[j] = -1;
-        if (e < KH * NT * KT) {
-            const int n = e % NT, ar = e / NT;
-            const int r = ar % KT, a = ar / KT;
-            bl[j] = ((a * NT + n) * KTB + r) | (r << 24);
-            if (n0 + n < p.k_c) bg[j] = (int)(((int64_t)a * p.R + r) * p.k_c + n0 + n);
+        br[j] = 0;
+        bn[j] = 0;
+        if (it < C::B_ITEMS) {
+            const int ng = it % NG, t2 = it / NG;
+            const int r = t2 % KT, a = t2 / KT;
+            bl[j] = A_SIZE + (a * KT + r) * NT + 4 * ng;
+            br[j] = r;
+            const int64_t c0 = n0 + 4 * ng;
+            bn[j] = (int)(p.k_c - c0 < 4 ? (p.k_c - c0 > 0 ? p.k_c - c0 : 0) : 4);  // valid channels
+            if (bn[j] > 0) bg[j] = (uint32_t)(((int64_t)a * p.R + r) * p.k_c + c0);
         }
     }
+    const uint32_t kstep = (uint32_t)(KT * p.k_c);  // K elements per r-chunk
 
-    VecN<VA, E> areg[AJ];
-    VecN<VB, E> breg[BJ];
-    auto load_stage = [&](int rc) {
-        const int r0 = rc * KT;
+    VecN<VA, uint32_t> areg[AJ][4];
+    VecN<4, uint32_t> breg[BJ];
+    // global -> registers for r-chunk rc; FULL: no entry needs predication
+    auto load_stage = [&](int rc, auto full_tag) {
+        constexpr bool FULL = decltype(full_tag)::value;
+        const uint32_t r0 = (uint32_t)(rc * KT);
 #pragma unroll
         for (int j = 0; j < AJ; ++j) {
-            areg[j].zero();
-            if (ag[j] >= 0 && r0 + (al[j] >> 24) < p.R) areg[j].load(Atile + ag[j] + r0);
-        }
+            if (FULL && (j + 1) * C::THREADS <= C::A_ITEMS) {
 #pragma unroll
-        for (int j = 0; j < BJ; ++j) {
-            breg[j].zero();
-            if (bg[j] >= 0 && r0 + (bl[j] >> 24) < p.R) breg[j].load(Kg + bg[j] + (int64_t)r0 * p.k_c);
-        }
-    };
-    auto store_stage = [&](int buf) {
-        E* st = lds + buf * STAGE;
+                for (int q = 0; q < 4; ++q) areg[j][q].load(Atile + (ag[j][q] + r0));
+            } else {
+                const bool rok = (int64_t)r0 + ar[j] < p.R;
 #pragma unroll
-        for (int j = 0; j < AJ; ++j) {
-            if (al[j] >= 0) {
-                E* d = st + (al[j] & 0xffffff);
-#pragma unroll
-                for (int k = 0; k < VA; ++k) d[k] = areg[j].e[k];
+                for (int q = 0; q < 4; ++q) {
+                    areg[j][q].zero();
+                    if (rok && ag[j][q] != 0xffffffffu) areg[j][q].load(Atile + (ag[j][q] + r0));
+                }
             }
         }
 #pragma unroll
         for (int j = 0; j < BJ; ++j) {
-            if (bl[j] >= 0) {
-                E* d = st + A_ELEMS + (bl[j] & 0xffffff);
+            const uint32_t off = bg[j] + (uint32_t)rc * kstep;
+            if (FULL && VB == 4 && (j + 1) * C::THREADS <= C::B_ITEMS) {
+                breg[j].load(Kg + off);
+            } else {
+                breg[j].zero();
+                if (bg[j] != 0xffffffffu && (int64_t)r0 + br[j] < p.R) {
+                    if (VB == 4) {
+                        breg[j].load(Kg + off);
+                    } else {
 #pragma unroll
-                for (int k = 0; k < VB; ++k) d[k * KTB] = breg[j].e[k];
+                        for (int k = 0; k < 4; ++k)
+                            if (k < bn[j]) breg[j].e[k] = Kg[off + k];
+                    }
+                }
+            }
+        }
+    };
+    auto store_stage = [&](int buf) {
+        uint32_t* st = lds + buf * STAGE;
+#pragma unroll
+        for (int j = 0; j < AJ; ++j) {
+            if ((j + 1) * C::THREADS <= C::A_ITEMS || al[j] >= 0) {
+#pragma unroll
+                for (int k = 0; k < VA; ++k) {
+                    uint4 v;
+                    v.x = areg[j][0].e[k];
+                    v.y = areg[j][1].e[k];
+                    v.z = areg[j][2].e[k];
+                    v.w = areg[j][3].e[k];
+                    *reinterpret_cast<uint4*>(st + al[j] + k * kPairs) = v;
+                }
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < BJ; ++j)
+            if ((j + 1) * C::THREADS <= C::B_ITEMS || bl[j] >= 0)
+                *reinterpret_cast<uint4*>(st + bl[j]) =
+                    make_uint4(breg[j].e[0], breg[j].e[1], breg[j].e[2], breg[j].e[3]);
+    };
+
+    floatx16 acc[HW][NBW];
+#pragma unroll
+    for (int i = 0; i < HW; ++i)
+#pragma unroll
+        for (int j = 0; j < NBW; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+    const int row = lane & 31;
+    const int kofs = lane >> 5;
+    const int a_lane = (wh * HW * SH) * KT * kPairs + kofs * kPairs + row;
+    const int b_lane = A_SIZE + kofs * NT + (wn * NBW) * 32 + row;
+
+    // The MFMAs of one r-chunk; `mid` runs after the first k-step's MFMAs are
+    // issued, so the next chunk's global loads overlap the matrix pipe.
+    auto compute = [&](int buf, auto mid) {
+        const uint32_t* As = lds + buf * STAGE + a_lane;
+        const uint32_t* Bs = lds + buf * STAGE + b_lane;
+#pragma unroll
+        for (int kk = 0; kk < KT; kk += 2) {
+            float af[XW];
+            float bf[KH][NBW];
+#pragma unroll
+            for (int i = 0; i < XW; ++i) af[i] = __builtin_bit_cast(float, As[(i * KT + kk) * kPairs]);
+#pragma unroll
+            for (int a = 0; a < KH; ++a)
+#pragma unroll
+                for (int nb = 0; nb < NBW; ++nb)
+                    bf[a][nb] = __builtin_bit_cast(float, Bs[(a * KT + kk) * NT + nb * 32]);
+#pragma unroll
+            for (int a = 0; a < KH; ++a)
+#pragma unroll
+                for (int hw = 0; hw < HW; ++hw)
+#pragma unroll
+                    for (int nb = 0; nb < NBW; ++nb)
+                        acc[hw][nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[hw * SH + a], bf[a][nb],
+                                                                         acc[hw][nb], 0, 0, 0);
+            if (kk == 0) mid();
+        }
+    };
+
+    auto main_loop = [&](auto full_tag) {
+        load_stage(0, full_tag);
+        store_stage(0);
+        __syncthreads();
+        for (int rc = 0; rc < p.nchunks; ++rc) {
+            const bool more = rc + 1 < p.nchunks;
+            compute(rc & 1, [&] {
+                if (more) load_stage(rc + 1, full_tag);
+            });
+            if (more) store_stage((rc + 1) & 1);
+            __syncthreads();
+        }
+    };
+    if (full)
+        main_loop(std::true_type{});
+    else
+        main_loop(std::false_type{});
+
+    const int64_t ostride_h = p.o_w * p.k_c;
+#pragma unroll
+    for (int hw = 0; hw < HW; ++hw) {
+        const int64_t h = h0 + wh * HW + hw;
+        if (h >= p.o_h) continue;
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb) {
+            const int c = n0 + (wn * NBW + nb) * 32 + row;
+            if (c >= p.k_c) continue;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int64_t ob = obase_s[acc_row(v, lane)];
+                if (ob >= 0) p.O[ob + h * ostride_h + c] = acc[hw][nb][v];
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------- bf16 kernel
+// bf16 fragments hold 8 consecutive k per lane (v_mfma_f32_32x32x16_bf16), so
+// both stages keep r innermost, rows padded by 8 elements (16 bytes):
+//   A stage [x][pair][KT + 8]   filled by 16-byte loads and 16-byte LDS stores
+//   B stage [a][channel][KT + 8] K is channel-contiguous in memory, so each
+//        thread loads an 8 (r) x 8 (channel) block with eight 16-byte loads and
+//        transposes it in registers into eight 16-byte LDS stores.
+// The padding puts the 8 rows of each 128-byte LDS access phase in distinct banks.
+template <int HT, int NB, int WAVES_H, int KT, int KH, int SH, bool FUSED, int WAVES = 4>
+struct BF16Cfg {
+    using T = TraitsBF16;
+    using E = uint16_t;
+    static constexpr int kHT = HT, kKT = KT, kKH = KH, kSH = SH, kVA = 8, kVB = 8;
+    static constexpr bool kFused = FUSED;
+    static constexpr int kWaves = WAVES;
+    static constexpr int NT = 32 * NB;
+    static constexpr int THREADS = 64 * WAVES;
+    static constexpr int WAVES_N = WAVES / WAVES_H;
+    static constexpr int HW = HT / WAVES_H;
+    static constexpr int NBW = NB / WAVES_N;
+    static constexpr int HROWS = (HT - 1) * SH + KH;
+    static constexpr int XW = (HW - 1) * SH + KH;
+    static constexpr int KTP = KT + 8;                      // padded row (elements)
+    static constexpr int A_SIZE = HROWS * kPairs * KTP;
+    static constexpr int B_SIZE = KH * NT * KTP;
+    static constexpr int STAGE = A_SIZE + B_SIZE;
+    static constexpr int RG = KT / 8;
+    static constexpr int A_ITEMS = HROWS * kPairs * RG;     // (x, pair, 8-r group)
+    static constexpr int AJ = (A_ITEMS + THREADS - 1) / THREADS;
+    static constexpr int B_ITEMS = KH * RG * (NT / 8);      // (a, 8-r group, 8-channel group)
+    static constexpr int BJ = (B_ITEMS + THREADS - 1) / THREADS;
+    static constexpr size_t LDS_BYTES = 2 * STAGE * sizeof(E);
+    static_assert(WAVES % WAVES_H == 0 && HT % WAVES_H == 0 && NB % WAVES_N == 0, "wave split");
+    static_assert(KT % 16 == 0, "chunk");
+    static_assert(LDS_BYTES + 1024 <= 160 * 1024, "LDS");
+};
+
+// Transpose an 8x8 block of 16-bit values: in[i] holds row i (8 values),
+// out[j] receives column j.
+__device__ inline void transpose8x8_b16(const uint4 (&in)[8], uint4 (&out)[8]) {
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+        uint32_t d[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const uint32_t* r0 = reinterpret_cast<const uint32_t*>(&in[2 * j]);
+            const uint32_t* r1 = reinterpret_cast<const uint32_t*>(&in[2 * j + 1]);
+            const uint32_t a = r0[c >> 1], b = r1[c >> 1];
+            d[j] = (c & 1) ? ((a >> 16) | (b & 0xffff0000u)) : ((a & 0xffffu) | (b << 16));
+        }
+        out[c] = make_uint4(d[0], d[1], d[2], d[3]);
+    }
+}
+
+template <class C>
+__global__ __launch_bounds__(C::THREADS) void slab_gemm_bf16_kernel(FixedParams p) {
+    constexpr int KT = C::kKT, NT = C::NT, HW = C::HW, NBW = C::NBW, KTP = C::KTP;
+    constexpr int KH = C::kKH, SH = C::kSH, HROWS = C::HROWS, XW = C::XW, RG = C::RG;
+    constexpr int A_SIZE = C::A_SIZE, STAGE = C::STAGE, AJ = C::AJ, BJ = C::BJ;
+
+    __shared__ __align__(16) uint16_t lds[2 * STAGE];
+    __shared__ int64_t abase_s[kPairs];
+    __shared__ int64_t obase_s[kPairs];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wh = wave % (C::kWaves / C::WAVES_N), wn = wave / (C::kWaves / C::WAVES_N);
+
+    const uint32_t t = xcd_remap(blockIdx.x, p.ntiles);
+    const int n_tile = (int)(t % (uint32_t)p.n_tiles);
+    const uint32_t rest = t / (uint32_t)p.n_tiles;
+    const int h_tile = (int)(rest % (uint32_t)p.h_tiles);
+    const int64_t pair0 = (int64_t)(rest / (uint32_t)p.h_tiles) * kPairs;
+    const int64_t h0 = (int64_t)h_tile * C::kHT;
+    const int64_t x0 = h0 * SH;
+    const int n0 = n_tile * NT;
+
+    if (tid < kPairs) {
+        const int64_t pair = pair0 + tid;
+        if (pair < p.pairs) {
+            const int64_t n = pair / p.o_w, w = pair % p.o_w;
+            abase_s[tid] = C::kFused ? ((n * p.i_h) * p.i_w + p.s_w * w) * p.i_c : pair * p.i_h * p.R;
+            obase_s[tid] = (n * p.o_h * p.o_w + w) * p.k_c;
+        } else {
+            abase_s[tid] = -1;
+            obase_s[tid] = -1;
+        }
+    }
+    __syncthreads();
+
+    int64_t abase0;
+    {
+        const int64_t n_first = pair0 / p.o_w, w_first = pair0 % p.o_w;
+        abase0 = C::kFused ? ((n_first * p.i_h) * p.i_w + p.s_w * w_first) * p.i_c : pair0 * p.i_h * p.R;
+    }
+    const uint16_t* __restrict__ Atile = reinterpret_cast<const uint16_t*>(p.A) + abase0;
+    const uint16_t* __restrict__ Kg = reinterpret_cast<const uint16_t*>(p.K);
+    const bool full = pair0 + kPairs <= p.pairs && x0 + HROWS <= p.i_h && p.R % KT == 0 &&
+                      n0 + NT <= p.k_c;
+
+    // A entries: one 16-byte piece (8 consecutive r) of (x, pair)
+    uint32_t ag[AJ];
+    int al[AJ], ar[AJ];
+#pragma unroll
+    for (int j = 0; j < AJ; ++j) {
+        const int it = tid + j * C::THREADS;
+        ag[j] = 0xffffffffu;
+        al[j] = -1;
+        ar[j] = 0;
+        if (it < C::A_ITEMS) {
+            const int rg = it % RG, t2 = it / RG;
+            const int pp = t2 % kPairs, x = t2 / kPairs;
+            al[j] = (x * kPairs + pp) * KTP + rg * 8;
+            ar[j] = rg * 8;
+            const int64_t ab = abase_s[pp];
+            if (ab >= 0 && x0 + x < p.i_h) ag[j] = (uint32_t)(ab - abase0 + (x0 + x) * p.a_xstride + rg * 8);
+        }
+    }
+    // B entries: an 8 (r) x 8 (channel) block of K for kernel row a
+    uint32_t bg[BJ];
+    int bl[BJ], br[BJ];
+#pragma unroll
+    for (int j = 0; j < BJ; ++j) {
+        const int it = tid + j * C::THREADS;
+        bg[j] = 0xffffffffu;
+        bl[j] = -1;
+        br[j] = 0;
+        if (it < C::B_ITEMS) {
+            const int rg = it % RG, t2 = it / RG;
+            const int cg = t2 % (NT / 8), a = t2 / (NT / 8);
+            bl[j] = (a * NT + cg * 8) * KTP + rg * 8;
+            br[j] = rg * 8;
+            if (n0 + cg * 8 < p.k_c) bg[j] = (uint32_t)(((int64_t)a * p.R + rg * 8) * p.k_c + n0 + cg * 8);
+        }
+    }
+    const uint32_t kstep = (uint32_t)(KT * p.k_c);
+    const uint32_t krow = (uint32_t)p.k_c;
+
+    uint4 areg[AJ];
+    uint4 breg[BJ][8];
+    auto load_stage = [&](int rc, auto full_tag) {
+        constexpr bool FULL = decltype(full_tag)::value;
+        const uint32_t r0 = (uint32_t)(rc * KT);
+#pragma unroll
+        for (int j = 0; j < AJ; ++j) {
+            if (FULL && (j + 1) * C::THREADS <= C::A_ITEMS) {
+                areg[j] = *reinterpret_cast<const uint4*>(Atile + (ag[j] + r0));
+            } else {
+                areg[j] = make_uint4(0, 0, 0, 0);
+                if (ag[j] != 0xffffffffu && (int64_t)r0 + ar[j] < p.R)
+                    areg[j] = *reinterpret_cast<const uint4*>(Atile + (ag[j] + r0));
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < BJ; ++j) {
+            const uint32_t off = bg[j] + (uint32_t)rc * kstep;
+            const bool ok = (FULL && (j + 1) * C::THREADS <= C::B_ITEMS) ||
+                            (bg[j] != 0xffffffffu && (int64_t)r0 + br[j] < p.R);
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                breg[j][i] = ok ? *reinterpret_cast<const uint4*>(Kg + (off + i * krow)) : make_uint4(0, 0, 0, 0);
+        }
+    };
+    auto store_stage = [&](int buf) {
+        uint16_t* st = lds + buf * STAGE;
+#pragma unroll
+        for (int j = 0; j < AJ; ++j)
+            if ((j + 1) * C::THREADS <= C::A_ITEMS || al[j] >= 0)
+                *reinterpret_cast<uint4*>(st + al[j]) = areg[j];
+#pragma unroll
+        for (int j = 0; j < BJ; ++j) {
+            if ((j + 1) * C::THREADS <= C::B_ITEMS || bl[j] >= 0) {
+                uint4 col[8];
+                transpose8x8_b16(breg[j], col);
+#pragma unroll
+                for (int c = 0; c < 8; ++c) *reinterpret_cast<uint4*>(st + A_SIZE + bl[j] + c * KTP) = col[c];
             }
         }
     };
@@ -171,45 +488,55 @@ __global__ __launch_bounds__(kThreads) void slab_gemm_fixed_kernel(FixedParams p
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
     const int row = lane & 31;
-    const int kofs = (lane >> 5) * Tr::KL;
-    // this wave's first staged row is wh*HW*SH; its fragments cover XW rows
-    const int a_lane = row * PS + (wh * HW * SH) * KT + kofs;
-    const int b_lane = A_ELEMS + ((wn * NBW) * 32 + row) * KTB + kofs;
+    const int kofs = (lane >> 5) * 8;
+    const int a_lane = ((wh * HW * SH) * kPairs + row) * KTP + kofs;
+    const int b_lane = A_SIZE + ((wn * NBW) * 32 + row) * KTP + kofs;
 
-    auto compute = [&](int buf) {
-        const E* As = lds + buf * STAGE + a_lane;
-        const E* Bs = lds + buf * STAGE + b_lane;
+    auto compute = [&](int buf, auto mid) {
+        const uint16_t* As = lds + buf * STAGE + a_lane;
+        const uint16_t* Bs = lds + buf * STAGE + b_lane;
 #pragma unroll
-        for (int kk = 0; kk < KT; kk += Tr::KS) {
-            Frag af[XW];
-            Frag bf[KH][NBW];
+        for (int kk = 0; kk < KT; kk += 16) {
+            bf16x8 af[XW];
+            bf16x8 bf[KH][NBW];
 #pragma unroll
-            for (int i = 0; i < XW; ++i) af[i] = Tr::frag(As + i * KT + kk);
+            for (int i = 0; i < XW; ++i)
+                af[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(As + i * kPairs * KTP + kk));
 #pragma unroll
             for (int a = 0; a < KH; ++a)
 #pragma unroll
-                for (int nb = 0; nb < NBW; ++nb) bf[a][nb] = Tr::frag(Bs + (a * NT + nb * 32) * KTB + kk);
-            // kernel row outermost: consecutive MFMAs update different accumulators
+                for (int nb = 0; nb < NBW; ++nb)
+                    bf[a][nb] = __builtin_bit_cast(
+                        bf16x8, *reinterpret_cast<const uint4*>(Bs + (a * NT + nb * 32) * KTP + kk));
 #pragma unroll
             for (int a = 0; a < KH; ++a)
 #pragma unroll
                 for (int hw = 0; hw < HW; ++hw)
 #pragma unroll
                     for (int nb = 0; nb < NBW; ++nb)
-                        acc[hw][nb] = Tr::mfma(af[hw * SH + a], bf[a][nb], acc[hw][nb]);
+                        acc[hw][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[hw * SH + a], bf[a][nb],
+                                                                           acc[hw][nb], 0, 0, 0);
+            if (kk == 0) mid();
         }
     };
 
-    load_stage(0);
-    store_stage(0);
-    __syncthreads();
-    for (int rc = 0; rc < p.nchunks; ++rc) {
-        const bool more = rc + 1 < p.nchunks;
-        if (more) load_stage(rc + 1);  // global loads in flight during the MFMAs
-        compute(rc & 1);
-        if (more) store_stage((rc + 1) & 1);
+    auto main_loop = [&](auto full_tag) {
+        load_stage(0, full_tag);
+        store_stage(0);
         __syncthreads();
-    }
+        for (int rc = 0; rc < p.nchunks; ++rc) {
+            const bool more = rc + 1 < p.nchunks;
+            compute(rc & 1, [&] {
+                if (more) load_stage(rc + 1, full_tag);
+            });
+            if (more) store_stage((rc + 1) & 1);
+            __syncthreads();
+        }
+    };
+    if (full)
+        main_loop(std::true_type{});
+    else
+        main_loop(std::false_type{});
 
     const int64_t ostride_h = p.o_w * p.k_c;
 #pragma unroll
@@ -234,7 +561,7 @@ inline bool aligned16(const void* ptr) { return ((uintptr_t)ptr & 15u) == 0; }
 // Offsets staged through 32-bit registers must fit: the source span of one
 // tile's 32 pairs, and K.
 bool offsets_fit(const Shape& s, bool fused) {
-    const int64_t lim = int64_t(1) << 31;
+    const int64_t lim = int64_t(1) << 30;  // element offsets, as 32-bit byte offsets
     if (s.k_h * s.R * s.k_c >= lim) return false;
     if (!fused) return kPairs * s.i_h * s.R < lim;
     const int64_t images = (kPairs - 1) / s.o_w + 2;  // images 32 consecutive pairs can touch
@@ -258,6 +585,19 @@ bool usable(const Shape& s, const void* A, const void* K) {
 }
 
 template <class C>
+struct KernelOf;
+template <int HT, int NB, int WH, int KT, int KH, int SH, bool F, int W>
+struct KernelOf<BF16Cfg<HT, NB, WH, KT, KH, SH, F, W>> {
+    static constexpr auto fn = slab_gemm_bf16_kernel<BF16Cfg<HT, NB, WH, KT, KH, SH, F, W>>;
+    static constexpr int threads = 64 * W;
+};
+template <int HT, int NB, int WH, int KT, int KH, int SH, int VA, int VB, bool F, int W>
+struct KernelOf<F32Cfg<HT, NB, WH, KT, KH, SH, VA, VB, F, W>> {
+    static constexpr auto fn = slab_gemm_f32_kernel<F32Cfg<HT, NB, WH, KT, KH, SH, VA, VB, F, W>>;
+    static constexpr int threads = 64 * W;
+};
+
+template <class C>
 hipError_t run_fixed(const Shape& s, const void* A, const void* K, float* O, hipStream_t stream) {
     FixedParams p{};
     p.A = A;
@@ -273,19 +613,21 @@ hipError_t run_fixed(const Shape& s, const void* A, const void* K, float* O, hip
     const int64_t ntiles = pair_tiles * p.h_tiles * p.n_tiles;
     if (ntiles > 0x7fffffff) return hipErrorInvalidValue;
     p.ntiles = (uint32_t)ntiles;
-    hipLaunchKernelGGL(slab_gemm_fixed_kernel<C>, dim3(p.ntiles), dim3(kThreads), 0, stream, p);
+    hipLaunchKernelGGL(KernelOf<C>::fn, dim3(p.ntiles), dim3(KernelOf<C>::threads), 0, stream, p);
     return hipGetLastError();
 }
 
-// fp32, 3x3 stride 1, long rows (R % 4 == 0): 32 pairs x 8 rows x 64 channels,
+// fp32, 3x3 stride 1, long rows (R % 4 == 0): 32 pairs x 14 rows x 64 channels,
 // r-chunks of 16, 16-byte loads of L (or I) and K.
-template <bool F> using F32K3S1Wide = FCfg<TraitsF32, 8, 2, 4, 16, 3, 1, 4, 4, F>;
+template <bool F> using F32K3S1Wide = F32Cfg<14, 2, 2, 16, 3, 1, 4, 4, F>;
 // fp32, 3x3 stride 1, short rows (R = 3 i_c with i_c not a multiple of 4).
-template <bool F> using F32K3S1Narrow = FCfg<TraitsF32, 8, 2, 4, 2, 3, 1, 1, 1, F>;
-// fp32, 11x11 stride 4: 32 pairs x 8 rows x 96 channels, 39 staged rows.
-template <bool F> using F32K11S4 = FCfg<TraitsF32, 8, 3, 4, 2, 11, 4, 1, 1, F>;
-// bf16, 3x3 stride 1: 32 pairs x 14 rows x 128 channels, r-chunks of 32.
-template <bool F> using BF16K3S1 = FCfg<TraitsBF16, 14, 4, 2, 32, 3, 1, 8, 8, F>;
+template <bool F> using F32K3S1Narrow = F32Cfg<8, 2, 4, 2, 3, 1, 1, 1, F>;
+// fp32, 11x11 stride 4. From L: 32 pairs x 4 rows x 96 channels (23 staged
+// rows), r-chunks of 4. From I: 8 waves, 32 pairs x 8 rows (39 staged rows).
+template <bool F> using F32K11S4 = typename std::conditional<F, F32Cfg<8, 3, 8, 2, 11, 4, 1, 1, true, 8>,
+                                                             F32Cfg<4, 3, 4, 4, 11, 4, 1, 1, false>>::type;
+// bf16, 3x3 stride 1: 8 waves, 32 pairs x 14 rows x 128 channels, r-chunks of 32.
+template <bool F> using BF16K3S1 = BF16Cfg<14, 4, 2, 32, 3, 1, F, 8>;
 
 template <bool F>
 hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O, int dtype,
