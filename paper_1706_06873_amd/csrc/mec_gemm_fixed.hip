@@ -622,10 +622,12 @@ hipError_t run_fixed(const Shape& s, const void* A, const void* K, float* O, hip
 template <bool F> using F32K3S1Wide = F32Cfg<14, 2, 2, 16, 3, 1, 4, 4, F>;
 // fp32, 3x3 stride 1, short rows (R = 3 i_c with i_c not a multiple of 4).
 template <bool F> using F32K3S1Narrow = F32Cfg<8, 2, 4, 2, 3, 1, 1, 1, F>;
-// fp32, 11x11 stride 4. From L: 32 pairs x 4 rows x 96 channels (23 staged
-// rows), r-chunks of 4. From I: 8 waves, 32 pairs x 8 rows (39 staged rows).
-template <bool F> using F32K11S4 = typename std::conditional<F, F32Cfg<8, 3, 8, 2, 11, 4, 1, 1, true, 8>,
-                                                             F32Cfg<4, 3, 4, 4, 11, 4, 1, 1, false>>::type;
+// fp32, 11x11 stride 4, 96-channel tiles. From L: 32 pairs x 4 rows (23 staged
+// rows), r-chunks of 4. From I: 8 waves, 32 pairs x 8 rows (39 staged rows),
+// r-chunks of 2. VB = 4 loads K four channels at a time (k_c % 4 == 0).
+template <bool F, int VB>
+using F32K11S4 = typename std::conditional<F, F32Cfg<8, 3, 8, 2, 11, 4, 1, VB, true, 8>,
+                                           F32Cfg<4, 3, 4, 4, 11, 4, 1, VB, false>>::type;
 // bf16, 3x3 stride 1: 8 waves, 32 pairs x 14 rows x 128 channels, r-chunks of 32.
 template <bool F> using BF16K3S1 = BF16Cfg<14, 4, 2, 32, 3, 1, F, 8>;
 
@@ -639,7 +641,10 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
     if (dtype == 0) {
         if (s.R >= 32) MEC_TRY_FIXED(F32K3S1Wide<F>);
         MEC_TRY_FIXED(F32K3S1Narrow<F>);
-        MEC_TRY_FIXED(F32K11S4<F>);
+        using K11V4 = F32K11S4<F, 4>;
+        using K11V1 = F32K11S4<F, 1>;
+        MEC_TRY_FIXED(K11V4);
+        MEC_TRY_FIXED(K11V1);
     } else {
         MEC_TRY_FIXED(BF16K3S1<F>);
     }

@@ -55,6 +55,7 @@ SWEEP = [
     (2, 23, 25, 3, 3, 3, 64, 1, 1),      # narrow (R = 9)
     (3, 31, 30, 3, 11, 11, 96, 4, 4),    # tall (11x11 s4)
     (1, 35, 33, 3, 11, 11, 100, 4, 3),   # tall, ragged channels and strides
+    (2, 27, 29, 3, 11, 11, 30, 4, 4),    # tall, k_c not a multiple of 4 (scalar K loads)
     (2, 13, 12, 5, 5, 5, 33, 2, 2),
     (1, 30, 9, 2, 20, 3, 7, 1, 1),       # generic HT=4 (tall k_h)
     (1, 40, 9, 1, 13, 3, 130, 9, 1),     # generic HT=4, large s_h
@@ -77,6 +78,8 @@ SWEEP_BF16 = [
     (1, 12, 12, 8, 5, 3, 130, 2, 1),
     (2, 6, 5, 7, 6, 5, 3, 1, 1),
     (1, 4, 400, 64, 3, 3, 16, 1, 1),     # wide rows (gather lowering)
+    (3, 18, 16, 40, 3, 3, 136, 1, 1),    # bf16 3x3: two channel tiles, the second ragged
+    (2, 9, 40, 24, 3, 3, 8, 1, 2),       # bf16 3x3, R not a multiple of the r-chunk
 ]
 
 
