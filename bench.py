@@ -46,9 +46,45 @@ def parse():
                     help="after timing, run one plain device-to-device copy of this many MiB "
                          "(a known-size reference for rocprofv3 byte counters)")
     ap.add_argument("--traffic", default=None,
-                    help="JSON file with per-launch HBM bytes of the slab-product kernel "
-                         "from rocprofv3 counters")
+                    help="profile summary holding the slab-product kernel's per-launch HBM "
+                         "bytes from rocprofv3 counters (default: profiles/slab_gemm_<dtype>_<layer>_"
+                         "<algo>_traffic.md when present)")
     return ap.parse_args()
+
+
+def csrc_digest():
+    """sha256 over the native sources; a traffic figure taken from another
+    version of the kernels is not reported."""
+    import hashlib
+    d = os.path.join(REPO, "paper_1706_06873_amd", "csrc")
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(d)):
+        if name.endswith((".hip", ".h", ".cpp")):
+            h.update(name.encode())
+            with open(os.path.join(d, name), "rb") as f:
+                h.update(f.read())
+    return h.hexdigest()
+
+
+def load_traffic(path, kdt, layer_name, algo):
+    """Per-launch HBM bytes of the slab-product kernel from a profile summary:
+    the line starting with 'traffic-json:' holds FETCH_SIZE and WRITE_SIZE (KiB
+    per dispatch), the factors that make each counter read a plain copy of known
+    size correctly, and the digest of the sources the counters were taken on."""
+    if path is None:
+        path = os.path.join(REPO, "profiles", "slab_gemm_%s_%s_%s_traffic.md" % (kdt, layer_name, algo))
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        for line in f:
+            if line.startswith("traffic-json:"):
+                t = json.loads(line[len("traffic-json:"):])
+                break
+        else:
+            return None
+    if t.get("workload") != "%s %s" % (layer_name, algo) or t.get("csrc_sha256") != csrc_digest():
+        return None
+    return int(round((t["fetch_kib"] * t["fetch_scale"] + t["write_kib"] * t["write_scale"]) * 1024))
 
 
 def main():
@@ -149,19 +185,16 @@ def main():
     # roofline of the dominant kernel: algorithmic flops per launch / its average duration
     peak = PEAK_TFLOPS[layer.dtype]
     achieved = flops / (kern_avg * 1e-3) / 1e12
+    kname = "slab_gemm_%s_kernel" % ("bf16" if layer.dtype == "bf16" else "f32")
     if args.algo == "fused":
         alg_bytes = es * (size_I + size_K) + 4 * size_O
-        kname = "slab_gemm_kernel (fused)"
+        kname += " (from I)"
     else:
         alg_bytes = es * (size_L + size_K) + 4 * size_O
-        kname = "slab_gemm_kernel"
     # a kernel whose arithmetic intensity is below the ridge point is HBM-bound
     ridge = peak * 1e12 / (PEAK_HBM_GBS * 1e9)
     bound = "mfma" if flops / alg_bytes >= ridge else "hbm"
-    traffic = None
-    if args.traffic and os.path.exists(args.traffic):
-        with open(args.traffic) as f:
-            traffic = json.load(f).get(kname)
+    traffic = load_traffic(args.traffic, "bf16" if layer.dtype == "bf16" else "f32", layer.name, args.algo) if args.batch <= 0 else None
     if bound == "mfma":
         roof = {"bound": "mfma", "kernel": kname, "achieved": round(achieved, 2),
                 "peak": peak, "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
