@@ -36,7 +36,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--layer", default=DEFAULT_LAYER)
-    ap.add_argument("--algo", default="lowered", choices=["lowered", "fused"])
+    ap.add_argument("--algo", default="lowered", choices=["lowered", "fused", "im2col"],
+                    help="MEC from L (default), MEC fused, or the im2col + product baseline")
     ap.add_argument("--sets", type=int, default=4, help="rotating buffer sets")
     ap.add_argument("--batch", type=int, default=0,
                     help="override the layer's batch size i_n (0 keeps the layer's own)")
@@ -122,6 +123,8 @@ def main():
     size_K = k_h * k_w * i_c * k_c
     size_O = i_n * o_h * o_w * k_c
     size_L = ws_bytes // es
+    size_M = im2col_bytes // es
+    P = k_h * k_w * i_c  # im2col row length
 
     dev = torch.device("cuda:0")
     I0, K0 = wl.make_inputs(layer)
@@ -130,8 +133,9 @@ def main():
         I = I0.to(dev)
         if j:
             I = I.clone()
+        lshape = (i_n, o_w, o_h, k_h, k_w, i_c) if args.algo == "im2col" else (i_n, o_w, i_h, k_w, i_c)
         sets.append(dict(I=I, K=K0.to(dev),
-                         L=torch.empty((i_n, o_w, i_h, k_w, i_c), dtype=I0.dtype, device=dev),
+                         L=torch.empty(lshape, dtype=I0.dtype, device=dev),
                          O=torch.empty((i_n, o_h, o_w, k_c), dtype=torch.float32, device=dev)))
     stream = torch.cuda.Stream(device=dev)  # default priority
     torch.cuda.synchronize()
@@ -146,10 +150,19 @@ def main():
             return
         if ev:
             ev[0].record(stream)
-        mec.lower(bufs["I"], k_h, k_w, k_c, s_h, s_w, L=bufs["L"], stream=stream)
+        if args.algo == "im2col":
+            mec.im2col(bufs["I"], k_h, k_w, k_c, s_h, s_w, M=bufs["L"], stream=stream)
+        else:
+            mec.lower(bufs["I"], k_h, k_w, k_c, s_h, s_w, L=bufs["L"], stream=stream)
         if ev:
             ev[1].record(stream)
-        mec.gemm(bufs["L"], bufs["K"], i_h, i_w, s_h, s_w, O=bufs["O"], stream=stream)
+        if args.algo == "im2col":
+            # the product of M and K: MEC's product phase of the 1x1 convolution
+            # whose pixels (n, y, x) carry the patches as channels
+            mec.gemm(bufs["L"].view(i_n, o_w, o_h, 1, P), bufs["K"].view(1, 1, P, k_c),
+                     o_h, o_w, 1, 1, O=bufs["O"], stream=stream)
+        else:
+            mec.gemm(bufs["L"], bufs["K"], i_h, i_w, s_h, s_w, O=bufs["O"], stream=stream)
         if ev:
             ev[2].record(stream)
 
@@ -189,6 +202,9 @@ def main():
     if args.algo == "fused":
         alg_bytes = es * (size_I + size_K) + 4 * size_O
         kname += " (from I)"
+    elif args.algo == "im2col":
+        alg_bytes = es * (size_M + size_K) + 4 * size_O
+        kname += " (im2col product, k_h = 1)"
     else:
         alg_bytes = es * (size_L + size_K) + 4 * size_O
     # a kernel whose arithmetic intensity is below the ridge point is HBM-bound
@@ -223,7 +239,7 @@ def main():
                                % (layer.name, i_n, i_h, i_w, i_c, layer.dtype, k_h, k_w, i_c, k_c,
                                   s_h, s_w, o_h, o_w),
                    "algo": args.algo, "buffer_sets": args.sets},
-        "workspace_bytes": ws_bytes if args.algo == "lowered" else 0,
+        "workspace_bytes": {"lowered": ws_bytes, "fused": 0, "im2col": im2col_bytes}[args.algo],
         "im2col_bytes": im2col_bytes,
         "workspace_vs_im2col": round(im2col_bytes / ws_bytes, 4),
         "wall_s": round(wall, 4),
@@ -233,10 +249,11 @@ def main():
     }
     if lower_ms is not None:
         lavg = sum(lower_ms) / len(lower_ms)
-        lbytes = es * (size_I + size_L)
+        lbytes = es * (size_I + (size_M if args.algo == "im2col" else size_L))
         out["lower_ms"] = {"avg": round(lavg, 5), "median": round(lower_ms[len(lower_ms) // 2], 5),
                            "min": round(lower_ms[0], 5)}
-        out["roofline_lower"] = {"bound": "hbm", "kernel": "lower_*_kernel",
+        out["roofline_lower"] = {"bound": "hbm",
+                                 "kernel": "im2col_*_kernel" if args.algo == "im2col" else "lower_*_kernel",
                                  "achieved": round(lbytes / (lavg * 1e-3) / 1e9, 1),
                                  "peak": PEAK_HBM_GBS, "unit": "GB/s",
                                  "frac": round(lbytes / (lavg * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),

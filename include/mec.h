@@ -54,8 +54,11 @@ enum mec_dtype { MEC_F32 = 0, MEC_BF16 = 1 };
 /* MEC_ALGO_LOWERED: Algorithm 2 as two kernels -- the lowering writes L into
  *   the caller's workspace, then the slab products read it.
  * MEC_ALGO_FUSED: one kernel forms each slab of L in on-chip memory straight
- *   from I; L is never written to device memory and no workspace is used. */
-enum mec_algo { MEC_ALGO_LOWERED = 0, MEC_ALGO_FUSED = 1 };
+ *   from I; L is never written to device memory and no workspace is used.
+ * MEC_ALGO_IM2COL: the baseline MEC replaces (Section 3.1): im2col lowering
+ *   into the workspace (see mec_im2col), then one matrix product by the same
+ *   product kernels with no slab overlap. */
+enum mec_algo { MEC_ALGO_LOWERED = 0, MEC_ALGO_FUSED = 1, MEC_ALGO_IM2COL = 2 };
 
 enum mec_status {
     MEC_OK = 0,
@@ -80,6 +83,7 @@ int mec_output_dims(int i_h, int i_w, int k_h, int k_w, int s_h, int s_w,
  *   Algorithm 2 allocates (Section 3.4, Eq. (3), read with i_c where the
  *   printed equation has k_c). No rounding up.
  * MEC_ALGO_FUSED: 0.
+ * MEC_ALGO_IM2COL: exactly mec_im2col_bytes.
  * Returns the byte count (>= 0) or a negative status. */
 int64_t mec_workspace_bytes(int i_n, int i_h, int i_w, int i_c,
                             int k_h, int k_w, int k_c, int s_h, int s_w,
@@ -87,7 +91,6 @@ int64_t mec_workspace_bytes(int i_n, int i_h, int i_w, int i_c,
 
 /* Size of the im2col lowered matrix that MEC's L replaces, in bytes:
  * (i_n*o_h*o_w) x (k_h*k_w*i_c) elements (Section 3.1, Eq. (2), i_c reading).
- * Provided so callers can report MEC's saving; no kernel uses it.
  * Returns the byte count (>= 0) or a negative status. */
 int64_t mec_im2col_bytes(int i_n, int i_h, int i_w, int i_c,
                          int k_h, int k_w, int k_c, int s_h, int s_w, int dtype);
@@ -118,12 +121,30 @@ int mec_gemm(const void* L, const void* K, float* O,
              int k_h, int k_w, int k_c, int s_h, int s_w,
              int dtype, void* stream);
 
-/* The convolution O = I * K by MEC (Algorithm 2).
+/* im2col lowering (Section 3.1, Fig. 1(b)), the method MEC is compared with:
+ * every output pixel's k_h x k_w x i_c input patch becomes one row of M. Rows
+ * are stored column-major over the output image, (n, x, y):
+ *   M[n, x, y, a, b, c] = I[n, y*s_h + a, x*s_w + b, c]
+ * for n < i_n, x < o_w, y < o_h, a < k_h, b < k_w, c < i_c. In this order M is
+ * the MEC lowered tensor of a 1x1, stride-1 convolution whose input pixel
+ * (n, y, x) holds that patch as its k_h*k_w*i_c channels, so
+ *   mec_gemm(M, K, O, i_n, o_h, o_w, k_h*k_w*i_c, 1, 1, k_c, 1, 1, dtype, stream)
+ * computes O = M x K, the convolution, with the same product kernels.
+ * M must hold mec_im2col_bytes and must not overlap I. A bit copy in `dtype`.
+ * Returns MEC_OK or a negative status. */
+int mec_im2col(const void* I, void* M,
+               int i_n, int i_h, int i_w, int i_c,
+               int k_h, int k_w, int k_c, int s_h, int s_w,
+               int dtype, void* stream);
+
+/* The convolution O = I * K by MEC (Algorithm 2), or by the im2col baseline.
  * MEC_ALGO_LOWERED: mec_lower into `workspace`, then mec_gemm from it;
  *   workspace_bytes must be >= mec_workspace_bytes(..., MEC_ALGO_LOWERED) and
  *   the workspace must be aligned to the element size. On return (after the
  *   stream completes) the workspace holds L exactly as mec_lower writes it.
  * MEC_ALGO_FUSED: one kernel; workspace may be NULL and is not touched.
+ * MEC_ALGO_IM2COL: mec_im2col into `workspace` (at least mec_im2col_bytes),
+ *   then the product of M and K; the workspace then holds M.
  * O must not overlap I, K or the workspace.
  * Returns MEC_OK or a negative status. */
 int mec_conv2d(const void* I, const void* K, float* O,

@@ -21,16 +21,17 @@ import os
 import torch  # noqa: E402,F401
 
 __all__ = [
-    "MecError", "F32", "BF16", "LOWERED", "FUSED", "lib", "output_dims", "workspace_bytes",
-    "im2col_bytes", "lower", "gemm", "conv2d", "strerror",
+    "MecError", "F32", "BF16", "LOWERED", "FUSED", "IM2COL", "lib", "output_dims",
+    "workspace_bytes", "im2col_bytes", "lower", "im2col", "gemm", "conv2d", "strerror",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libmec.so")
 
 F32, BF16 = 0, 1
-LOWERED, FUSED = 0, 1
-_ALGOS = {"lowered": LOWERED, "fused": FUSED, LOWERED: LOWERED, FUSED: FUSED}
+LOWERED, FUSED, IM2COL = 0, 1, 2
+_ALGOS = {"lowered": LOWERED, "fused": FUSED, "im2col": IM2COL,
+          LOWERED: LOWERED, FUSED: FUSED, IM2COL: IM2COL}
 
 if not os.path.exists(LIB_PATH):
     raise ImportError("%s is not built; run `python paper_1706_06873_amd/build.py`" % LIB_PATH)
@@ -50,6 +51,8 @@ def _load(path):
     L.mec_im2col_bytes.restype = ctypes.c_int64
     L.mec_lower.argtypes = [_vp, _vp] + _DIMS + [_i, _vp]
     L.mec_lower.restype = _i
+    L.mec_im2col.argtypes = [_vp, _vp] + _DIMS + [_i, _vp]
+    L.mec_im2col.restype = _i
     L.mec_gemm.argtypes = [_vp, _vp, _vp] + _DIMS + [_i, _vp]
     L.mec_gemm.restype = _i
     L.mec_conv2d.argtypes = [_vp, _vp, _vp, _vp, ctypes.c_size_t] + _DIMS + [_i, _i, _vp]
@@ -165,6 +168,21 @@ def lower(I, k_h, k_w, k_c, s_h, s_w, L=None, stream=None):
     return L
 
 
+def im2col(I, k_h, k_w, k_c, s_h, s_w, M=None, stream=None):
+    """im2col lowering of I, rows in (n, x, y) order: M is
+    i_n x o_w x o_h x k_h x k_w x i_c. Returns M."""
+    import torch
+    i_n, i_h, i_w, i_c = I.shape
+    o_h, o_w = output_dims(i_h, i_w, k_h, k_w, s_h, s_w)
+    if M is None:
+        M = torch.empty((i_n, o_w, o_h, k_h, k_w, i_c), dtype=I.dtype, device=I.device)
+    if M.numel() != i_n * o_w * o_h * k_h * k_w * i_c or M.dtype != I.dtype:
+        raise ValueError("M has the wrong size or dtype")
+    _check(lib.mec_im2col(_dev_ptr(I, "I"), _dev_ptr(M, "M"), i_n, i_h, i_w, i_c, k_h, k_w, k_c,
+                          s_h, s_w, _dtype_code(I), _stream_handle(stream)), "mec_im2col")
+    return M
+
+
 def _out(I, K, s_h, s_w, O):
     import torch
     d = _dims(I, K, s_h, s_w)
@@ -194,14 +212,15 @@ def gemm(L, K, i_h, i_w, s_h, s_w, O=None, stream=None):
 
 
 def conv2d(I, K, s_h=1, s_w=1, algo="lowered", workspace=None, O=None, stream=None):
-    """O = I * K by MEC. With algo="lowered" a workspace of
-    workspace_bytes(...) bytes is allocated unless given (a uint8 device
-    tensor); after the call it holds L. Returns O."""
+    """O = I * K by MEC ("lowered", "fused") or by the im2col baseline
+    ("im2col"). With "lowered" or "im2col" a workspace of workspace_bytes(...)
+    bytes is allocated unless given (a uint8 device tensor); after the call it
+    holds L (or the im2col matrix). Returns O."""
     import torch
     d, O = _out(I, K, s_h, s_w, O)
     a = _ALGOS[algo]
     ws_ptr, ws_bytes = None, 0
-    if a == LOWERED:
+    if a != FUSED:
         need = workspace_bytes(*d, dtype=_dtype_code(I), algo=a)
         if workspace is None:
             workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=I.device)

@@ -55,6 +55,24 @@ int make_shape(mec::Shape& s, int i_n, int i_h, int i_w, int i_c, int k_h, int k
 }
 
 int64_t lowered_elems(const mec::Shape& s) { return s.i_n * s.o_w * s.i_h * s.k_w * s.i_c; }
+int64_t im2col_elems(const mec::Shape& s) { return s.i_n * s.o_h * s.o_w * s.k_h * s.k_w * s.i_c; }
+
+// The product phase of im2col + GEMM as MEC's product phase of a 1x1,
+// stride-1 convolution: the image has pixels (n, y, x), each with the
+// k_h*k_w*i_c values of its patch as channels; its MEC lowered tensor is the
+// (n, x, y)-ordered im2col matrix.
+mec::Shape im2col_product_shape(const mec::Shape& s) {
+    mec::Shape v = s;
+    v.i_h = s.o_h;
+    v.i_w = s.o_w;
+    v.i_c = s.k_h * s.k_w * s.i_c;
+    v.k_h = v.k_w = v.s_h = v.s_w = 1;
+    v.o_h = s.o_h;
+    v.o_w = s.o_w;
+    v.R = v.i_c;
+    v.pairs = s.i_n * s.o_w;
+    return v;
+}
 
 bool aligned(const void* p, int64_t bytes) { return ((uintptr_t)p % (uintptr_t)bytes) == 0; }
 
@@ -94,6 +112,7 @@ int64_t mec_workspace_bytes(int i_n, int i_h, int i_w, int i_c, int k_h, int k_w
     if (rc != MEC_OK) return rc;
     if (!valid_dtype(dtype)) return MEC_ERR_INVALID_ARG;
     if (algo == MEC_ALGO_FUSED) return 0;
+    if (algo == MEC_ALGO_IM2COL) return im2col_elems(s) * elem_bytes(dtype);
     if (algo != MEC_ALGO_LOWERED) return MEC_ERR_INVALID_ARG;
     return lowered_elems(s) * elem_bytes(dtype);
 }
@@ -104,7 +123,7 @@ int64_t mec_im2col_bytes(int i_n, int i_h, int i_w, int i_c, int k_h, int k_w, i
     int rc = make_shape(s, i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w);
     if (rc != MEC_OK) return rc;
     if (!valid_dtype(dtype)) return MEC_ERR_INVALID_ARG;
-    return s.i_n * s.o_h * s.o_w * s.k_h * s.k_w * s.i_c * elem_bytes(dtype);
+    return im2col_elems(s) * elem_bytes(dtype);
 }
 
 int mec_lower(const void* I, void* L, int i_n, int i_h, int i_w, int i_c, int k_h, int k_w,
@@ -117,6 +136,18 @@ int mec_lower(const void* I, void* L, int i_n, int i_h, int i_w, int i_c, int k_
     if (!aligned(I, es) || !aligned(L, es)) return MEC_ERR_ALIGNMENT;
     clear_stale_error();
     return hip_status(mec::launch_lower(s, I, L, (int)es, (hipStream_t)stream), "lowering");
+}
+
+int mec_im2col(const void* I, void* M, int i_n, int i_h, int i_w, int i_c, int k_h, int k_w,
+               int k_c, int s_h, int s_w, int dtype, void* stream) {
+    mec::Shape s;
+    int rc = make_shape(s, i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w);
+    if (rc != MEC_OK) return rc;
+    if (!valid_dtype(dtype) || !I || !M) return MEC_ERR_INVALID_ARG;
+    const int64_t es = elem_bytes(dtype);
+    if (!aligned(I, es) || !aligned(M, es)) return MEC_ERR_ALIGNMENT;
+    clear_stale_error();
+    return hip_status(mec::launch_im2col(s, I, M, (int)es, (hipStream_t)stream), "im2col");
 }
 
 int mec_gemm(const void* L, const void* K, float* O, int i_n, int i_h, int i_w, int i_c, int k_h,
@@ -139,21 +170,28 @@ int mec_conv2d(const void* I, const void* K, float* O, void* workspace, size_t w
     mec::Shape s;
     int rc = make_shape(s, i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w);
     if (rc != MEC_OK) return rc;
-    if (!valid_dtype(dtype) || (algo != MEC_ALGO_LOWERED && algo != MEC_ALGO_FUSED) || !I || !K ||
-        !O)
+    if (!valid_dtype(dtype) ||
+        (algo != MEC_ALGO_LOWERED && algo != MEC_ALGO_FUSED && algo != MEC_ALGO_IM2COL) || !I ||
+        !K || !O)
         return MEC_ERR_INVALID_ARG;
     const int64_t es = elem_bytes(dtype);
     if (!aligned(I, es) || !aligned(K, es) || !aligned(O, 4)) return MEC_ERR_ALIGNMENT;
-    if (algo == MEC_ALGO_LOWERED) {
-        const int64_t need = lowered_elems(s) * es;
+    if (algo != MEC_ALGO_FUSED) {
+        const int64_t need = (algo == MEC_ALGO_IM2COL ? im2col_elems(s) : lowered_elems(s)) * es;
         if (!workspace || (uint64_t)workspace_bytes < (uint64_t)need) return MEC_ERR_WORKSPACE;
         if (!aligned(workspace, es)) return MEC_ERR_ALIGNMENT;
     }
-    if (!mec::gemm_supported(s, dtype)) return MEC_ERR_UNSUPPORTED;
+    const mec::Shape g = algo == MEC_ALGO_IM2COL ? im2col_product_shape(s) : s;
+    if (g.R > (int64_t(1) << 26) || !mec::gemm_supported(g, dtype)) return MEC_ERR_UNSUPPORTED;
     const hipStream_t st = (hipStream_t)stream;
     clear_stale_error();
     if (algo == MEC_ALGO_FUSED)
         return hip_status(mec::launch_gemm(s, I, K, O, dtype, true, st), "fused slab products");
+    if (algo == MEC_ALGO_IM2COL) {
+        rc = hip_status(mec::launch_im2col(s, I, workspace, (int)es, st), "im2col");
+        if (rc != MEC_OK) return rc;
+        return hip_status(mec::launch_gemm(g, workspace, K, O, dtype, false, st), "im2col product");
+    }
     rc = hip_status(mec::launch_lower(s, I, workspace, (int)es, st), "lowering");
     if (rc != MEC_OK) return rc;
     return hip_status(mec::launch_gemm(s, workspace, K, O, dtype, false, st), "slab products");

@@ -1,6 +1,7 @@
 // MEC's slab products (Section 3.3, Algorithm 2, product phase) for kernel
-// heights and strides fixed at compile time: 3x3 stride 1 and 11x11 stride 4
-// in fp32, 3x3 stride 1 in bf16. Same tiling as mec_gemm.hip -- a tile of 32
+// heights and strides fixed at compile time: in fp32 3x3 stride 1, 5x5 stride
+// 1, 7x7 stride 2, 11x11 stride 4 and k_h = 1; in bf16 3x3 stride 1 and
+// k_h = 1 (the shapes of the paper's benchmark layers, Table 2). Same tiling as mec_gemm.hip -- a tile of 32
 // (n, w) pairs x HT output rows x NT channels stages the union of the slab rows
 // it needs, hrows = (HT-1)*s_h + k_h, once per r-chunk -- but with k_h and s_h
 // known the reduction over the kernel rows is fully unrolled: each wave loads
@@ -10,6 +11,7 @@
 // relative to the tile's first pair so they fit 32-bit registers; the next
 // r-chunk's global loads are issued after the first MFMA k-step of the current
 // one, and their LDS stores go to the other of two stage buffers.
+#include <initializer_list>
 #include <type_traits>
 
 #include "mec_mfma.h"
@@ -620,6 +622,10 @@ hipError_t run_fixed(const Shape& s, const void* A, const void* K, float* O, hip
 // fp32, 3x3 stride 1, long rows (R % 4 == 0): 32 pairs x 14 rows x 64 channels,
 // r-chunks of 16, 16-byte loads of L (or I) and K.
 template <bool F> using F32K3S1Wide = F32Cfg<14, 2, 2, 16, 3, 1, 4, 4, F>;
+// the same with 4 and 2 output rows per tile, for layers whose few pair tiles
+// and small o_h would leave most compute units idle with 14-row tiles
+template <bool F> using F32K3S1Wide4 = F32Cfg<4, 2, 2, 16, 3, 1, 4, 4, F>;
+template <bool F> using F32K3S1Wide2 = F32Cfg<2, 2, 2, 16, 3, 1, 4, 4, F>;
 // fp32, 3x3 stride 1, short rows (R = 3 i_c with i_c not a multiple of 4).
 template <bool F> using F32K3S1Narrow = F32Cfg<8, 2, 4, 2, 3, 1, 1, 1, F>;
 // fp32, 11x11 stride 4, 96-channel tiles. From L: 32 pairs x 4 rows (23 staged
@@ -628,8 +634,44 @@ template <bool F> using F32K3S1Narrow = F32Cfg<8, 2, 4, 2, 3, 1, 1, 1, F>;
 template <bool F, int VB>
 using F32K11S4 = typename std::conditional<F, F32Cfg<8, 3, 8, 2, 11, 4, 1, VB, true, 8>,
                                            F32Cfg<4, 3, 4, 4, 11, 4, 1, VB, false>>::type;
+// fp32, 7x7 stride 2: 32 pairs x 8 rows (21 staged rows) x 64 channels.
+template <bool F> using F32K7S2Wide = F32Cfg<8, 2, 2, 8, 7, 2, 4, 4, F>;
+template <bool F> using F32K7S2Narrow = F32Cfg<8, 2, 4, 4, 7, 2, 1, 4, F>;
+template <bool F> using F32K7S2Scalar = F32Cfg<8, 2, 4, 4, 7, 2, 1, 1, F>;
+// fp32, 5x5 stride 1: 32 pairs x 4 rows (8 staged rows) x 64 channels.
+template <bool F> using F32K5S1Wide = F32Cfg<4, 2, 2, 16, 5, 1, 4, 4, F>;
+template <bool F> using F32K5S1Narrow = F32Cfg<4, 2, 2, 4, 5, 1, 1, 4, F>;
+template <bool F> using F32K5S1Scalar = F32Cfg<4, 2, 2, 4, 5, 1, 1, 1, F>;
+// k_h = 1, stride 1: plain products with no slab overlap (1x1 convolutions,
+// and the im2col baseline's product). 32 pairs x 8 rows x 64 channels, or
+// 96 channels for the short-row form when k_c > 64; bf16: 7 rows x 256
+// channels.
+template <bool F> using F32K1S1Wide = F32Cfg<8, 2, 2, 16, 1, 1, 4, 4, F>;
+template <bool F> using F32K1S1Narrow = F32Cfg<8, 2, 2, 4, 1, 1, 1, 4, F>;
+template <bool F> using F32K1S1Narrow96 = F32Cfg<8, 3, 4, 8, 1, 1, 1, 4, F>;
+template <bool F> using F32K1S1Scalar = F32Cfg<8, 2, 2, 4, 1, 1, 1, 1, F>;
+template <bool F> using BF16K1S1 = BF16Cfg<7, 8, 1, 32, 1, 1, F, 8>;
 // bf16, 3x3 stride 1: 8 waves, 32 pairs x 14 rows x 128 channels, r-chunks of 32.
 template <bool F> using BF16K3S1 = BF16Cfg<14, 4, 2, 32, 3, 1, F, 8>;
+
+// Of tiles that differ only in their number of output rows, the one that
+// minimises (rounds of tiles over the 256 compute units) x (input rows each
+// tile stages): fewer, taller tiles stage the overlap rows less often; more,
+// shorter tiles keep every compute unit busy on small layers.
+int pick_rows(const Shape& s, int nt, std::initializer_list<int> rows) {
+    int best = 0;
+    int64_t best_cost = 0;
+    for (int ht : rows) {
+        const int64_t tiles = ((s.pairs + kPairs - 1) / kPairs) * ((s.o_h + ht - 1) / ht) *
+                              ((s.k_c + nt - 1) / nt);
+        const int64_t cost = ((tiles + 255) / 256) * ((ht - 1) * s.s_h + s.k_h);
+        if (best == 0 || cost < best_cost) {
+            best = ht;
+            best_cost = cost;
+        }
+    }
+    return best;
+}
 
 template <bool F>
 hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O, int dtype,
@@ -639,14 +681,30 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
         return dry_run ? hipSuccess : run_fixed<CFG>(s, A, K, O, stream);   \
     }
     if (dtype == 0) {
-        if (s.R >= 32) MEC_TRY_FIXED(F32K3S1Wide<F>);
+        if (s.R >= 32) {
+            const int ht = s.k_h == 3 && s.s_h == 1 ? pick_rows(s, 64, {14, 4, 2}) : 14;
+            if (ht == 2) MEC_TRY_FIXED(F32K3S1Wide2<F>);
+            if (ht == 4) MEC_TRY_FIXED(F32K3S1Wide4<F>);
+            MEC_TRY_FIXED(F32K3S1Wide<F>);
+        }
         MEC_TRY_FIXED(F32K3S1Narrow<F>);
+        MEC_TRY_FIXED(F32K7S2Wide<F>);
+        MEC_TRY_FIXED(F32K7S2Narrow<F>);
+        MEC_TRY_FIXED(F32K7S2Scalar<F>);
+        MEC_TRY_FIXED(F32K5S1Wide<F>);
+        MEC_TRY_FIXED(F32K5S1Narrow<F>);
+        MEC_TRY_FIXED(F32K5S1Scalar<F>);
         using K11V4 = F32K11S4<F, 4>;
         using K11V1 = F32K11S4<F, 1>;
         MEC_TRY_FIXED(K11V4);
         MEC_TRY_FIXED(K11V1);
+        MEC_TRY_FIXED(F32K1S1Wide<F>);
+        if (s.k_c > 64) MEC_TRY_FIXED(F32K1S1Narrow96<F>);
+        MEC_TRY_FIXED(F32K1S1Narrow<F>);
+        MEC_TRY_FIXED(F32K1S1Scalar<F>);
     } else {
         MEC_TRY_FIXED(BF16K3S1<F>);
+        MEC_TRY_FIXED(BF16K1S1<F>);
     }
 #undef MEC_TRY_FIXED
     return hipErrorNotSupported;

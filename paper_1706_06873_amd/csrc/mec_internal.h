@@ -63,6 +63,11 @@ struct LowerParams {
 hipError_t launch_lower(const Shape& s, const void* I, void* L, int elem_bytes,
                         hipStream_t stream);
 
+// Enqueue the im2col lowering, rows in (n, x, y) order. Returns the launch
+// status.
+hipError_t launch_im2col(const Shape& s, const void* I, void* M, int elem_bytes,
+                         hipStream_t stream);
+
 // ---------------------------------------------------------------- slab products
 struct GemmParams {
     const void* A;     // L (lowered) or I (fused)

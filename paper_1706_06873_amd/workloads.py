@@ -65,6 +65,37 @@ LAYERS = {
 }
 LAYER_ORDER = ["tiny", "resnet_mid", "vgg_first", "alexnet_conv1", "deep_bf16"]
 
+# The twelve benchmark layers of Table 2 (input i_h x i_w x i_c, kernel
+# k_h x k_w x k_c, stride), taken as printed: no padding is added.
+TABLE2 = {
+    "cv1": (227, 227, 3, 11, 11, 96, 4),
+    "cv2": (231, 231, 3, 11, 11, 96, 4),
+    "cv3": (227, 227, 3, 7, 7, 64, 2),
+    "cv4": (224, 224, 64, 7, 7, 64, 2),
+    "cv5": (24, 24, 96, 5, 5, 256, 1),
+    "cv6": (12, 12, 256, 3, 3, 512, 1),
+    "cv7": (224, 224, 3, 3, 3, 64, 1),
+    "cv8": (112, 112, 64, 3, 3, 128, 1),
+    "cv9": (56, 56, 64, 3, 3, 64, 1),
+    "cv10": (28, 28, 128, 3, 3, 128, 1),
+    "cv11": (14, 14, 256, 3, 3, 256, 1),
+    "cv12": (7, 7, 512, 3, 3, 512, 1),
+}
+
+
+def table2_layer(name, i_n=32, dtype="f32", stride=None, dist="u11"):
+    """A Table 2 layer at batch i_n; ``stride`` overrides s_h = s_w (the
+    stride sweep of Fig. 4(a) runs cv1 with s = 1..10). Seed: the layer's
+    number (cv1 -> 101, ..., cv12 -> 112), plus 100 * stride when overridden."""
+    i_h, i_w, i_c, k_h, k_w, k_c, s = TABLE2[name]
+    num = int(name[2:])
+    seed = 100 + num + (100 * stride if stride else 0)
+    s = stride or s
+    return Layer("%s%s" % (name, "_s%d" % stride if stride else ""), i_n, i_h, i_w, i_c, k_h, k_w,
+                 k_c, s, s, 0, dtype, dist, dist, seed,
+                 "Table 2 %s: %dx%dx%d input, %dx%dx%d kernel, stride %d"
+                 % (name, i_h, i_w, i_c, k_h, k_w, k_c, s))
+
 
 def _draw(gen, shape, dist):
     if dist == "u11":

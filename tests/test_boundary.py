@@ -50,6 +50,7 @@ def test_status_codes_match_header():
     codes = dict((k, int(v)) for k, v in re.findall(r"(MEC_\w+)\s*=\s*(-?\d+)", text))
     assert codes["MEC_F32"] == mec.F32 and codes["MEC_BF16"] == mec.BF16
     assert codes["MEC_ALGO_LOWERED"] == mec.LOWERED and codes["MEC_ALGO_FUSED"] == mec.FUSED
+    assert codes["MEC_ALGO_IM2COL"] == mec.IM2COL
     for name in ("MEC_OK", "MEC_ERR_INVALID_ARG", "MEC_ERR_WORKSPACE", "MEC_ERR_ALIGNMENT",
                  "MEC_ERR_HIP", "MEC_ERR_UNSUPPORTED"):
         msg = mec.strerror(codes[name])
@@ -76,6 +77,7 @@ def test_sizes_agree_with_oracle(orc, shape):
     for dt, es in ((mec.F32, 4), (mec.BF16, 2)):
         assert mec.workspace_bytes(*shape, dtype=dt, algo=mec.LOWERED) == nL * es
         assert mec.workspace_bytes(*shape, dtype=dt, algo=mec.FUSED) == 0
+        assert mec.workspace_bytes(*shape, dtype=dt, algo=mec.IM2COL) == nM * es
         assert mec.im2col_bytes(*shape, dtype=dt) == nM * es
     o = mec.output_dims(shape[1], shape[2], shape[4], shape[5], shape[7], shape[8])
     assert o == (orc.out_dim(shape[1], shape[4], shape[7]), orc.out_dim(shape[2], shape[5], shape[8]))
@@ -113,9 +115,11 @@ def test_invalid_dims_rejected_everywhere(dims):
     assert L.mec_workspace_bytes(*dims, 0, 0) == E
     assert L.mec_im2col_bytes(*dims, 0) == E
     assert L.mec_lower(FAKE, FAKE, *dims, 0, NULL) == E
+    assert L.mec_im2col(FAKE, FAKE, *dims, 0, NULL) == E
     assert L.mec_gemm(FAKE, FAKE, FAKE, *dims, 0, NULL) == E
     assert L.mec_conv2d(FAKE, FAKE, FAKE, FAKE, 1 << 40, *dims, 0, 0, NULL) == E
     assert L.mec_conv2d(FAKE, FAKE, FAKE, NULL, 0, *dims, 0, 1, NULL) == E
+    assert L.mec_conv2d(FAKE, FAKE, FAKE, FAKE, 1 << 40, *dims, 0, 2, NULL) == E
 
 
 def test_output_dims_errors_and_floor():
@@ -134,7 +138,10 @@ GOOD = (2, 9, 8, 4, 3, 3, 5, 1, 2)
 def test_bad_enums_and_null_pointers():
     L = mec.lib
     assert L.mec_workspace_bytes(*GOOD, 2, 0) == -1
-    assert L.mec_workspace_bytes(*GOOD, 0, 2) == -1
+    assert L.mec_workspace_bytes(*GOOD, 0, 3) == -1
+    assert L.mec_im2col(NULL, FAKE, *GOOD, 0, NULL) == -1
+    assert L.mec_im2col(FAKE, NULL, *GOOD, 0, NULL) == -1
+    assert L.mec_im2col(FAKE, FAKE, *GOOD, 2, NULL) == -1
     assert L.mec_im2col_bytes(*GOOD, -1) == -1
     assert L.mec_lower(NULL, FAKE, *GOOD, 0, NULL) == -1
     assert L.mec_lower(FAKE, NULL, *GOOD, 0, NULL) == -1
@@ -153,6 +160,8 @@ def test_alignment_rejected():
     # fp32 needs 4-byte alignment, bf16 2-byte; O is always fp32
     assert L.mec_lower(ODD, FAKE, *GOOD, 0, NULL) == -3
     assert L.mec_lower(FAKE, ODD, *GOOD, 0, NULL) == -3
+    assert L.mec_im2col(ODD, FAKE, *GOOD, 0, NULL) == -3
+    assert L.mec_im2col(FAKE, ODD, *GOOD, 0, NULL) == -3
     assert L.mec_gemm(FAKE, FAKE, ODD, *GOOD, 1, NULL) == -3
     assert L.mec_gemm(ODD, FAKE, FAKE, *GOOD, 0, NULL) == -3
     assert L.mec_conv2d(ODD, FAKE, FAKE, FAKE, 1 << 30, *GOOD, 0, 0, NULL) == -3
@@ -168,6 +177,11 @@ def test_workspace_rejected():
     need16 = mec.workspace_bytes(*GOOD, dtype=mec.BF16)
     assert need16 * 2 == need
     assert L.mec_conv2d(FAKE, FAKE, FAKE, FAKE, need16 - 2, *GOOD, 1, 0, NULL) == -2
+    # the im2col baseline needs the (larger) im2col matrix as workspace
+    needM = mec.workspace_bytes(*GOOD, algo=mec.IM2COL)
+    assert needM == mec.im2col_bytes(*GOOD) > need
+    assert L.mec_conv2d(FAKE, FAKE, FAKE, FAKE, needM - 4, *GOOD, 0, 2, NULL) == -2
+    assert L.mec_conv2d(FAKE, FAKE, FAKE, NULL, needM, *GOOD, 0, 2, NULL) == -2
 
 
 def test_unsupported_kernel_height():

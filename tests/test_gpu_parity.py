@@ -68,6 +68,11 @@ SWEEP = [
     (33, 4, 4, 4, 2, 2, 33, 1, 1),       # pairs = 99
     (1, 5, 200, 64, 3, 3, 8, 1, 1),      # input rows wider than the lowering's LDS stage
     (2, 6, 130, 33, 3, 2, 5, 1, 3),      # wide odd rows
+    (16, 28, 28, 128, 3, 3, 128, 1, 1),  # 3x3 tiles of 4 output rows (many channel tiles)
+    (2, 21, 19, 16, 7, 7, 40, 2, 2),     # 7x7 s2, 16-byte rows, ragged channels
+    (1, 23, 25, 3, 7, 7, 70, 2, 3),      # 7x7 s2, short rows, k_c not a multiple of 4
+    (2, 14, 13, 32, 5, 5, 64, 1, 2),     # 5x5 s1, 16-byte rows
+    (2, 14, 13, 32, 5, 5, 66, 1, 1),     # 5x5 s1, k_c not a multiple of 4
 ]
 
 SWEEP_BF16 = [
@@ -150,6 +155,71 @@ def test_lower_bitwise_sweep(orc, dims, dtype):
     assert got.shape == ref.shape and np.array_equal(got, ref)
 
 
+def im2col_ref(orc, I, k_h, k_w, s_h, s_w):
+    """The oracle's im2col (rows n, y, x) reordered to the library's (n, x, y)."""
+    i_n, i_h, i_w, i_c = I.shape
+    o_h, o_w = orc.out_dim(i_h, k_h, s_h), orc.out_dim(i_w, k_w, s_w)
+    M = orc.im2col(host(I), k_h, k_w, s_h, s_w).reshape(i_n, o_h, o_w, k_h, k_w, i_c)
+    return np.ascontiguousarray(M.transpose(0, 2, 1, 3, 4, 5))
+
+
+@pytest.mark.parametrize("dims", SWEEP + SWEEP_BF16)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_im2col_bitwise_sweep(orc, dims, dtype):
+    say("im2col", dtype, dims)
+    I, _ = case(13 * sum(dims), dims, dtype=dtype)
+    k_h, k_w, k_c, s_h, s_w = dims[4:]
+    ref = im2col_ref(orc, I, k_h, k_w, s_h, s_w)
+    M = mec.im2col(to_dev(I), k_h, k_w, k_c, s_h, s_w)
+    torch.cuda.synchronize()
+    got = host(M.cpu())
+    assert got.shape == ref.shape and np.array_equal(got, ref)
+
+
+@pytest.mark.parametrize("dims", SWEEP + SWEEP_BF16)
+def test_conv_im2col_baseline(orc, dims):
+    """The im2col + product baseline computes the same convolution."""
+    say("conv im2col", dims)
+    I, K = case(17 + sum(dims), dims, dist="int")
+    s_h, s_w = dims[7], dims[8]
+    ref = orc.conv2d_direct(host(I), host(K), s_h, s_w)
+    got = run_conv(I, K, s_h, s_w, "im2col")
+    assert np.array_equal(got, ref.astype(np.float32))
+    Ib, Kb = I.to(torch.bfloat16), K.to(torch.bfloat16)
+    refb = orc.conv2d_direct(host(Ib), host(Kb), s_h, s_w)
+    assert np.array_equal(run_conv(Ib, Kb, s_h, s_w, "im2col"), refb.astype(np.float32))
+
+
+@pytest.mark.parametrize("dims", [
+    (1, 40, 30, 256, 3, 3, 8, 1, 1),      # fp32 runs of 3 KB: output rows split in blocks
+    (2, 50, 20, 300, 5, 2, 4, 3, 2),      # blocks with stride 3, runs not 16-byte multiples
+    (1, 30, 12, 2000, 3, 4, 3, 1, 3),     # runs of 8000 elements: only a few rows per block
+])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_im2col_row_blocks(orc, dims, dtype):
+    say("im2col row blocks", dtype, dims)
+    I, _ = case(29 + sum(dims), dims, dtype=dtype)
+    k_h, k_w, k_c, s_h, s_w = dims[4:]
+    ref = im2col_ref(orc, I, k_h, k_w, s_h, s_w)
+    M = mec.im2col(to_dev(I), k_h, k_w, k_c, s_h, s_w)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(M.cpu()), ref)
+
+
+def test_im2col_workspace_holds_M(orc):
+    dims = (3, 20, 21, 16, 3, 3, 40, 1, 2)
+    say("im2col workspace", dims)
+    I, K = case(23, dims)
+    k_h, k_w, k_c, s_h, s_w = dims[4:]
+    ws = torch.empty(mec.workspace_bytes(*dims, algo=mec.IM2COL), dtype=torch.uint8, device=DEV)
+    O = mec.conv2d(to_dev(I), to_dev(K), s_h, s_w, algo="im2col", workspace=ws)
+    torch.cuda.synchronize()
+    ref_M = im2col_ref(orc, I, k_h, k_w, s_h, s_w)
+    assert np.array_equal(ws.cpu().numpy().view(np.float32).reshape(ref_M.shape), ref_M)
+    ref = orc.conv2d_direct(host(I), host(K), s_h, s_w)
+    assert rel_l2(O.cpu().numpy(), ref) <= TOL_F32
+
+
 @pytest.mark.parametrize("shift", [1, 2, 3])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_unaligned_tensors(orc, shift, dtype):
@@ -185,6 +255,18 @@ def test_unaligned_tensors(orc, shift, dtype):
         mec.conv2d(Id, Kd, s_h, s_w, algo=algo, O=Od, workspace=ws)
         torch.cuda.synchronize()
         assert np.array_equal(Od.cpu().numpy(), ref), algo
+    # im2col baseline on the same unaligned tensors
+    nM = orc.im2col_elems(*dims)
+    Md = torch.zeros(nM + 8, dtype=tdt, device=DEV)[shift:shift + nM]
+    mec.im2col(Id, k_h, k_w, k_c, s_h, s_w, M=Md)
+    torch.cuda.synchronize()
+    ref_M = im2col_ref(orc, I, k_h, k_w, s_h, s_w)
+    assert np.array_equal(host(Md.cpu()).reshape(ref_M.shape), ref_M)
+    wsM = torch.zeros(nM * es + 64, dtype=torch.uint8, device=DEV)[es * shift:]
+    Od.zero_()
+    mec.conv2d(Id, Kd, s_h, s_w, algo="im2col", O=Od, workspace=wsM)
+    torch.cuda.synchronize()
+    assert np.array_equal(Od.cpu().numpy(), ref), "im2col"
 
 
 @pytest.mark.parametrize("dims", SWEEP[:8])
@@ -283,3 +365,43 @@ def test_layer_full_size_sampled(orc, name):
     assert rel_l2(g1[tuple(idx.T)], ref) <= TOL_F32
     assert torch.equal(O1, O2)
     assert np.isfinite(g1).all()
+
+
+# ---------------------------------------------------------------- Table 2 and the stride sweep
+
+@pytest.mark.parametrize("name", list(wl.TABLE2))
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_table2_layer_all_algos_bitwise(orc, name, dtype):
+    """Each benchmark layer of Table 2 (batch 1, small-integer inputs): MEC from
+    L, MEC fused and the im2col baseline all equal the oracle bit for bit."""
+    layer = wl.table2_layer(name, i_n=1, dtype=dtype, dist="int")
+    say("table2", name, dtype, layer.dims)
+    I, K = wl.make_inputs(layer)
+    s = layer.s_h
+    ref = orc.conv2d_direct(host(I), host(K), s, s)
+    assert np.abs(ref).max() < 2 ** 24
+    for algo in ("lowered", "fused", "im2col"):
+        assert np.array_equal(run_conv(I, K, s, s, algo), ref.astype(np.float32)), algo
+
+
+@pytest.mark.parametrize("name", ["cv1", "cv4", "cv5", "cv12"])
+def test_table2_layer_float_inputs(orc, name):
+    layer = wl.table2_layer(name, i_n=2)
+    say("table2 float", name, layer.dims)
+    I, K = wl.make_inputs(layer)
+    s = layer.s_h
+    ref = orc.conv2d_direct(host(I), host(K), s, s)
+    for algo in ("lowered", "fused", "im2col"):
+        assert rel_l2(run_conv(I, K, s, s, algo), ref) <= TOL_F32, algo
+
+
+@pytest.mark.parametrize("stride", list(range(1, 11)))
+def test_stride_sweep_cv1_bitwise(orc, stride):
+    """cv1 with s = 1..10 (Fig. 4(a)), including s >= k_w / 2 and the strides
+    where s does not divide i - k."""
+    layer = wl.table2_layer("cv1", i_n=1, stride=stride, dist="int")
+    say("stride sweep", stride, layer.dims)
+    I, K = wl.make_inputs(layer)
+    ref = orc.conv2d_direct(host(I), host(K), stride, stride).astype(np.float32)
+    for algo in ("lowered", "fused", "im2col"):
+        assert np.array_equal(run_conv(I, K, stride, stride, algo), ref), algo
