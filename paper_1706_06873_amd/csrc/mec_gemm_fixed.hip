@@ -27,6 +27,7 @@ struct FixedParams {
     int64_t a_xstride;  // elements between consecutive rows x of one pair's source
     int32_t nchunks, h_tiles, n_tiles;
     uint32_t ntiles;
+    int32_t o_vec;      // k_c % 4 == 0 and O 16-byte aligned: O rows stored 16 bytes per lane
 };
 
 // ---------------------------------------------------------------- fp32 kernel
@@ -62,7 +63,9 @@ struct F32Cfg {
     static constexpr int NG = NT / 4;                   // 4-channel groups
     static constexpr int B_ITEMS = KH * KT * NG;        // (a, r, 4-channel group)
     static constexpr int BJ = (B_ITEMS + THREADS - 1) / THREADS;
-    static constexpr size_t LDS_BYTES = 2 * STAGE * sizeof(E);
+    static constexpr int EPI_WORDS = WAVES * 32 * 40;   // epilogue: one 32x40 block per wave
+    static constexpr int LDS_WORDS = 2 * STAGE > EPI_WORDS ? 2 * STAGE : EPI_WORDS;
+    static constexpr size_t LDS_BYTES = LDS_WORDS * sizeof(E);
     static_assert(WAVES % WAVES_H == 0 && HT % WAVES_H == 0 && NB % WAVES_N == 0, "wave split");
     static_assert(KT % 2 == 0 && KT % VA == 0 && (VB == 1 || VB == 4), "chunk");
     static_assert(LDS_BYTES + 1024 <= 160 * 1024, "LDS");
@@ -74,7 +77,7 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_kernel(FixedParams p
     constexpr int KH = C::kKH, SH = C::kSH, HROWS = C::HROWS, XW = C::XW, RG = C::RG, NG = C::NG;
     constexpr int A_SIZE = C::A_SIZE, STAGE = C::STAGE, AJ = C::AJ, BJ = C::BJ;
 
-    __shared__ __align__(16) uint32_t lds[2 * STAGE];
+    __shared__ __align__(16) uint32_t lds[C::LDS_WORDS];
     __shared__ int64_t abase_s[kPairs];
     __shared__ int64_t obase_s[kPairs];
 
@@ -165,26 +168,24 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_kernel(FixedParams p
 
     VecN<VA, uint32_t> areg[AJ][4];
     VecN<4, uint32_t> breg[BJ];
-    // global -> registers for r-chunk rc; FULL: no entry needs predication
-    auto load_stage = [&](int rc, auto full_tag) {
+    // global -> registers for r-chunk rc, one load ("piece") at a time: pieces
+    // 0 .. 4*AJ-1 are the A loads (item j, pair q), the rest the K loads.
+    // FULL: no entry needs predication.
+    constexpr int NPA = AJ * 4, NP = NPA + BJ;
+    auto load_piece = [&](int rc, auto full_tag, int pc) {
         constexpr bool FULL = decltype(full_tag)::value;
         const uint32_t r0 = (uint32_t)(rc * KT);
-#pragma unroll
-        for (int j = 0; j < AJ; ++j) {
+        if (pc < NPA) {
+            const int j = pc / 4, q = pc % 4;
             if (FULL && (j + 1) * C::THREADS <= C::A_ITEMS) {
-#pragma unroll
-                for (int q = 0; q < 4; ++q) areg[j][q].load(Atile + (ag[j][q] + r0));
+                areg[j][q].load(Atile + (ag[j][q] + r0));
             } else {
-                const bool rok = (int64_t)r0 + ar[j] < p.R;
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    areg[j][q].zero();
-                    if (rok && ag[j][q] != 0xffffffffu) areg[j][q].load(Atile + (ag[j][q] + r0));
-                }
+                areg[j][q].zero();
+                if ((int64_t)r0 + ar[j] < p.R && ag[j][q] != 0xffffffffu)
+                    areg[j][q].load(Atile + (ag[j][q] + r0));
             }
-        }
-#pragma unroll
-        for (int j = 0; j < BJ; ++j) {
+        } else {
+            const int j = pc - NPA;
             const uint32_t off = bg[j] + (uint32_t)rc * kstep;
             if (FULL && VB == 4 && (j + 1) * C::THREADS <= C::B_ITEMS) {
                 breg[j].load(Kg + off);
@@ -201,6 +202,10 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_kernel(FixedParams p
                 }
             }
         }
+    };
+    auto load_stage = [&](int rc, auto full_tag) {
+#pragma unroll
+        for (int pc = 0; pc < NP; ++pc) load_piece(rc, full_tag, pc);
     };
     auto store_stage = [&](int buf) {
         uint32_t* st = lds + buf * STAGE;
@@ -238,9 +243,13 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_kernel(FixedParams p
     const int a_lane = (wh * HW * SH) * KT * kPairs + kofs * kPairs + row;
     const int b_lane = A_SIZE + kofs * NT + (wn * NBW) * 32 + row;
 
-    // The MFMAs of one r-chunk; `mid` runs after the first k-step's MFMAs are
-    // issued, so the next chunk's global loads overlap the matrix pipe.
-    auto compute = [&](int buf, auto mid) {
+    // The MFMAs of one r-chunk. After k-step ks, issue(ks) issues its share of
+    // the next chunk's global loads: they are spread over the first half of the
+    // chunk so that the wave never stalls on a burst of loads with the matrix
+    // pipe idle, and still have half a chunk to land.
+    constexpr int KS = KT / 2;                    // MFMA k-steps per chunk
+    constexpr int KSL = KS > 1 ? KS / 2 : 1;      // k-steps that issue loads
+    auto compute = [&](int buf, auto issue) {
         const uint32_t* As = lds + buf * STAGE + a_lane;
         const uint32_t* Bs = lds + buf * STAGE + b_lane;
 #pragma unroll
@@ -262,7 +271,8 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_kernel(FixedParams p
                     for (int nb = 0; nb < NBW; ++nb)
                         acc[hw][nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[hw * SH + a], bf[a][nb],
                                                                          acc[hw][nb], 0, 0, 0);
-            if (kk == 0) mid();
+            const int ks = kk / 2;
+            if (ks < KSL) issue(ks * NP / KSL, (ks + 1) * NP / KSL);
         }
     };
 
@@ -272,8 +282,10 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_kernel(FixedParams p
         __syncthreads();
         for (int rc = 0; rc < p.nchunks; ++rc) {
             const bool more = rc + 1 < p.nchunks;
-            compute(rc & 1, [&] {
-                if (more) load_stage(rc + 1, full_tag);
+            compute(rc & 1, [&](int pc0, int pc1) {
+                if (more)
+#pragma unroll
+                    for (int pc = pc0; pc < pc1; ++pc) load_piece(rc + 1, full_tag, pc);
             });
             if (more) store_stage((rc + 1) & 1);
             __syncthreads();
@@ -285,6 +297,35 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_kernel(FixedParams p
         main_loop(std::false_type{});
 
     const int64_t ostride_h = p.o_w * p.k_c;
+    if (p.o_vec) {
+        // Through LDS (free since the loop's last barrier): each 32x32 block is
+        // written row-major (rows 40 floats apart), then read back as four
+        // 16-byte pieces per lane, so every lane stores 16 contiguous bytes of
+        // an O row and a store instruction covers 8 whole 128-byte row segments.
+        float* blk = reinterpret_cast<float*>(lds) + wave * (32 * 40);
+        const int rr = lane >> 3, cc = (lane & 7) * 4;
+#pragma unroll
+        for (int hw = 0; hw < HW; ++hw) {
+            const int64_t h = h0 + wh * HW + hw;
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb) {
+#pragma unroll
+                for (int v = 0; v < 16; ++v) blk[acc_row(v, lane) * 40 + row] = acc[hw][nb][v];
+                __syncthreads();
+                const int c = n0 + (wn * NBW + nb) * 32 + cc;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int r = rr + 8 * i;
+                    const float4 val = *reinterpret_cast<const float4*>(blk + r * 40 + cc);
+                    const int64_t ob = obase_s[r];
+                    if (h < p.o_h && c < p.k_c && ob >= 0)
+                        *reinterpret_cast<float4*>(p.O + ob + h * ostride_h + c) = val;
+                }
+                __syncthreads();
+            }
+        }
+        return;
+    }
 #pragma unroll
     for (int hw = 0; hw < HW; ++hw) {
         const int64_t h = h0 + wh * HW + hw;
@@ -333,7 +374,9 @@ struct BF16Cfg {
     static constexpr int AJ = (A_ITEMS + THREADS - 1) / THREADS;
     static constexpr int B_ITEMS = KH * RG * (NT / 8);      // (a, 8-r group, 8-channel group)
     static constexpr int BJ = (B_ITEMS + THREADS - 1) / THREADS;
-    static constexpr size_t LDS_BYTES = 2 * STAGE * sizeof(E);
+    static constexpr int EPI_HALVES = WAVES * 32 * 40 * 2;  // epilogue: one 32x40 fp32 block per wave
+    static constexpr int LDS_HALVES = 2 * STAGE > EPI_HALVES ? 2 * STAGE : EPI_HALVES;
+    static constexpr size_t LDS_BYTES = LDS_HALVES * sizeof(E);
     static_assert(WAVES % WAVES_H == 0 && HT % WAVES_H == 0 && NB % WAVES_N == 0, "wave split");
     static_assert(KT % 16 == 0, "chunk");
     static_assert(LDS_BYTES + 1024 <= 160 * 1024, "LDS");
@@ -362,7 +405,7 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_bf16_kernel(FixedParams 
     constexpr int KH = C::kKH, SH = C::kSH, HROWS = C::HROWS, XW = C::XW, RG = C::RG;
     constexpr int A_SIZE = C::A_SIZE, STAGE = C::STAGE, AJ = C::AJ, BJ = C::BJ;
 
-    __shared__ __align__(16) uint16_t lds[2 * STAGE];
+    __shared__ __align__(16) uint16_t lds[C::LDS_HALVES];
     __shared__ int64_t abase_s[kPairs];
     __shared__ int64_t obase_s[kPairs];
 
@@ -541,6 +584,32 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_bf16_kernel(FixedParams 
         main_loop(std::false_type{});
 
     const int64_t ostride_h = p.o_w * p.k_c;
+    if (p.o_vec) {
+        // 16-byte O stores through LDS, as in the fp32 kernel
+        float* blk = reinterpret_cast<float*>(lds) + wave * (32 * 40);
+        const int rr = lane >> 3, cc = (lane & 7) * 4;
+#pragma unroll
+        for (int hw = 0; hw < HW; ++hw) {
+            const int64_t h = h0 + wh * HW + hw;
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb) {
+#pragma unroll
+                for (int v = 0; v < 16; ++v) blk[acc_row(v, lane) * 40 + row] = acc[hw][nb][v];
+                __syncthreads();
+                const int c = n0 + (wn * NBW + nb) * 32 + cc;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int r = rr + 8 * i;
+                    const float4 val = *reinterpret_cast<const float4*>(blk + r * 40 + cc);
+                    const int64_t ob = obase_s[r];
+                    if (h < p.o_h && c < p.k_c && ob >= 0)
+                        *reinterpret_cast<float4*>(p.O + ob + h * ostride_h + c) = val;
+                }
+                __syncthreads();
+            }
+        }
+        return;
+    }
 #pragma unroll
     for (int hw = 0; hw < HW; ++hw) {
         const int64_t h = h0 + wh * HW + hw;
@@ -615,6 +684,7 @@ hipError_t run_fixed(const Shape& s, const void* A, const void* K, float* O, hip
     const int64_t ntiles = pair_tiles * p.h_tiles * p.n_tiles;
     if (ntiles > 0x7fffffff) return hipErrorInvalidValue;
     p.ntiles = (uint32_t)ntiles;
+    p.o_vec = s.k_c % 4 == 0 && ((uintptr_t)O & 15u) == 0;
     hipLaunchKernelGGL(KernelOf<C>::fn, dim3(p.ntiles), dim3(KernelOf<C>::threads), 0, stream, p);
     return hipGetLastError();
 }
@@ -627,7 +697,8 @@ template <bool F> using F32K3S1Wide = F32Cfg<14, 2, 2, 16, 3, 1, 4, 4, F>;
 template <bool F> using F32K3S1Wide4 = F32Cfg<4, 2, 2, 16, 3, 1, 4, 4, F>;
 template <bool F> using F32K3S1Wide2 = F32Cfg<2, 2, 2, 16, 3, 1, 4, 4, F>;
 // fp32, 3x3 stride 1, short rows (R = 3 i_c with i_c not a multiple of 4).
-template <bool F> using F32K3S1Narrow = F32Cfg<8, 2, 4, 2, 3, 1, 1, 1, F>;
+template <bool F> using F32K3S1Narrow = F32Cfg<8, 2, 4, 2, 3, 1, 1, 4, F>;
+template <bool F> using F32K3S1NarrowScalar = F32Cfg<8, 2, 4, 2, 3, 1, 1, 1, F>;
 // fp32, 11x11 stride 4, 96-channel tiles. From L: 32 pairs x 4 rows (23 staged
 // rows), r-chunks of 4. From I: 8 waves, 32 pairs x 8 rows (39 staged rows),
 // r-chunks of 2. VB = 4 loads K four channels at a time (k_c % 4 == 0).
@@ -688,6 +759,7 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
             MEC_TRY_FIXED(F32K3S1Wide<F>);
         }
         MEC_TRY_FIXED(F32K3S1Narrow<F>);
+        MEC_TRY_FIXED(F32K3S1NarrowScalar<F>);
         MEC_TRY_FIXED(F32K7S2Wide<F>);
         MEC_TRY_FIXED(F32K7S2Narrow<F>);
         MEC_TRY_FIXED(F32K7S2Scalar<F>);
