@@ -223,9 +223,10 @@ hipError_t launch_strip(const Shape& s, const void* I, void* L, hipStream_t stre
     const int64_t es = sizeof(E);
     const int64_t row_bytes = s.i_w * s.i_c * es;
     // Hb rows per workgroup: chunks of about 1 KB of L, enough workgroups to
-    // fill the chip (about 1024), and Hb rows within the LDS limit.
+    // fill the chip (about 512, two per compute unit), and Hb rows within the
+    // LDS limit.
     int64_t hb = (1024 + s.R * es - 1) / (s.R * es);
-    const int64_t by_count = (s.i_n * s.i_h) / 1024;
+    const int64_t by_count = (s.i_n * s.i_h) / 512;
     if (hb > by_count) hb = by_count;
     if (hb > kStripLdsLimit / row_bytes) hb = kStripLdsLimit / row_bytes;
     if (hb > s.i_h) hb = s.i_h;
