@@ -41,6 +41,7 @@ struct Args {
     GemmParams g;
     Lds lds;
     FastDiv div_hrows;
+    int32_t o_vec;  // k_c % 4 == 0 and O 16-byte aligned: O rows stored 16 bytes per lane
 };
 
 // PF: stage through registers so the next chunk's global loads overlap this
@@ -272,6 +273,34 @@ __global__ __launch_bounds__(kThreads) void slab_gemm_kernel(Args args) {
 
     // epilogue: lane holds C[i][j], j = lane % 32, i = (v/4)*8 + (lane/32)*4 + v%4
     const int64_t ostride_h = p.o_w * p.k_c;
+    if (args.o_vec) {
+        // Through LDS (the stages are free after the loop's last barrier): each
+        // 32x32 block is written row-major (rows 40 floats apart) and read back
+        // as 16-byte pieces, so each lane stores 16 contiguous bytes of an O row.
+        float* blk = reinterpret_cast<float*>(stages) + wave * (32 * 40);
+        const int rr = lane >> 3, cc = (lane & 7) * 4;
+#pragma unroll
+        for (int hw = 0; hw < HW; ++hw) {
+            const int64_t h = h0 + wh * HW + hw;
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb) {
+#pragma unroll
+                for (int v = 0; v < 16; ++v) blk[acc_row(v, lane) * 40 + row] = acc[hw][nb][v];
+                __syncthreads();
+                const int c = n0 + (wn * NBW + nb) * 32 + cc;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int r = rr + 8 * i;
+                    const float4 val = *reinterpret_cast<const float4*>(blk + r * 40 + cc);
+                    const int64_t ob = obase[r];
+                    if (h < p.o_h && c < p.k_c && ob >= 0)
+                        *reinterpret_cast<float4*>(p.O + ob + h * ostride_h + c) = val;
+                }
+                __syncthreads();
+            }
+        }
+        return;
+    }
 #pragma unroll
     for (int hw = 0; hw < HW; ++hw) {
         const int64_t h = h0 + wh * HW + hw;
@@ -347,8 +376,11 @@ hipError_t run(const Shape& s, const void* A, const void* K, float* O, hipStream
     g.ntiles = (uint32_t)ntiles;
     args.lds = lds_layout<C>(g.hrows, (int)s.k_h);
     args.div_hrows = FastDiv((uint32_t)g.hrows);
-    hipLaunchKernelGGL(slab_gemm_kernel<C>, dim3(g.ntiles), dim3(kThreads), lds_bytes<C>(args.lds),
-                       stream, args);
+    args.o_vec = s.k_c % 4 == 0 && aligned16(O);
+    // the epilogue reuses the stage memory for one 32x40 fp32 block per wave
+    const size_t epi = 2 * kPairs * sizeof(int64_t) + (size_t)(kThreads / 64) * 32 * 40 * sizeof(float);
+    const size_t lds = lds_bytes<C>(args.lds) > epi ? lds_bytes<C>(args.lds) : epi;
+    hipLaunchKernelGGL(slab_gemm_kernel<C>, dim3(g.ntiles), dim3(kThreads), lds, stream, args);
     return hipGetLastError();
 }
 

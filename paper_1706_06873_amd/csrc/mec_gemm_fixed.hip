@@ -724,6 +724,8 @@ template <bool F> using F32K1S1Scalar = F32Cfg<8, 2, 2, 4, 1, 1, 1, 1, F>;
 template <bool F> using BF16K1S1 = BF16Cfg<7, 8, 1, 32, 1, 1, F, 8>;
 // bf16, 3x3 stride 1: 8 waves, 32 pairs x 14 rows x 128 channels, r-chunks of 32.
 template <bool F> using BF16K3S1 = BF16Cfg<14, 4, 2, 32, 3, 1, F, 8>;
+template <bool F> using BF16K3S1R4 = BF16Cfg<4, 4, 2, 32, 3, 1, F, 8>;
+template <bool F> using BF16K3S1R2 = BF16Cfg<2, 4, 2, 32, 3, 1, F, 8>;
 
 // Of tiles that differ only in their number of output rows, the one that
 // minimises (rounds of tiles over the 256 compute units) x (input rows each
@@ -775,7 +777,12 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
         MEC_TRY_FIXED(F32K1S1Narrow<F>);
         MEC_TRY_FIXED(F32K1S1Scalar<F>);
     } else {
-        MEC_TRY_FIXED(BF16K3S1<F>);
+        {
+            const int ht = s.k_h == 3 && s.s_h == 1 ? pick_rows(s, 128, {14, 4, 2}) : 14;
+            if (ht == 2) MEC_TRY_FIXED(BF16K3S1R2<F>);
+            if (ht == 4) MEC_TRY_FIXED(BF16K3S1R4<F>);
+            MEC_TRY_FIXED(BF16K3S1<F>);
+        }
         MEC_TRY_FIXED(BF16K1S1<F>);
     }
 #undef MEC_TRY_FIXED
