@@ -244,11 +244,13 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_kernel(FixedParams p
     const int b_lane = A_SIZE + kofs * NT + (wn * NBW) * 32 + row;
 
     // The MFMAs of one r-chunk. After k-step ks, issue(ks) issues its share of
-    // the next chunk's global loads: they are spread over the first half of the
-    // chunk so that the wave never stalls on a burst of loads with the matrix
-    // pipe idle, and still have half a chunk to land.
+    // the next chunk's global loads. When a k-step carries enough MFMAs to cover
+    // them, the loads are spread over the first half of the chunk so that the
+    // wave never stalls on a burst of loads with the matrix pipe idle, and still
+    // have half a chunk to land; with few MFMAs per k-step they all go out after
+    // the first one, to have as long as possible to land.
     constexpr int KS = KT / 2;                    // MFMA k-steps per chunk
-    constexpr int KSL = KS > 1 ? KS / 2 : 1;      // k-steps that issue loads
+    constexpr int KSL = (KH * HW * NBW >= 8 && KS > 1) ? KS / 2 : 1;  // k-steps that issue loads
     auto compute = [&](int buf, auto issue) {
         const uint32_t* As = lds + buf * STAGE + a_lane;
         const uint32_t* Bs = lds + buf * STAGE + b_lane;
