@@ -22,7 +22,8 @@
 // v_mfma_f32_32x32x2_f32 (each lane supplies A[pair][k] and B[k][col] for one
 // k); bf16 uses v_mfma_f32_32x32x16_bf16 (8 consecutive k per lane) with fp32
 // accumulation. The epilogue stores each accumulator straight into n-h-w-c O,
-// which replaces Solution A's h-n-w-c result and its transposition.
+// which replaces Solution A's h-n-w-c result and its transposition, with
+// non-temporal stores (O is not read again by the kernel).
 #include "mec_mfma.h"
 
 namespace mec {
@@ -294,7 +295,7 @@ __global__ __launch_bounds__(kThreads) void slab_gemm_kernel(Args args) {
                     const float4 val = *reinterpret_cast<const float4*>(blk + r * 40 + cc);
                     const int64_t ob = obase[r];
                     if (h < p.o_h && c < p.k_c && ob >= 0)
-                        *reinterpret_cast<float4*>(p.O + ob + h * ostride_h + c) = val;
+                        store_o4_nt(p.O + ob + h * ostride_h + c, val);
                 }
                 __syncthreads();
             }
@@ -312,7 +313,7 @@ __global__ __launch_bounds__(kThreads) void slab_gemm_kernel(Args args) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 const int64_t ob = obase[acc_row(v, lane)];
-                if (ob >= 0) p.O[ob + h * ostride_h + c] = acc[hw][nb][v];
+                if (ob >= 0) __builtin_nontemporal_store(acc[hw][nb][v], p.O + ob + h * ostride_h + c);
             }
         }
     }

@@ -10,7 +10,8 @@
 // in registers as well as in LDS. Staging offsets are computed once per tile,
 // relative to the tile's first pair so they fit 32-bit registers; the next
 // r-chunk's global loads are issued after the first MFMA k-step of the current
-// one, and their LDS stores go to the other of two stage buffers.
+// one, and their LDS stores go to the other of two stage buffers. O is written
+// n-h-w-c with non-temporal stores.
 #include <initializer_list>
 #include <type_traits>
 
@@ -321,7 +322,7 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_kernel(FixedParams p
                     const float4 val = *reinterpret_cast<const float4*>(blk + r * 40 + cc);
                     const int64_t ob = obase_s[r];
                     if (h < p.o_h && c < p.k_c && ob >= 0)
-                        *reinterpret_cast<float4*>(p.O + ob + h * ostride_h + c) = val;
+                        store_o4_nt(p.O + ob + h * ostride_h + c, val);
                 }
                 __syncthreads();
             }
@@ -339,7 +340,7 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_kernel(FixedParams p
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 const int64_t ob = obase_s[acc_row(v, lane)];
-                if (ob >= 0) p.O[ob + h * ostride_h + c] = acc[hw][nb][v];
+                if (ob >= 0) __builtin_nontemporal_store(acc[hw][nb][v], p.O + ob + h * ostride_h + c);
             }
         }
     }
@@ -605,7 +606,7 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_bf16_kernel(FixedParams 
                     const float4 val = *reinterpret_cast<const float4*>(blk + r * 40 + cc);
                     const int64_t ob = obase_s[r];
                     if (h < p.o_h && c < p.k_c && ob >= 0)
-                        *reinterpret_cast<float4*>(p.O + ob + h * ostride_h + c) = val;
+                        store_o4_nt(p.O + ob + h * ostride_h + c, val);
                 }
                 __syncthreads();
             }
@@ -623,7 +624,7 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_bf16_kernel(FixedParams 
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 const int64_t ob = obase_s[acc_row(v, lane)];
-                if (ob >= 0) p.O[ob + h * ostride_h + c] = acc[hw][nb][v];
+                if (ob >= 0) __builtin_nontemporal_store(acc[hw][nb][v], p.O + ob + h * ostride_h + c);
             }
         }
     }

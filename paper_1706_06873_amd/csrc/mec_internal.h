@@ -111,5 +111,15 @@ __device__ inline uint32_t xcd_remap(uint32_t b, uint32_t G) {
     const uint32_t base = G >> 3, rem = G & 7u;
     return xcd * base + (xcd < rem ? xcd : rem) + slot;
 }
+
+// 16-byte store of four output values that bypasses the caches' retention
+// policy: O is written once and not read back by the kernel, so streaming it
+// out keeps dirty O lines from being evicted later, on the time of whichever
+// kernel runs next.
+__device__ inline void store_o4_nt(float* dst, const float4& v) {
+    typedef float f32x4 __attribute__((ext_vector_type(4)));
+    const f32x4 t = {v.x, v.y, v.z, v.w};
+    __builtin_nontemporal_store(t, reinterpret_cast<f32x4*>(dst));
+}
 }  // namespace mec
 #endif

@@ -88,63 +88,91 @@ struct StripParams {
     const void* I;
     void* L;
     uint32_t i_h, o_w, rowlen, R, swic, Hb, hblocks, vpw, nblocks;
+    uint32_t extra;      // rows staged beyond the chunk: a granule may reach into them
+    int32_t in_total;    // elements of I (bound of the staging loads)
+    int32_t ioff, loff;  // elements from the 16-byte boundary below I and below L
     FastDiv div_hblocks, div_R, div_vpw;
 };
 
-// VECIN: input rows are 16-byte vectors; VECOUT: L is 16-byte aligned.
-template <typename E, bool VECIN, bool VECOUT>
+// Chunk j of column (n, w) is written by workgroup (n, j). Ownership goes by
+// 16-byte granule of L: the workgroup writes every granule whose first
+// address lies in its chunk, L[n, w, h0 : h0+Hb, :], so no granule inside a
+// column is split between workgroups and every store there is one 16-byte
+// vector; only the granules that straddle two columns (or the ends of L) are
+// written element by element, each column's part by its own workgroup. A
+// granule starting near the chunk's end reaches into the next rows, so the
+// workgroup stages `extra` rows past its chunk. The staged rows are one
+// contiguous span of I, loaded as 16-byte granules of I, with element loads
+// for the granules that cross either end of I.
+template <typename E>
 __global__ __launch_bounds__(kStripThreads) void lower_strip_kernel(StripParams p) {
     constexpr int VEC = Vec16<E>::N;
     extern __shared__ u32x4 strip4[];
     E* rows = reinterpret_cast<E*>(strip4);
     const uint32_t blk = xcd_remap(blockIdx.x, p.nblocks);
-    const uint32_t n = p.div_hblocks.div(blk), h0 = (blk - n * p.hblocks) * p.Hb;
-    const uint32_t hb = min(p.Hb, p.i_h - h0);
-    const uint32_t nin = hb * p.rowlen;
-    const E* __restrict__ I = reinterpret_cast<const E*>(p.I) + ((size_t)n * p.i_h + h0) * p.rowlen;
-    if (VECIN) {
-        for (uint32_t i = threadIdx.x; i < nin / VEC; i += kStripThreads)
-            strip4[i] = reinterpret_cast<const u32x4*>(I)[i];
-    } else {
-        for (uint32_t i = threadIdx.x; i < nin; i += kStripThreads) rows[i] = I[i];
+    const uint32_t n = p.div_hblocks.div(blk), j = blk - n * p.hblocks;
+    const uint32_t h0 = j * p.Hb;
+    const uint32_t hend = min(h0 + p.Hb, p.i_h);          // chunk rows [h0, hend)
+    const uint32_t sh = min(hend + p.extra, p.i_h) - h0;  // staged rows
+    {
+        // span [first, first + nin) of I; granules of I start at k*VEC - ioff
+        const int32_t first = (int32_t)((n * p.i_h + h0) * p.rowlen);
+        const int32_t nin = (int32_t)(sh * p.rowlen);
+        const int32_t a0 = ((first + p.ioff) & ~(VEC - 1)) - p.ioff;
+        const int32_t nv = (first - a0 + nin + VEC - 1) / VEC;
+        const E* __restrict__ I = reinterpret_cast<const E*>(p.I);
+        for (int32_t i = threadIdx.x; i < nv; i += kStripThreads) {
+            const int32_t a = a0 + i * VEC;
+            if (a >= 0 && a + VEC <= p.in_total) {
+                strip4[i] = *reinterpret_cast<const u32x4*>(I + a);
+            } else {
+                for (int32_t k = 0; k < VEC; ++k)
+                    if (a + k >= 0 && a + k < p.in_total) rows[i * VEC + k] = I[a + k];
+            }
+        }
     }
     __syncthreads();
+    const uint32_t shift = (uint32_t)((((n * p.i_h + h0) * p.rowlen) + p.ioff) & (VEC - 1));
 
-    const uint32_t len = hb * p.R;  // elements of the chunk L[n, w, h0:h0+hb, :]
     E* __restrict__ L = reinterpret_cast<E*>(p.L);
+    const int64_t col_len = (int64_t)p.i_h * p.R;
     const uint32_t total = p.o_w * p.vpw;
     for (uint32_t f = threadIdx.x; f < total; f += kStripThreads) {
         const uint32_t w = p.div_vpw.div(f);
         const uint32_t v = f - w * p.vpw;
-        const size_t g0 = (((size_t)n * p.o_w + w) * p.i_h + h0) * p.R;  // chunk start in L
-        // the chunk is covered by the 16-byte-aligned vectors starting at a0
-        const size_t a0 = VECOUT ? g0 & ~(size_t)(VEC - 1) : g0;
-        const size_t gv = a0 + (size_t)v * VEC;
-        if (gv >= g0 + len) continue;
-        const int e0 = (int)((long long)gv - (long long)g0);  // chunk index of the vector's first element
-        uint32_t ee = e0 < 0 ? 0u : (uint32_t)e0;
-        uint32_t r = p.div_R.div(ee), c = ee - r * p.R;
-        const E* src = rows + w * p.swic;
+        const int64_t base = ((int64_t)n * p.o_w + w) * col_len;  // column start in L
+        // granules of L start at k*VEC - loff; the first one of chunk 0 may
+        // start before the column
+        const int64_t from = base + (int64_t)h0 * p.R + (j == 0 ? 0 : VEC - 1);
+        const int64_t lo = ((from + p.loff) & ~(int64_t)(VEC - 1)) - p.loff;
+        const int64_t hi = base + (int64_t)hend * p.R;  // granule starts below hi
+        const int64_t gv = lo + (int64_t)v * VEC;
+        if (gv >= hi) continue;
+        const int e0 = (int)(gv - base);  // column index of the granule's first element
+        const uint32_t ee = e0 < 0 ? 0u : (uint32_t)e0;
+        const uint32_t r = p.div_R.div(ee);
+        uint32_t c = ee - r * p.R;
+        const E* src = rows + shift + w * p.swic + (r - h0) * p.rowlen;
         Vec16<E> val;
 #pragma unroll
         for (int k = 0; k < VEC; ++k) {
             const int e = e0 + k;
             val.e[k] = E(0);
-            if (e >= 0 && e < (int)len) {
-                val.e[k] = src[r * p.rowlen + c];
+            if (e >= 0 && e < (int)col_len) {
+                val.e[k] = src[c];
                 if (++c == p.R) {
                     c = 0;
-                    ++r;
+                    src += p.rowlen;
                 }
             }
         }
-        if (VECOUT && e0 >= 0 && e0 + VEC <= (int)len) {
+        if (e0 >= 0 && e0 + VEC <= (int)col_len) {
             __builtin_nontemporal_store(val.v, reinterpret_cast<u32x4*>(L + gv));
         } else {
 #pragma unroll
             for (int k = 0; k < VEC; ++k) {
                 const int e = e0 + k;
-                if (e >= 0 && e < (int)len) L[gv + k] = val.e[k];
+                if (e >= 0 && e < (int)col_len) L[gv + k] = val.e[k];
             }
         }
     }
@@ -217,18 +245,23 @@ hipError_t launch_rows(const Shape& s, const void* I, void* L, hipStream_t strea
     return hipGetLastError();
 }
 
+// Rows staged past a chunk so that every granule starting in it is covered.
+inline int64_t strip_extra(int64_t R, int VEC) { return (VEC - 2) / R + 1; }
+
 template <typename E>
 hipError_t launch_strip(const Shape& s, const void* I, void* L, hipStream_t stream) {
     constexpr int VEC = Vec16<E>::N;
     const int64_t es = sizeof(E);
     const int64_t row_bytes = s.i_w * s.i_c * es;
+    const int64_t extra = strip_extra(s.R, VEC);
     // Hb rows per workgroup: chunks of about 1 KB of L, enough workgroups to
-    // fill the chip (about 512, two per compute unit), and Hb rows within the
-    // LDS limit.
+    // fill the chip (about 512, two per compute unit), and Hb + extra rows
+    // within the LDS limit (the caller checked that Hb = 1 fits).
     int64_t hb = (1024 + s.R * es - 1) / (s.R * es);
     const int64_t by_count = (s.i_n * s.i_h) / 512;
     if (hb > by_count) hb = by_count;
-    if (hb > kStripLdsLimit / row_bytes) hb = kStripLdsLimit / row_bytes;
+    const int64_t fit = (kStripLdsLimit - 2 * 16) / row_bytes - extra;
+    if (hb > fit) hb = fit;
     if (hb > s.i_h) hb = s.i_h;
     if (hb < 1) hb = 1;
     StripParams p{};
@@ -240,23 +273,20 @@ hipError_t launch_strip(const Shape& s, const void* I, void* L, hipStream_t stre
     p.R = (uint32_t)s.R;
     p.swic = (uint32_t)(s.s_w * s.i_c);
     p.Hb = (uint32_t)hb;
+    p.extra = (uint32_t)extra;
+    p.in_total = (int32_t)(s.i_n * s.i_h * s.i_w * s.i_c);
+    p.ioff = (int32_t)(((uintptr_t)I / es) % VEC);
+    p.loff = (int32_t)(((uintptr_t)L / es) % VEC);
     p.hblocks = (uint32_t)((s.i_h + hb - 1) / hb);
-    p.vpw = (uint32_t)((hb * s.R + VEC - 1) / VEC + 1);
+    p.vpw = (uint32_t)((hb * s.R + VEC - 1) / VEC + 2);
     p.nblocks = (uint32_t)(s.i_n * p.hblocks);
     p.div_hblocks = FastDiv(p.hblocks);
     p.div_R = FastDiv(p.R);
     p.div_vpw = FastDiv(p.vpw);
-    const size_t lds = (size_t)hb * row_bytes;
-    const bool vin = (s.i_w * s.i_c) % VEC == 0 && aligned16(I);
-    const bool vout = aligned16(L);
-#define MEC_STRIP(VI, VO)                                                                      \
-    hipLaunchKernelGGL((lower_strip_kernel<E, VI, VO>), dim3(p.nblocks), dim3(kStripThreads), \
-                       lds, stream, p)
-    if (vin && vout) MEC_STRIP(true, true);
-    else if (vin) MEC_STRIP(true, false);
-    else if (vout) MEC_STRIP(false, true);
-    else MEC_STRIP(false, false);
-#undef MEC_STRIP
+    // staged rows plus up to one granule on each side of the span
+    const int64_t staged = std::min<int64_t>(hb + extra, s.i_h);
+    const size_t lds = (size_t)(staged * row_bytes + 2 * 16);
+    hipLaunchKernelGGL(lower_strip_kernel<E>, dim3(p.nblocks), dim3(kStripThreads), lds, stream, p);
     return hipGetLastError();
 }
 
@@ -300,7 +330,12 @@ hipError_t launch_typed(const Shape& s, const void* I, void* L, hipStream_t stre
     const bool small = s.i_n * s.i_h < (int64_t(1) << 31) && s.i_h * s.R < (int64_t(1) << 31) &&
                        s.o_w * (s.R / VEC + 2) < (int64_t(1) << 31);
     if (small && vec_runs && row_bytes <= kRowsLdsLimit) return launch_rows<E>(s, I, L, stream);
-    if (small && row_bytes <= kStripLdsLimit) return launch_strip<E>(s, I, L, stream);
+    // strip: 32-bit offsets into I and within a workgroup's o_w chunks, and at
+    // least one chunk row plus its extra rows in LDS
+    const bool strip_ok = small && s.i_n * s.i_h * s.i_w * s.i_c < (int64_t(1) << 31) &&
+                          s.o_w * (s.i_h * s.R / VEC + 3) < (int64_t(1) << 31) &&
+                          (1 + strip_extra(s.R, VEC)) * row_bytes + 2 * 16 <= kStripLdsLimit;
+    if (strip_ok) return launch_strip<E>(s, I, L, stream);
     return launch_gather<E>(s, I, L, stream);
 }
 

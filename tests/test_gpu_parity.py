@@ -155,6 +155,44 @@ def test_lower_bitwise_sweep(orc, dims, dtype):
     assert got.shape == ref.shape and np.array_equal(got, ref)
 
 
+# Short or unaligned runs take the strip lowering. Enough images x rows that a
+# workgroup owns chunks of several rows (the chunk height grows with
+# i_n * i_h), with I and L placed off their 16-byte boundaries.
+STRIP_CASES = [
+    (8, 150, 20, 3, 5, 5, 4, 1, 1),       # R = 15
+    (16, 200, 21, 3, 11, 11, 4, 4, 4),    # R = 33, the 11x11 stride-4 layout
+    (12, 256, 13, 1, 1, 1, 2, 1, 1),      # R = 1: a granule spans several rows
+    (6, 180, 40, 2, 3, 1, 3, 2, 2),       # R = 2
+    (8, 160, 19, 5, 3, 3, 4, 1, 2),       # R = 15, stride 2
+]
+
+
+@pytest.mark.parametrize("dims", STRIP_CASES)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("offs", [(0, 0), (1, 3), (3, 1), (2, 5)])
+def test_lower_strip_offsets_and_guards(orc, dims, dtype, offs):
+    """L bit for bit, and nothing written outside it, for I and L starting
+    ioff and loff elements past a 16-byte boundary."""
+    ioff, loff = offs
+    say("lower strip", dtype, dims, offs)
+    I, _ = case(31 * sum(dims) + ioff, dims, dtype=dtype)
+    k_h, k_w, k_c, s_h, s_w = dims[4:]
+    ref = orc.mec_lower(host(I), k_h, k_w, k_c, s_h, s_w)
+    tdt = I.dtype
+    ibuf = torch.zeros(I.numel() + 16, dtype=tdt, device=DEV)
+    Id = ibuf[ioff:ioff + I.numel()].view(I.shape)
+    Id.copy_(I.to(DEV))
+    nL = ref.size
+    guard = 24
+    lbuf = torch.full((nL + 2 * guard,), -3.0, dtype=tdt, device=DEV)
+    Ld = lbuf[guard + loff:guard + loff + nL]
+    mec.lower(Id, k_h, k_w, k_c, s_h, s_w, L=Ld)
+    torch.cuda.synchronize()
+    out = lbuf.cpu()
+    assert np.array_equal(host(out[guard + loff:guard + loff + nL]).reshape(ref.shape), ref)
+    assert bool((out[:guard + loff] == -3.0).all()) and bool((out[guard + loff + nL:] == -3.0).all())
+
+
 def im2col_ref(orc, I, k_h, k_w, s_h, s_w):
     """The oracle's im2col (rows n, y, x) reordered to the library's (n, x, y)."""
     i_n, i_h, i_w, i_c = I.shape
