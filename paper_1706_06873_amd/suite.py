@@ -2,9 +2,13 @@
 
     python -m paper_1706_06873_amd.suite table2 [--batch 32] [--dtype f32|bf16|both]
     python -m paper_1706_06873_amd.suite stride [--batch 32] [--dtype f32]
+    python -m paper_1706_06873_amd.suite resnet101 [--batch 1] [--dtype f32]
 
 ``table2`` runs the twelve layers of Table 2 (cv1-cv12), ``stride`` runs cv1
-(227x227x3 input, 11x11x96 kernel) with s_h = s_w = 1..10 as in Fig. 4(a).
+(227x227x3 input, 11x11x96 kernel) with s_h = s_w = 1..10 as in Fig. 4(a),
+``resnet101`` runs the five layers of Table 3 (cv4, cv9-cv12) and ends with a
+summary line weighing each layer by its count in ResNet-101, as Table 3 does:
+weighted workspace (MiB) and weighted time of MEC against im2col.
 For every layer it times MEC from L (compact lowering + slab products), MEC
 fused, and the im2col baseline (im2col lowering + one product through the
 same kernels), each kernel between HIP events on its stream, on seeded
@@ -95,8 +99,9 @@ def _time_layer(layer, reps, warmup, sets):
 
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
-    ap.add_argument("which", choices=["table2", "stride"])
-    ap.add_argument("--batch", type=int, default=32)
+    ap.add_argument("which", choices=["table2", "stride", "resnet101"])
+    ap.add_argument("--batch", type=int, default=None,
+                    help="images per layer (default 32; 1 for resnet101, as in Table 3)")
     ap.add_argument("--dtype", default="f32", choices=["f32", "bf16", "both"])
     ap.add_argument("--reps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
@@ -107,15 +112,50 @@ def main(argv=None):
         print("the suite needs a GPU", file=sys.stderr)
         return 1
     dtypes = ["f32", "bf16"] if args.dtype == "both" else [args.dtype]
+    batch = args.batch or (1 if args.which == "resnet101" else 32)
     if args.which == "table2":
         names = args.layers.split(",") if args.layers else list(wl.TABLE2)
-        layers = [wl.table2_layer(n, args.batch, d) for d in dtypes for n in names]
+        layers = [wl.table2_layer(n, batch, d) for d in dtypes for n in names]
+    elif args.which == "resnet101":
+        names = args.layers.split(",") if args.layers else list(wl.TABLE3_WEIGHTS)
+        layers = [wl.table2_layer(n, batch, d) for d in dtypes for n in names]
     else:
         strides = [int(x) for x in args.layers.split(",")] if args.layers else list(range(1, 11))
-        layers = [wl.table2_layer("cv1", args.batch, d, stride=s) for d in dtypes for s in strides]
+        layers = [wl.table2_layer("cv1", batch, d, stride=s) for d in dtypes for s in strides]
+    rows = []
     for layer in layers:
-        print(json.dumps(_time_layer(layer, args.reps, args.warmup, args.sets)), flush=True)
+        rows.append(_time_layer(layer, args.reps, args.warmup, args.sets))
+        print(json.dumps(rows[-1]), flush=True)
+    if args.which == "resnet101":
+        for d in dtypes:
+            print(json.dumps(weighted_summary([r for r in rows if r["dtype"] == d], batch)),
+                  flush=True)
     return 0
+
+
+def weighted_summary(rows, batch):
+    """Table 3's weighted totals: each layer's workspace and time times its
+    count in ResNet-101, summed, for MEC (from L and fused) and im2col."""
+    mib = 2.0 ** 20
+    tot = {"workspace_im2col_mib": 0.0, "workspace_mec_mib": 0.0, "im2col_us": 0.0,
+           "mec_lowered_us": 0.0, "mec_fused_us": 0.0}
+    for r in rows:
+        wgt = wl.TABLE3_WEIGHTS[r["layer"]]
+        tot["workspace_im2col_mib"] += wgt * r["workspace_im2col"] / mib
+        tot["workspace_mec_mib"] += wgt * r["workspace_mec"] / mib
+        tot["im2col_us"] += wgt * r["timings"]["im2col"]["us"]
+        tot["mec_lowered_us"] += wgt * r["timings"]["lowered"]["us"]
+        tot["mec_fused_us"] += wgt * r["timings"]["fused"]["us"]
+    out = {"summary": "ResNet-101 weighted (Table 3 layers and weights)", "batch": batch,
+           "dtype": rows[0]["dtype"] if rows else None,
+           "layers": {r["layer"]: wl.TABLE3_WEIGHTS[r["layer"]] for r in rows}}
+    out.update({k: round(v, 3) for k, v in tot.items()})
+    if tot["workspace_mec_mib"] > 0:
+        out["workspace_ratio"] = round(tot["workspace_im2col_mib"] / tot["workspace_mec_mib"], 3)
+    if tot["mec_lowered_us"] > 0:
+        out["time_ratio_lowered"] = round(tot["im2col_us"] / tot["mec_lowered_us"], 3)
+        out["time_ratio_fused"] = round(tot["im2col_us"] / tot["mec_fused_us"], 3)
+    return out
 
 
 if __name__ == "__main__":

@@ -82,6 +82,9 @@ TABLE2 = {
     "cv12": (7, 7, 512, 3, 3, 512, 1),
 }
 
+# Table 3 weighs five Table 2 layers by how often ResNet-101 uses them.
+TABLE3_WEIGHTS = {"cv4": 1, "cv9": 3, "cv10": 4, "cv11": 23, "cv12": 3}
+
 
 def table2_layer(name, i_n=32, dtype="f32", stride=None, dist="u11"):
     """A Table 2 layer at batch i_n; ``stride`` overrides s_h = s_w (the

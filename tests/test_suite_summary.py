@@ -1,0 +1,52 @@
+"""Host logic of the timing suite: Table 3's weighted ResNet-101 summary.
+
+The summary weighs each layer's workspace by its ResNet-101 count; fed the
+library's own workspace sizes at batch 1 in fp32 it must reproduce Table 3's
+memory columns (sums 203.6 MB for im2col and 64.6 MB for MEC, ratio 3.2, the
+paper's MB read as MiB). Timings here are made up: only the arithmetic of the
+weighting is under test, no kernel runs.
+"""
+import json
+import os
+
+import pytest
+
+import paper_1706_06873_amd as mec
+from paper_1706_06873_amd import suite
+from paper_1706_06873_amd import workloads as wl
+from conftest import REPO
+
+GOLDEN = os.path.join(REPO, "tests", "golden", "table3_resnet101_mem.json")
+
+
+def fake_rows(batch=1):
+    rows = []
+    for i, name in enumerate(wl.TABLE3_WEIGHTS):
+        layer = wl.table2_layer(name, batch)
+        rows.append({"layer": layer.name, "dtype": "f32",
+                     "workspace_mec": mec.workspace_bytes(*layer.dims, dtype=mec.F32),
+                     "workspace_im2col": mec.im2col_bytes(*layer.dims, dtype=mec.F32),
+                     "timings": {"im2col": {"us": 10.0 + i}, "lowered": {"us": 4.0 + i},
+                                 "fused": {"us": 2.0 + i}}})
+    return rows
+
+
+def test_weights_match_table3():
+    gold = json.load(open(GOLDEN))
+    assert wl.TABLE3_WEIGHTS == {r["name"]: r["weight"] for r in gold["rows"]}
+
+
+def test_weighted_workspace_reproduces_table3_sums():
+    gold = json.load(open(GOLDEN))
+    s = suite.weighted_summary(fake_rows(), 1)
+    assert s["workspace_im2col_mib"] == pytest.approx(gold["sum"]["conv_mem"], abs=0.1)
+    assert s["workspace_mec_mib"] == pytest.approx(gold["sum"]["mec_mem"], abs=0.1)
+    assert round(s["workspace_ratio"], 1) == gold["ratio"]["conv_mem"]
+
+
+def test_weighted_times():
+    s = suite.weighted_summary(fake_rows(), 1)
+    w = list(wl.TABLE3_WEIGHTS.values())
+    assert s["im2col_us"] == pytest.approx(sum(wi * (10.0 + i) for i, wi in enumerate(w)))
+    assert s["mec_fused_us"] == pytest.approx(sum(wi * (2.0 + i) for i, wi in enumerate(w)))
+    assert s["time_ratio_lowered"] == pytest.approx(s["im2col_us"] / s["mec_lowered_us"], rel=1e-3)
