@@ -19,7 +19,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 _lib = None
 
-F32, BF16 = 0, 1
+F32, BF16, F64 = 0, 1, 2
 
 _i64 = ctypes.c_int64
 _DIMS = [_i64] * 9
@@ -48,6 +48,11 @@ def _load(path):
     L.oracle_mec_conv2d.restype = ctypes.c_int
     L.oracle_vanilla_mec.argtypes = [vp, vp, dp, vp] + [_i64] * 6
     L.oracle_vanilla_mec.restype = None
+    for name in ("oracle_conv2d_dgrad", "oracle_conv2d_wgrad", "oracle_mec_dgrad_lowered",
+                 "oracle_mec_wgrad_lowered", "oracle_mec_fold"):
+        getattr(L, name).argtypes = [vp, vp, dp] if name != "oracle_mec_fold" else [vp, dp]
+        getattr(L, name).argtypes += _DIMS + [ctypes.c_int]
+        getattr(L, name).restype = None
     L.oracle_num_threads.argtypes = []
     L.oracle_num_threads.restype = ctypes.c_int
     return L
@@ -189,6 +194,75 @@ def vanilla_mec(I, K, s_h, s_w):
     L = np.empty((o_w, i_h * k_w), np.float32)
     lib().oracle_vanilla_mec(_ptr(I), _ptr(K), _dptr(O), _ptr(L), i_h, i_w, k_h, k_w, s_h, s_w)
     return O, L
+
+
+# ---------------------------------------------------------------- training
+# Gradients of the convolution (derived from its definition; the paper gives
+# no backward algorithm). G = dloss/dO has O's shape, i_n x o_h x o_w x k_c.
+
+def _grad_dims(G, i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w):
+    o_h, o_w = out_dim(i_h, k_h, s_h), out_dim(i_w, k_w, s_w)
+    if G.shape != (i_n, o_h, o_w, k_c):
+        raise ValueError("G must be i_n x o_h x o_w x k_c = %s, got %s"
+                         % ((i_n, o_h, o_w, k_c), G.shape))
+    return (i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w)
+
+
+def conv2d_dgrad(G, K, i_h, i_w, s_h, s_w):
+    """dI = dloss/dI of the direct convolution (fp64, n-h-w-c)."""
+    k_h, k_w, i_c, k_c = K.shape
+    d = _grad_dims(G, G.shape[0], i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w)
+    dt = _dtype_code(G)
+    assert _dtype_code(K) == dt
+    dI = np.empty((d[0], i_h, i_w, i_c), np.float64)
+    lib().oracle_conv2d_dgrad(_ptr(G), _ptr(K), _dptr(dI), *d, dt)
+    return dI
+
+
+def conv2d_wgrad(I, G, k_h, k_w, s_h, s_w):
+    """dK = dloss/dK of the direct convolution (fp64, k_h x k_w x i_c x k_c)."""
+    i_n, i_h, i_w, i_c = I.shape
+    d = _grad_dims(G, i_n, i_h, i_w, i_c, k_h, k_w, G.shape[3], s_h, s_w)
+    dt = _dtype_code(I)
+    assert _dtype_code(G) == dt
+    dK = np.empty((k_h, k_w, i_c, G.shape[3]), np.float64)
+    lib().oracle_conv2d_wgrad(_ptr(I), _ptr(G), _dptr(dK), *d, dt)
+    return dK
+
+
+def mec_dgrad_lowered(G, K, i_h, i_w, s_h, s_w):
+    """dL = dloss/dL through the slab products (fp64, L's shape)."""
+    k_h, k_w, i_c, k_c = K.shape
+    d = _grad_dims(G, G.shape[0], i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w)
+    dt = _dtype_code(G)
+    assert _dtype_code(K) == dt
+    dL = np.empty((d[0], G.shape[2], i_h, k_w, i_c), np.float64)
+    lib().oracle_mec_dgrad_lowered(_ptr(G), _ptr(K), _dptr(dL), *d, dt)
+    return dL
+
+
+def mec_wgrad_lowered(L, G, k_h, s_h, s_w):
+    """dK as the sum over output rows of A_h^T G_h, A_h the slabs of L (fp64)."""
+    i_n, o_w, i_h, k_w, i_c = L.shape
+    i_w = (o_w - 1) * s_w + k_w
+    d = _grad_dims(G, i_n, i_h, i_w, i_c, k_h, k_w, G.shape[3], s_h, s_w)
+    dt = _dtype_code(L)
+    assert _dtype_code(G) == dt
+    dK = np.empty((k_h, k_w, i_c, G.shape[3]), np.float64)
+    lib().oracle_mec_wgrad_lowered(_ptr(L), _ptr(G), _dptr(dK), *d, dt)
+    return dK
+
+
+def mec_fold(dL, i_w, s_w):
+    """The adjoint of the lowering: dI[n, h, s_w*w + b, c] += dL[n, w, h, b, c]
+    (fp64). dL is float32, bf16 bits (uint16) or float64."""
+    i_n, o_w, i_h, k_w, i_c = dL.shape
+    if out_dim(i_w, k_w, s_w) != o_w:
+        raise ValueError("i_w, s_w do not give o_w = %d columns" % o_w)
+    dt = F64 if dL.dtype == np.float64 else _dtype_code(dL)
+    dI = np.empty((i_n, i_h, i_w, i_c), np.float64)
+    lib().oracle_mec_fold(_ptr(dL), _dptr(dI), i_n, i_h, i_w, i_c, 1, k_w, 1, 1, s_w, dt)
+    return dI
 
 
 def num_threads():

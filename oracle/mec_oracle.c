@@ -15,7 +15,7 @@
  * applied to I already (Section 2.1).
  *
  * Element types of I, K and L: dtype 0 is IEEE fp32, dtype 1 is bfloat16
- * stored as its 16-bit pattern. Every product and sum here is done in fp64;
+ * stored as its 16-bit pattern, dtype 2 is fp64 (accepted where noted). Every product and sum here is done in fp64;
  * bf16 and fp32 values widen to fp64 exactly, so each output is the exact
  * dot product up to one fp64 rounding per addition.
  *
@@ -38,6 +38,7 @@
 
 #define DT_F32 0
 #define DT_BF16 1
+#define DT_F64 2
 
 /* Widen one element of a dtype-tagged array to fp64. Both conversions are
  * exact: a bf16 pattern is the top half of an fp32 pattern. */
@@ -45,6 +46,8 @@ static double elem(const void* base, int64_t idx, int dtype)
 {
     if (dtype == DT_F32) {
         return (double)((const float*)base)[idx];
+    } else if (dtype == DT_F64) {
+        return ((const double*)base)[idx];
     } else {
         uint32_t bits = (uint32_t)((const uint16_t*)base)[idx] << 16;
         float f;
@@ -53,7 +56,7 @@ static double elem(const void* base, int64_t idx, int dtype)
     }
 }
 
-static int64_t elem_bytes(int dtype) { return dtype == DT_F32 ? 4 : 2; }
+static int64_t elem_bytes(int dtype) { return dtype == DT_F32 ? 4 : (dtype == DT_F64 ? 8 : 2); }
 
 /* Eq. (1): o = (i - k) / s + 1, read with floor division. Callers keep
  * i >= k >= 1 and s >= 1, so C's truncating division is the floor. */
@@ -315,6 +318,146 @@ void oracle_im2col(const void* I, void* M,
                             int64_t src = ((n * i_h + (y * s_h + a)) * i_w + (x * s_w + b)) * i_c + c;
                             memcpy((char*)M + dst * es, (const char*)I + src * es, (size_t)es);
                         }
+}
+
+/* ------------------------------------------------------------------------
+ * Training passes. The paper names training as a use of MEC (Section 1, and
+ * the training set-ups of Section 4) but gives no backward algorithm; these
+ * are the derivatives of the direct convolution above, written out. For a
+ * loss with gradient G = dloss/dO (i_n x o_h x o_w x k_c, n-h-w-c), the
+ * definition O[n,y,x,m] = sum_{a,b,c} I[n, y*s_h+a, x*s_w+b, c] K[a,b,c,m]
+ * is linear in I and in K, so
+ *   dI[n, y*s_h+a, x*s_w+b, c] += G[n,y,x,m] K[a,b,c,m]   over all (n,y,x,m,a,b,c)
+ *   dK[a,b,c,m] = sum_{n,y,x} I[n, y*s_h+a, x*s_w+b, c] G[n,y,x,m].
+ * Input pixels no window covers receive 0. G, K and I share one dtype tag
+ * (0 or 1); results are fp64.
+ * ------------------------------------------------------------------------ */
+
+/* dI by the scatter form above. Images are independent, so the loop over n
+ * runs in parallel. */
+void oracle_conv2d_dgrad(const void* G, const void* K, double* dI,
+                         int64_t i_n, int64_t i_h, int64_t i_w, int64_t i_c,
+                         int64_t k_h, int64_t k_w, int64_t k_c,
+                         int64_t s_h, int64_t s_w, int dtype)
+{
+    int64_t o_h = oracle_out_dim(i_h, k_h, s_h);
+    int64_t o_w = oracle_out_dim(i_w, k_w, s_w);
+#pragma omp parallel for schedule(static)
+    for (int64_t n = 0; n < i_n; ++n) {
+        double* d = dI + n * i_h * i_w * i_c;
+        for (int64_t e = 0; e < i_h * i_w * i_c; ++e) d[e] = 0.0;
+        for (int64_t y = 0; y < o_h; ++y)
+            for (int64_t x = 0; x < o_w; ++x)
+                for (int64_t m = 0; m < k_c; ++m) {
+                    double g = elem(G, ((n * o_h + y) * o_w + x) * k_c + m, dtype);
+                    for (int64_t a = 0; a < k_h; ++a)
+                        for (int64_t b = 0; b < k_w; ++b)
+                            for (int64_t c = 0; c < i_c; ++c)
+                                d[((y * s_h + a) * i_w + (x * s_w + b)) * i_c + c] +=
+                                    g * elem(K, ((a * k_w + b) * i_c + c) * k_c + m, dtype);
+                }
+    }
+}
+
+/* dK by the sum above; each kernel element is one independent sum. */
+void oracle_conv2d_wgrad(const void* I, const void* G, double* dK,
+                         int64_t i_n, int64_t i_h, int64_t i_w, int64_t i_c,
+                         int64_t k_h, int64_t k_w, int64_t k_c,
+                         int64_t s_h, int64_t s_w, int dtype)
+{
+    int64_t o_h = oracle_out_dim(i_h, k_h, s_h);
+    int64_t o_w = oracle_out_dim(i_w, k_w, s_w);
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t a = 0; a < k_h; ++a)
+        for (int64_t b = 0; b < k_w; ++b)
+            for (int64_t c = 0; c < i_c; ++c)
+                for (int64_t m = 0; m < k_c; ++m) {
+                    double acc = 0.0;
+                    for (int64_t n = 0; n < i_n; ++n)
+                        for (int64_t y = 0; y < o_h; ++y)
+                            for (int64_t x = 0; x < o_w; ++x)
+                                acc += elem(I, ((n * i_h + (y * s_h + a)) * i_w + (x * s_w + b)) * i_c + c, dtype) *
+                                       elem(G, ((n * o_h + y) * o_w + x) * k_c + m, dtype);
+                    dK[((a * k_w + b) * i_c + c) * k_c + m] = acc;
+                }
+}
+
+/* The same two gradients through MEC's lowered tensor. Forward, output row
+ * h is the slab A_h = L[:, :][s_h*R*h : s_h*R*h + k_h*R] (one row per pair
+ * (n, w), R = k_w*i_c) times K viewed as (k_h*R) x k_c. Differentiating
+ * O_h = A_h K gives, with G_h = G[n, h, w, :] as a (i_n*o_w) x k_c matrix:
+ *   dL:  every slab receives G_h K^T, added where slabs overlap;
+ *   dK:  sum over h of A_h^T G_h.
+ * dL has L's shape (i_n x o_w x i_h x k_w x i_c); rows no slab covers are 0. */
+void oracle_mec_dgrad_lowered(const void* G, const void* K, double* dL,
+                              int64_t i_n, int64_t i_h, int64_t i_w, int64_t i_c,
+                              int64_t k_h, int64_t k_w, int64_t k_c,
+                              int64_t s_h, int64_t s_w, int dtype)
+{
+    int64_t o_h = oracle_out_dim(i_h, k_h, s_h);
+    int64_t o_w = oracle_out_dim(i_w, k_w, s_w);
+    int64_t R = k_w * i_c, KD = k_h * R, LD = i_h * R;
+#pragma omp parallel for schedule(static)
+    for (int64_t p = 0; p < i_n * o_w; ++p) {
+        int64_t n = p / o_w, w = p % o_w;
+        double* row = dL + p * LD;
+        for (int64_t e = 0; e < LD; ++e) row[e] = 0.0;
+        for (int64_t h = 0; h < o_h; ++h)
+            for (int64_t j = 0; j < KD; ++j) {
+                double acc = 0.0;
+                for (int64_t m = 0; m < k_c; ++m)
+                    acc += elem(G, ((n * o_h + h) * o_w + w) * k_c + m, dtype) *
+                           elem(K, j * k_c + m, dtype);
+                row[s_h * R * h + j] += acc;
+            }
+    }
+}
+
+void oracle_mec_wgrad_lowered(const void* L, const void* G, double* dK,
+                              int64_t i_n, int64_t i_h, int64_t i_w, int64_t i_c,
+                              int64_t k_h, int64_t k_w, int64_t k_c,
+                              int64_t s_h, int64_t s_w, int dtype)
+{
+    int64_t o_h = oracle_out_dim(i_h, k_h, s_h);
+    int64_t o_w = oracle_out_dim(i_w, k_w, s_w);
+    int64_t R = k_w * i_c, KD = k_h * R, LD = i_h * R;
+#pragma omp parallel for schedule(static)
+    for (int64_t j = 0; j < KD; ++j)
+        for (int64_t m = 0; m < k_c; ++m) {
+            double acc = 0.0;
+            for (int64_t h = 0; h < o_h; ++h)
+                for (int64_t p = 0; p < i_n * o_w; ++p) {
+                    int64_t n = p / o_w, w = p % o_w;
+                    acc += elem(L, p * LD + s_h * R * h + j, dtype) *
+                           elem(G, ((n * o_h + h) * o_w + w) * k_c + m, dtype);
+                }
+            dK[j * k_c + m] = acc;
+        }
+}
+
+/* The adjoint of the lowering (the transpose of the copy I -> L): every
+ * element of dL is added back to the input pixel it was copied from,
+ *   dI[n, h, s_w*w + b, c] += dL[n, w, h, b, c].
+ * dL may be fp32, bf16 or fp64 (dtype 0, 1, 2); dI is fp64, 0 where no
+ * column strip reaches. */
+void oracle_mec_fold(const void* dL, double* dI,
+                     int64_t i_n, int64_t i_h, int64_t i_w, int64_t i_c,
+                     int64_t k_h, int64_t k_w, int64_t k_c,
+                     int64_t s_h, int64_t s_w, int dtype)
+{
+    (void)k_h; (void)k_c; (void)s_h;
+    int64_t o_w = oracle_out_dim(i_w, k_w, s_w);
+#pragma omp parallel for schedule(static)
+    for (int64_t n = 0; n < i_n; ++n) {
+        double* d = dI + n * i_h * i_w * i_c;
+        for (int64_t e = 0; e < i_h * i_w * i_c; ++e) d[e] = 0.0;
+        for (int64_t w = 0; w < o_w; ++w)
+            for (int64_t h = 0; h < i_h; ++h)
+                for (int64_t b = 0; b < k_w; ++b)
+                    for (int64_t c = 0; c < i_c; ++c)
+                        d[(h * i_w + s_w * w + b) * i_c + c] +=
+                            elem(dL, (((n * o_w + w) * i_h + h) * k_w + b) * i_c + c, dtype);
+    }
 }
 
 /* Number of OpenMP threads a parallel region here would use (0 when built
