@@ -153,6 +153,86 @@ int mec_conv2d(const void* I, const void* K, float* O,
                int k_h, int k_w, int k_c, int s_h, int s_w,
                int dtype, int algo, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Training passes (fp32). The paper names training as a use of MEC (Section
+ * 1; Section 4 measures training set-ups) but gives no backward algorithm.
+ * These are the derivatives of the convolution above. For a loss whose
+ * gradient with respect to O is G (fp32, O's shape i_n x o_h x o_w x k_c):
+ *   dI[n, y*s_h + a, x*s_w + b, c] = sum of G[n, y, x, m] * K[a, b, c, m]
+ *                                    over all (y, x, m, a, b) that reach it
+ *   dK[a, b, c, m] = sum over n, y, x of I[n, y*s_h + a, x*s_w + b, c] * G[n, y, x, m]
+ * (input pixels no window covers get dI = 0). Both go through MEC's lowered
+ * layout: output row h is O_h = A_h K with A_h the slab of L for row h, so
+ *   dL = each slab receives G_h K^T (summed where slabs overlap),  dI = fold(dL),
+ *   dK = sum over h of A_h^T G_h,
+ * where G_h = G[:, h, :, :] as an (i_n*o_w) x k_c matrix and fold is the
+ * adjoint of the lowering (mec_fold). dtype must be MEC_F32 (MEC_BF16 gives
+ * MEC_ERR_UNSUPPORTED); all tensors are fp32, 4-byte aligned.
+ * ------------------------------------------------------------------------ */
+
+/* MEC_GRAD_INPUT: mec_conv2d_dgrad -- dL in fp32, |L| * 4 bytes exactly.
+ * MEC_GRAD_KERNEL: mec_conv2d_wgrad -- L (|L| * 4 bytes, rounded up to 256)
+ *   followed by the partial sums of dK.
+ * MEC_GRAD_KERNEL_FROM_L: mec_wgrad_gemm -- the partial sums of dK only:
+ *   s * k_h*k_w*i_c*k_c * 4 bytes, s (1 <= s <= 1024) fixed by the shape. */
+enum mec_grad_pass { MEC_GRAD_INPUT = 0, MEC_GRAD_KERNEL = 1, MEC_GRAD_KERNEL_FROM_L = 2 };
+
+/* Workspace of a training pass, in bytes (>= 0), or a negative status. */
+int64_t mec_grad_workspace_bytes(int i_n, int i_h, int i_w, int i_c,
+                                 int k_h, int k_w, int k_c, int s_h, int s_w,
+                                 int dtype, int pass);
+
+/* The adjoint of mec_lower: every element of dL (fp32, L's layout
+ * i_n x o_w x i_h x k_w x i_c) is added to the input pixel it was copied from,
+ *   dI[n, h, s_w*w + b, c] += dL[n, w, h, b, c],
+ * summed in increasing w; dI (fp32, I's shape) is overwritten, 0 where no
+ * column strip reaches. dL and dI must not overlap.
+ * Returns MEC_OK or a negative status. */
+int mec_fold(const float* dL, float* dI,
+             int i_n, int i_h, int i_w, int i_c,
+             int k_h, int k_w, int k_c, int s_h, int s_w, void* stream);
+
+/* dL = dloss/dL (fp32, L's layout): for every output row h, G_h K^T added
+ * into the slab L[n, w][s_h*R*h : s_h*R*h + k_h*R] of every pair (n, w), with
+ * R = k_w*i_c; rows of L that no slab covers get 0. dL is overwritten and
+ * must not overlap G or K. Returns MEC_OK or a negative status. */
+int mec_dgrad_gemm(const float* G, const float* K, float* dL,
+                   int i_n, int i_h, int i_w, int i_c,
+                   int k_h, int k_w, int k_c, int s_h, int s_w,
+                   int dtype, void* stream);
+
+/* dI = dloss/dI: mec_dgrad_gemm into `workspace` (which then holds dL),
+ * then mec_fold into dI. workspace_bytes must be at least
+ * mec_grad_workspace_bytes(..., MEC_GRAD_INPUT). dI must not overlap G, K or
+ * the workspace. Returns MEC_OK or a negative status. */
+int mec_conv2d_dgrad(const float* G, const void* K, float* dI,
+                     void* workspace, size_t workspace_bytes,
+                     int i_n, int i_h, int i_w, int i_c,
+                     int k_h, int k_w, int k_c, int s_h, int s_w,
+                     int dtype, void* stream);
+
+/* dK = dloss/dK from an already lowered L (mec_lower's output for the same
+ * shape, e.g. the workspace of a MEC_ALGO_LOWERED mec_conv2d, reused):
+ * partial sums of A_h^T G_h over shares of the (pair, h) reduction go to
+ * `workspace` (mec_grad_workspace_bytes(..., MEC_GRAD_KERNEL_FROM_L)), then
+ * dK (k_h x k_w x i_c x k_c, fp32) is their sum, taken in a fixed order.
+ * dK must not overlap L, G or the workspace. Returns MEC_OK or a negative
+ * status. */
+int mec_wgrad_gemm(const void* L, const float* G, float* dK,
+                   void* workspace, size_t workspace_bytes,
+                   int i_n, int i_h, int i_w, int i_c,
+                   int k_h, int k_w, int k_c, int s_h, int s_w,
+                   int dtype, void* stream);
+
+/* dK = dloss/dK from I: mec_lower into the start of `workspace`, then
+ * mec_wgrad_gemm with the rest of it (mec_grad_workspace_bytes(...,
+ * MEC_GRAD_KERNEL) in all). Returns MEC_OK or a negative status. */
+int mec_conv2d_wgrad(const void* I, const float* G, float* dK,
+                     void* workspace, size_t workspace_bytes,
+                     int i_n, int i_h, int i_w, int i_c,
+                     int k_h, int k_w, int k_c, int s_h, int s_w,
+                     int dtype, void* stream);
+
 /* Static, NUL-terminated description of a status code (never NULL). */
 const char* mec_strerror(int status);
 

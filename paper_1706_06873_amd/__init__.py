@@ -23,6 +23,8 @@ import torch  # noqa: E402,F401
 __all__ = [
     "MecError", "F32", "BF16", "LOWERED", "FUSED", "IM2COL", "lib", "output_dims",
     "workspace_bytes", "im2col_bytes", "lower", "im2col", "gemm", "conv2d", "strerror",
+    "GRAD_INPUT", "GRAD_KERNEL", "GRAD_KERNEL_FROM_L", "grad_workspace_bytes", "fold",
+    "dgrad_gemm", "conv2d_dgrad", "wgrad_gemm", "conv2d_wgrad",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -30,6 +32,7 @@ LIB_PATH = os.path.join(_HERE, "libmec.so")
 
 F32, BF16 = 0, 1
 LOWERED, FUSED, IM2COL = 0, 1, 2
+GRAD_INPUT, GRAD_KERNEL, GRAD_KERNEL_FROM_L = 0, 1, 2
 _ALGOS = {"lowered": LOWERED, "fused": FUSED, "im2col": IM2COL,
           LOWERED: LOWERED, FUSED: FUSED, IM2COL: IM2COL}
 
@@ -57,6 +60,15 @@ def _load(path):
     L.mec_gemm.restype = _i
     L.mec_conv2d.argtypes = [_vp, _vp, _vp, _vp, ctypes.c_size_t] + _DIMS + [_i, _i, _vp]
     L.mec_conv2d.restype = _i
+    L.mec_grad_workspace_bytes.argtypes = _DIMS + [_i, _i]
+    L.mec_grad_workspace_bytes.restype = ctypes.c_int64
+    L.mec_fold.argtypes = [_vp, _vp] + _DIMS + [_vp]
+    L.mec_fold.restype = _i
+    L.mec_dgrad_gemm.argtypes = [_vp, _vp, _vp] + _DIMS + [_i, _vp]
+    L.mec_dgrad_gemm.restype = _i
+    for name in ("mec_conv2d_dgrad", "mec_wgrad_gemm", "mec_conv2d_wgrad"):
+        getattr(L, name).argtypes = [_vp, _vp, _vp, _vp, ctypes.c_size_t] + _DIMS + [_i, _vp]
+        getattr(L, name).restype = _i
     L.mec_strerror.argtypes = [_i]
     L.mec_strerror.restype = ctypes.c_char_p
     L.mec_last_error.argtypes = []
@@ -229,3 +241,116 @@ def conv2d(I, K, s_h=1, s_w=1, algo="lowered", workspace=None, O=None, stream=No
     _check(lib.mec_conv2d(_dev_ptr(I, "I"), _dev_ptr(K, "K"), _dev_ptr(O, "O"), ws_ptr, ws_bytes,
                           *d, _dtype_code(I), a, _stream_handle(stream)), "mec_conv2d")
     return O
+
+
+# ---------------------------------------------------------------- training passes
+# Gradients of the convolution through MEC's lowered layout, fp32 only. G is
+# dloss/dO (O's shape, float32).
+
+def grad_workspace_bytes(i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w, dtype=F32,
+                         grad_pass=GRAD_INPUT):
+    return _check(lib.mec_grad_workspace_bytes(i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w, dtype,
+                                               grad_pass), "mec_grad_workspace_bytes")
+
+
+def _f32(t, name):
+    import torch
+    if t.dtype != torch.float32:
+        raise TypeError("%s must be float32" % name)
+    return _dev_ptr(t, name)
+
+
+def _workspace(need, workspace, device):
+    import torch
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=device)
+    return workspace, _dev_ptr(workspace, "workspace"), workspace.numel() * workspace.element_size()
+
+
+def fold(dL, i_w, s_w, dI=None, stream=None):
+    """The adjoint of the lowering: dI[n, h, s_w*w + b, c] += dL[n, w, h, b, c]
+    for dL of L's shape (i_n x o_w x i_h x k_w x i_c, float32). Returns dI."""
+    import torch
+    i_n, o_w, i_h, k_w, i_c = dL.shape
+    if output_dims(i_h, i_w, 1, k_w, 1, s_w)[1] != o_w:
+        raise ValueError("i_w, k_w, s_w do not give dL's o_w")
+    if dI is None:
+        dI = torch.empty((i_n, i_h, i_w, i_c), dtype=torch.float32, device=dL.device)
+    if tuple(dI.shape) != (i_n, i_h, i_w, i_c):
+        raise ValueError("dI must be i_n x i_h x i_w x i_c")
+    _check(lib.mec_fold(_f32(dL, "dL"), _f32(dI, "dI"), i_n, i_h, i_w, i_c, 1, k_w, 1, 1, s_w,
+                        _stream_handle(stream)), "mec_fold")
+    return dI
+
+
+def _grad_dims(G, K, i_h, i_w, s_h, s_w):
+    k_h, k_w, i_c, k_c = K.shape
+    i_n = G.shape[0]
+    o_h, o_w = output_dims(i_h, i_w, k_h, k_w, s_h, s_w)
+    if tuple(G.shape) != (i_n, o_h, o_w, k_c):
+        raise ValueError("G must be i_n x o_h x o_w x k_c = %s" % ((i_n, o_h, o_w, k_c),))
+    return (i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w)
+
+
+def dgrad_gemm(G, K, i_h, i_w, s_h=1, s_w=1, dL=None, stream=None):
+    """dL = dloss/dL (L's shape, float32): G_h K^T added into every slab."""
+    import torch
+    d = _grad_dims(G, K, i_h, i_w, s_h, s_w)
+    o_w = G.shape[2]
+    if dL is None:
+        dL = torch.empty((d[0], o_w, i_h, d[5], d[3]), dtype=torch.float32, device=G.device)
+    if dL.numel() != d[0] * o_w * i_h * d[5] * d[3]:
+        raise ValueError("dL has the wrong size")
+    _check(lib.mec_dgrad_gemm(_f32(G, "G"), _f32(K, "K"), _f32(dL, "dL"), *d, F32,
+                              _stream_handle(stream)), "mec_dgrad_gemm")
+    return dL
+
+
+def conv2d_dgrad(G, K, i_h, i_w, s_h=1, s_w=1, dI=None, workspace=None, stream=None):
+    """dI = dloss/dI (I's shape, float32); the workspace then holds dL."""
+    import torch
+    d = _grad_dims(G, K, i_h, i_w, s_h, s_w)
+    if dI is None:
+        dI = torch.empty((d[0], i_h, i_w, d[3]), dtype=torch.float32, device=G.device)
+    need = grad_workspace_bytes(*d, grad_pass=GRAD_INPUT)
+    workspace, wp, wb = _workspace(need, workspace, G.device)
+    _check(lib.mec_conv2d_dgrad(_f32(G, "G"), _f32(K, "K"), _f32(dI, "dI"), wp, wb, *d, F32,
+                                _stream_handle(stream)), "mec_conv2d_dgrad")
+    return dI
+
+
+def wgrad_gemm(L, G, k_h, i_w, s_h=1, s_w=1, dK=None, workspace=None, stream=None):
+    """dK = dloss/dK from a lowered L (i_n x o_w x i_h x k_w x i_c, float32):
+    the sum over h of A_h^T G_h. Returns dK (k_h x k_w x i_c x k_c)."""
+    import torch
+    i_n, o_w, i_h, k_w, i_c = L.shape
+    k_c = G.shape[3]
+    o_h, o_w2 = output_dims(i_h, i_w, k_h, k_w, s_h, s_w)
+    if o_w2 != o_w or tuple(G.shape) != (i_n, o_h, o_w, k_c):
+        raise ValueError("L and G do not match the shape")
+    d = (i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w)
+    if dK is None:
+        dK = torch.empty((k_h, k_w, i_c, k_c), dtype=torch.float32, device=G.device)
+    need = grad_workspace_bytes(*d, grad_pass=GRAD_KERNEL_FROM_L)
+    workspace, wp, wb = _workspace(need, workspace, G.device)
+    _check(lib.mec_wgrad_gemm(_f32(L, "L"), _f32(G, "G"), _f32(dK, "dK"), wp, wb, *d, F32,
+                              _stream_handle(stream)), "mec_wgrad_gemm")
+    return dK
+
+
+def conv2d_wgrad(I, G, k_h, k_w, s_h=1, s_w=1, dK=None, workspace=None, stream=None):
+    """dK = dloss/dK from I (lowered into the workspace first)."""
+    import torch
+    i_n, i_h, i_w, i_c = I.shape
+    k_c = G.shape[3]
+    o_h, o_w = output_dims(i_h, i_w, k_h, k_w, s_h, s_w)
+    if tuple(G.shape) != (i_n, o_h, o_w, k_c):
+        raise ValueError("G must be i_n x o_h x o_w x k_c = %s" % ((i_n, o_h, o_w, k_c),))
+    d = (i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w)
+    if dK is None:
+        dK = torch.empty((k_h, k_w, i_c, k_c), dtype=torch.float32, device=G.device)
+    need = grad_workspace_bytes(*d, grad_pass=GRAD_KERNEL)
+    workspace, wp, wb = _workspace(need, workspace, G.device)
+    _check(lib.mec_conv2d_wgrad(_f32(I, "I"), _f32(G, "G"), _f32(dK, "dK"), wp, wb, *d, F32,
+                                _stream_handle(stream)), "mec_conv2d_wgrad")
+    return dK

@@ -15,7 +15,8 @@ REPO = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(REPO, "include")
 LIB = os.path.join(PKG, "libmec.so")
-SOURCES = ["mec_api.cpp", "mec_lower.hip", "mec_im2col.hip", "mec_gemm.hip", "mec_gemm_fixed.hip"]
+SOURCES = ["mec_api.cpp", "mec_lower.hip", "mec_im2col.hip", "mec_gemm.hip", "mec_gemm_fixed.hip",
+           "mec_grad.hip"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

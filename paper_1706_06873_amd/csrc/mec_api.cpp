@@ -197,6 +197,125 @@ int mec_conv2d(const void* I, const void* K, float* O, void* workspace, size_t w
     return hip_status(mec::launch_gemm(s, workspace, K, O, dtype, false, st), "slab products");
 }
 
+// ---------------------------------------------------------------- training passes
+
+namespace {
+
+// Start of the partial sums inside a MEC_GRAD_KERNEL workspace.
+int64_t wgrad_l_region(const mec::Shape& s) { return (lowered_elems(s) * 4 + 255) / 256 * 256; }
+
+// Common checks of the training entry points: shape, dtype (fp32 only),
+// and the 32-bit index ranges of the kernels.
+int grad_shape(mec::Shape& s, int i_n, int i_h, int i_w, int i_c, int k_h, int k_w, int k_c,
+               int s_h, int s_w, int dtype) {
+    int rc = make_shape(s, i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w);
+    if (rc != MEC_OK) return rc;
+    if (!valid_dtype(dtype)) return MEC_ERR_INVALID_ARG;
+    if (dtype != MEC_F32) return MEC_ERR_UNSUPPORTED;
+    if (s.i_n * s.i_h * s.i_w * s.i_c >= (int64_t(1) << 31)) return MEC_ERR_UNSUPPORTED;
+    return MEC_OK;
+}
+
+}  // namespace
+
+int64_t mec_grad_workspace_bytes(int i_n, int i_h, int i_w, int i_c, int k_h, int k_w, int k_c,
+                                 int s_h, int s_w, int dtype, int pass) {
+    mec::Shape s;
+    int rc = grad_shape(s, i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w, dtype);
+    if (rc != MEC_OK) return rc;
+    switch (pass) {
+        case MEC_GRAD_INPUT: return lowered_elems(s) * 4;
+        case MEC_GRAD_KERNEL: return wgrad_l_region(s) + mec::wgrad_partial_bytes(s);
+        case MEC_GRAD_KERNEL_FROM_L: return mec::wgrad_partial_bytes(s);
+        default: return MEC_ERR_INVALID_ARG;
+    }
+}
+
+int mec_fold(const float* dL, float* dI, int i_n, int i_h, int i_w, int i_c, int k_h, int k_w,
+             int k_c, int s_h, int s_w, void* stream) {
+    mec::Shape s;
+    int rc = grad_shape(s, i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w, MEC_F32);
+    if (rc != MEC_OK) return rc;
+    if (!dL || !dI) return MEC_ERR_INVALID_ARG;
+    if (!aligned(dL, 4) || !aligned(dI, 4)) return MEC_ERR_ALIGNMENT;
+    clear_stale_error();
+    return hip_status(mec::launch_fold(s, dL, dI, (hipStream_t)stream), "fold");
+}
+
+int mec_dgrad_gemm(const float* G, const float* K, float* dL, int i_n, int i_h, int i_w, int i_c,
+                   int k_h, int k_w, int k_c, int s_h, int s_w, int dtype, void* stream) {
+    mec::Shape s;
+    int rc = grad_shape(s, i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w, dtype);
+    if (rc != MEC_OK) return rc;
+    if (!G || !K || !dL) return MEC_ERR_INVALID_ARG;
+    if (!aligned(G, 4) || !aligned(K, 4) || !aligned(dL, 4)) return MEC_ERR_ALIGNMENT;
+    if (!mec::dgrad_supported(s)) return MEC_ERR_UNSUPPORTED;
+    clear_stale_error();
+    return hip_status(mec::launch_dgrad_dl(s, G, K, dL, (hipStream_t)stream), "dgrad products");
+}
+
+int mec_conv2d_dgrad(const float* G, const void* K, float* dI, void* workspace,
+                     size_t workspace_bytes, int i_n, int i_h, int i_w, int i_c, int k_h, int k_w,
+                     int k_c, int s_h, int s_w, int dtype, void* stream) {
+    mec::Shape s;
+    int rc = grad_shape(s, i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w, dtype);
+    if (rc != MEC_OK) return rc;
+    if (!G || !K || !dI) return MEC_ERR_INVALID_ARG;
+    if (!aligned(G, 4) || !aligned(K, 4) || !aligned(dI, 4)) return MEC_ERR_ALIGNMENT;
+    if (!workspace || (uint64_t)workspace_bytes < (uint64_t)(lowered_elems(s) * 4))
+        return MEC_ERR_WORKSPACE;
+    if (!aligned(workspace, 4)) return MEC_ERR_ALIGNMENT;
+    if (!mec::dgrad_supported(s)) return MEC_ERR_UNSUPPORTED;
+    const hipStream_t st = (hipStream_t)stream;
+    float* dL = static_cast<float*>(workspace);
+    clear_stale_error();
+    rc = hip_status(mec::launch_dgrad_dl(s, G, static_cast<const float*>(K), dL, st),
+                    "dgrad products");
+    if (rc != MEC_OK) return rc;
+    return hip_status(mec::launch_fold(s, dL, dI, st), "fold");
+}
+
+int mec_wgrad_gemm(const void* L, const float* G, float* dK, void* workspace,
+                   size_t workspace_bytes, int i_n, int i_h, int i_w, int i_c, int k_h, int k_w,
+                   int k_c, int s_h, int s_w, int dtype, void* stream) {
+    mec::Shape s;
+    int rc = grad_shape(s, i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w, dtype);
+    if (rc != MEC_OK) return rc;
+    if (!L || !G || !dK) return MEC_ERR_INVALID_ARG;
+    if (!aligned(L, 4) || !aligned(G, 4) || !aligned(dK, 4)) return MEC_ERR_ALIGNMENT;
+    if (!mec::wgrad_supported(s)) return MEC_ERR_UNSUPPORTED;
+    if (!workspace || (uint64_t)workspace_bytes < (uint64_t)mec::wgrad_partial_bytes(s))
+        return MEC_ERR_WORKSPACE;
+    if (!aligned(workspace, 4)) return MEC_ERR_ALIGNMENT;
+    clear_stale_error();
+    return hip_status(mec::launch_wgrad(s, static_cast<const float*>(L), G,
+                                        static_cast<float*>(workspace), dK, (hipStream_t)stream),
+                      "wgrad products");
+}
+
+int mec_conv2d_wgrad(const void* I, const float* G, float* dK, void* workspace,
+                     size_t workspace_bytes, int i_n, int i_h, int i_w, int i_c, int k_h, int k_w,
+                     int k_c, int s_h, int s_w, int dtype, void* stream) {
+    mec::Shape s;
+    int rc = grad_shape(s, i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w, dtype);
+    if (rc != MEC_OK) return rc;
+    if (!I || !G || !dK) return MEC_ERR_INVALID_ARG;
+    if (!aligned(I, 4) || !aligned(G, 4) || !aligned(dK, 4)) return MEC_ERR_ALIGNMENT;
+    if (!mec::wgrad_supported(s)) return MEC_ERR_UNSUPPORTED;
+    const int64_t lreg = wgrad_l_region(s);
+    if (!workspace ||
+        (uint64_t)workspace_bytes < (uint64_t)(lreg + mec::wgrad_partial_bytes(s)))
+        return MEC_ERR_WORKSPACE;
+    if (!aligned(workspace, 4)) return MEC_ERR_ALIGNMENT;
+    const hipStream_t st = (hipStream_t)stream;
+    float* Lw = static_cast<float*>(workspace);
+    float* part = reinterpret_cast<float*>(static_cast<char*>(workspace) + lreg);
+    clear_stale_error();
+    rc = hip_status(mec::launch_lower(s, I, Lw, 4, st), "lowering");
+    if (rc != MEC_OK) return rc;
+    return hip_status(mec::launch_wgrad(s, Lw, G, part, dK, st), "wgrad products");
+}
+
 const char* mec_strerror(int status) {
     switch (status) {
         case MEC_OK: return "success";

@@ -1,0 +1,567 @@
+// Training passes of the convolution through MEC's lowered layout, fp32.
+//
+// The paper names training as a use of MEC (Section 1; the set-ups of
+// Section 4 include training) but gives no backward algorithm. With R =
+// k_w*i_c, the product phase computes for every output row h
+//   O_h = A_h K,   A_h = L[:, :][s_h*R*h : s_h*R*h + k_h*R]   ((i_n*o_w) x (k_h*R))
+// with K viewed as (k_h*R) x k_c. For a loss with gradient G = dloss/dO and
+// G_h = G[n, h, w, :] as an (i_n*o_w) x k_c matrix, differentiating gives
+//   dL = every slab receives G_h K^T, summed where slabs overlap,
+//   dK = sum over h of A_h^T G_h,
+// and since the lowering copies I into L, dI is the fold of dL: each element
+// of dL added back to the input pixel it was copied from.
+//
+//  dgrad_dl  dL from G and K on fp32 MFMA (v_mfma_f32_32x32x2_f32). A
+//            workgroup computes 32 (n, w) pairs x RT consecutive rows r of dL
+//            x 64 columns (b, c). Row r receives G[n, h, w, :] K[a]^T for every
+//            (h, a) with h*s_h + a = r, so the tile stages the hspan rows of G
+//            its rows draw on and the k_h kernel rows, once per chunk of KT
+//            output channels; each staged G row feeds up to ceil(k_h/s_h) rows
+//            of dL, the slab overlap of the forward pass seen from the other
+//            side. Rows of dL that no slab covers are written as zeros.
+//  fold      dI[n, h, x, c] = sum over w with 0 <= x - s_w*w < k_w of
+//            dL[n, w, h, x - s_w*w, c], in increasing w: a gather, one thread
+//            per element (or per 4 channels), bound by HBM bandwidth.
+//  wgrad     a share of the reduction over (pair, output row) on fp32 MFMA: a
+//            workgroup computes a 128 x 64 tile of dK (rows j = a*R + b*i_c + c,
+//            columns m) over the stages in its share, a stage being 16 pairs x
+//            4 output rows, and writes the tile to its own partial buffer.
+//  reduce    dK = the partial buffers summed in increasing share order, so the
+//            result does not depend on scheduling.
+// Global loads of the next stage go to registers before the current stage's
+// MFMAs and to LDS after them.
+#include "mec_mfma.h"
+
+namespace mec {
+namespace {
+
+constexpr int kGradThreads = 256;
+constexpr size_t kGradLdsBudget = 64 * 1024;
+
+// ---------------------------------------------------------------- dgrad: dL
+constexpr int kDgRT = 8;   // rows of dL per tile
+constexpr int kDgJT = 64;  // columns of dL per tile: two 32-wide MFMA blocks
+constexpr int kDgRW = 4;   // rows per wave; waves = 2 row groups x 2 column blocks
+
+struct DgradParams {
+    const float* G;
+    const float* K;
+    float* dL;
+    int32_t i_h, o_h, o_w, k_h, s_h, k_c, R;
+    int32_t pairs;
+    int32_t r_tiles, j_tiles;
+    uint32_t ntiles;
+    int32_t hspan;    // G rows a tile stages: (RT + k_h - 2) / s_h + 1
+    int32_t nchunks;  // chunks of KT output channels
+    int32_t gps;      // LDS stride between pairs in the G stage: hspan*KT + 1
+    int32_t gcount;   // elements of the G stage: 32 * hspan * KT
+    int32_t kbase;    // LDS offset of the K stage
+    int32_t kcount;   // elements of the K stage: k_h * JT * KT
+    int32_t stage;    // LDS elements of one stage
+    int32_t nbuf;     // stages in LDS: 2 (double-buffered) or 1
+    FastDiv div_hkt;  // by hspan * KT
+};
+
+// KT: output channels per chunk. MAXE: stage elements one thread moves
+// (registers of the prefetch); the host checks (gcount + kcount) fits.
+template <int KT, int MAXE>
+__global__ __launch_bounds__(kGradThreads) void dgrad_dl_kernel(DgradParams p) {
+    extern __shared__ __align__(16) float dg_smem[];
+    __shared__ int64_t gbase[kPairs];  // G offset of (n, 0, w, 0), or -1 past the last pair
+    __shared__ int64_t lbase[kPairs];  // dL offset of pair row (n, w)
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wr = wave & 1, wn = wave >> 1;
+
+    const uint32_t t = xcd_remap(blockIdx.x, p.ntiles);
+    const int jt = (int)(t % (uint32_t)p.j_tiles);
+    const uint32_t rest = t / (uint32_t)p.j_tiles;
+    const int rt = (int)(rest % (uint32_t)p.r_tiles);
+    const int pt = (int)(rest / (uint32_t)p.r_tiles);
+    const int r0 = rt * kDgRT, j0 = jt * kDgJT;
+    const int64_t pair0 = (int64_t)pt * kPairs;
+    // first G row any of rows r0.. needs: the smallest h with h*s_h >= r0 - k_h + 1
+    const int lo = r0 - p.k_h + 1;
+    const int h_min = lo > 0 ? (lo + p.s_h - 1) / p.s_h : 0;
+
+    if (tid < kPairs) {
+        const int64_t pair = pair0 + tid;
+        if (pair < p.pairs) {
+            const int64_t n = pair / p.o_w, w = pair - n * p.o_w;
+            gbase[tid] = (n * p.o_h * p.o_w + w) * p.k_c;
+            lbase[tid] = pair * p.i_h * p.R;
+        } else {
+            gbase[tid] = -1;
+            lbase[tid] = -1;
+        }
+    }
+    __syncthreads();
+
+    const int total = p.gcount + p.kcount;
+    // stage element e of the chunk starting at channel m0: its LDS offset and
+    // global source (nullptr where the stage holds zeros)
+    auto map = [&](int e, int m0, int& off) -> const float* {
+        if (e < p.gcount) {
+            const int pp = (int)p.div_hkt.div((uint32_t)e);
+            const int rem = e - pp * p.hspan * KT;
+            const int hh = rem / KT, mm = rem - (rem / KT) * KT;
+            off = pp * p.gps + hh * KT + mm;
+            const int h = h_min + hh, m = m0 + mm;
+            const int64_t gb = gbase[pp];
+            if (gb >= 0 && h < p.o_h && m < p.k_c) return p.G + gb + (int64_t)h * p.o_w * p.k_c + m;
+            return nullptr;
+        }
+        const int e2 = e - p.gcount;
+        const int a = e2 / (kDgJT * KT);
+        const int rem = e2 - a * (kDgJT * KT);
+        const int jj = rem / KT, mm = rem - (rem / KT) * KT;
+        off = p.kbase + (a * kDgJT + jj) * (KT + 1) + mm;
+        const int j = j0 + jj, m = m0 + mm;
+        if (j < p.R && m < p.k_c) return p.K + ((int64_t)a * p.R + j) * p.k_c + m;
+        return nullptr;
+    };
+
+    float regs[MAXE];
+    auto load = [&](int rc) {
+        int off;
+#pragma unroll
+        for (int i = 0; i < MAXE; ++i) {
+            const int e = tid + i * kGradThreads;
+            float v = 0.f;
+            if (e < total) {
+                const float* src = map(e, rc * KT, off);
+                if (src) v = *src;
+            }
+            regs[i] = v;
+        }
+    };
+    auto store = [&](float* st) {
+        int off;
+#pragma unroll
+        for (int i = 0; i < MAXE; ++i) {
+            const int e = tid + i * kGradThreads;
+            if (e < total) {
+                (void)map(e, 0, off);
+                st[off] = regs[i];
+            }
+        }
+    };
+
+    floatx16 acc[kDgRW];
+#pragma unroll
+    for (int i = 0; i < kDgRW; ++i)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[i][v] = 0.f;
+
+    const int row = lane & 31, khalf = lane >> 5;
+    auto compute = [&](const float* st) {
+        const float* Gs = st;
+        const float* Ks = st + p.kbase;
+#pragma unroll
+        for (int rr = 0; rr < kDgRW; ++rr) {
+            const int r = r0 + wr * kDgRW + rr;
+            for (int a = 0; a < p.k_h && a <= r; ++a) {
+                const int d = r - a;
+                const int h = d / p.s_h;
+                if (d - h * p.s_h != 0 || h >= p.o_h) continue;
+                const float* gp = Gs + row * p.gps + (h - h_min) * KT + khalf;
+                const float* kp = Ks + (a * kDgJT + wn * 32 + row) * (KT + 1) + khalf;
+#pragma unroll
+                for (int kk = 0; kk < KT; kk += 2)
+                    acc[rr] = __builtin_amdgcn_mfma_f32_32x32x2f32(gp[kk], kp[kk], acc[rr], 0, 0, 0);
+            }
+        }
+    };
+
+    const bool dbuf = p.nbuf == 2;
+    auto buf = [&](int rc) { return dg_smem + (dbuf ? (rc & 1) * p.stage : 0); };
+    load(0);
+    store(buf(0));
+    __syncthreads();
+    for (int rc = 0; rc < p.nchunks; ++rc) {
+        const bool more = rc + 1 < p.nchunks;
+        if (more) load(rc + 1);  // in flight during the MFMAs below
+        compute(buf(rc));
+        if (more) {
+            if (!dbuf) __syncthreads();  // every wave is done reading the single stage
+            store(buf(rc + 1));
+        }
+        __syncthreads();
+    }
+
+    // lane holds C[pair][col]: pair = acc_row(v, lane), col = lane % 32
+    const int col = j0 + wn * 32 + row;
+    if (col >= p.R) return;
+#pragma unroll
+    for (int rr = 0; rr < kDgRW; ++rr) {
+        const int r = r0 + wr * kDgRW + rr;
+        if (r >= p.i_h) continue;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int64_t lb = lbase[acc_row(v, lane)];
+            if (lb >= 0) p.dL[lb + (int64_t)r * p.R + col] = acc[rr][v];
+        }
+    }
+}
+
+// ---------------------------------------------------------------- fold
+struct FoldParams {
+    const float* dL;
+    float* dI;
+    uint32_t units;  // elements of dI, or groups of 4 channels
+    uint32_t i_h, i_w, i_c, k_w, s_w, o_w, R;
+    FastDiv div_ic, div_iw, div_ih;
+};
+
+// V = 4: four consecutive channels per thread (i_c % 4 == 0, 16-byte aligned
+// dL and dI); V = 1: one element.
+template <int V>
+__global__ __launch_bounds__(kGradThreads) void fold_kernel(FoldParams p) {
+    typedef float f32x4 __attribute__((ext_vector_type(4)));
+    const uint32_t stride = gridDim.x * kGradThreads;
+    for (uint32_t u = blockIdx.x * kGradThreads + threadIdx.x; u < p.units; u += stride) {
+        const uint32_t q = u * V;  // element index in dI
+        const uint32_t t = p.div_ic.div(q), c = q - t * p.i_c;
+        const uint32_t t2 = p.div_iw.div(t), x = t - t2 * p.i_w;
+        const uint32_t n = p.div_ih.div(t2), h = t2 - n * p.i_h;
+        // columns w whose strip [s_w*w, s_w*w + k_w) holds x
+        const uint32_t w_lo = x >= p.k_w ? (x - p.k_w) / p.s_w + 1 : 0;
+        uint32_t w_hi = x / p.s_w;
+        if (w_hi > p.o_w - 1) w_hi = p.o_w - 1;
+        const size_t col = (size_t)p.i_h * p.R;  // elements of one column strip L[n, w]
+        const float* src = p.dL + ((size_t)n * p.o_w * p.i_h + h) * p.R + c;
+        if (V == 4) {
+            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+            for (uint32_t w = w_lo; w <= w_hi; ++w)
+                acc += *reinterpret_cast<const f32x4*>(src + w * col + (size_t)(x - p.s_w * w) * p.i_c);
+            __builtin_nontemporal_store(acc, reinterpret_cast<f32x4*>(p.dI + q));
+        } else {
+            float acc = 0.f;
+            for (uint32_t w = w_lo; w <= w_hi; ++w) acc += src[w * col + (size_t)(x - p.s_w * w) * p.i_c];
+            __builtin_nontemporal_store(acc, p.dI + q);
+        }
+    }
+}
+
+// ---------------------------------------------------------------- wgrad
+constexpr int kWgPT = 16, kWgHT = 4;  // a stage: 16 pairs x 4 output rows
+constexpr int kWgC = kWgPT * kWgHT;   // (pair, row) combinations per stage
+constexpr int kWgJT = 128;            // dK rows per tile: one 32-row block per wave
+constexpr int kWgMT = 64;             // dK columns per tile: two 32-wide blocks
+constexpr int kWgA4 = kWgC * kWgJT / 4 / kGradThreads;  // float4 of the A stage per thread
+constexpr int kWgB4 = kWgC * kWgMT / 4 / kGradThreads;  // float4 of the B stage per thread
+
+struct WgradParams {
+    const float* L;
+    const float* G;
+    float* part;      // splits x KD x k_c partial sums
+    int32_t i_h, o_h, o_w, k_c, s_h, R, KD, pairs;
+    int32_t h_chunks;  // ceil(o_h / HT)
+    int32_t nstages;   // ceil(pairs / PT) * h_chunks
+    int32_t splits;
+    int32_t j_tiles, m_tiles;
+    uint32_t ntiles;
+    int32_t lvec;      // L loads as 16-byte vectors (R % 4 == 0, L aligned)
+    int32_t gvec;      // G loads as 16-byte vectors (k_c % 4 == 0, G aligned)
+    FastDiv div_ow;
+};
+
+__global__ __launch_bounds__(kGradThreads) void wgrad_kernel(WgradParams p) {
+    typedef float f32x4 __attribute__((ext_vector_type(4)));
+    __shared__ __align__(16) float As[kWgC * kWgJT];  // [combination][j]
+    __shared__ __align__(16) float Bs[kWgC * kWgMT];  // [combination][m]
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+
+    const uint32_t t = xcd_remap(blockIdx.x, p.ntiles);
+    const int jt = (int)(t % (uint32_t)p.j_tiles);
+    const uint32_t rest = t / (uint32_t)p.j_tiles;
+    const int mt = (int)(rest % (uint32_t)p.m_tiles);
+    const int s = (int)(rest / (uint32_t)p.m_tiles);
+    const int j0 = jt * kWgJT, m0 = mt * kWgMT;
+    const int st_begin = (int)((int64_t)s * p.nstages / p.splits);
+    const int st_end = (int)((int64_t)(s + 1) * p.nstages / p.splits);
+
+    f32x4 ra[kWgA4], rb[kWgB4];
+    auto load = [&](int st) {
+        const int pc = st / p.h_chunks, hc = st - (st / p.h_chunks) * p.h_chunks;
+#pragma unroll
+        for (int i = 0; i < kWgA4; ++i) {
+            const int u = tid + i * kGradThreads;
+            const int cidx = u >> 5, jq = (u & 31) * 4;
+            const int pair = pc * kWgPT + (cidx >> 2), h = hc * kWgHT + (cidx & 3);
+            const int j = j0 + jq;
+            f32x4 v = {0.f, 0.f, 0.f, 0.f};
+            if (pair < p.pairs && h < p.o_h) {
+                const float* src = p.L + ((int64_t)pair * p.i_h + (int64_t)h * p.s_h) * p.R + j;
+                if (p.lvec && j + 3 < p.KD) {
+                    v = *reinterpret_cast<const f32x4*>(src);
+                } else {
+#pragma unroll
+                    for (int k = 0; k < 4; ++k)
+                        if (j + k < p.KD) v[k] = src[k];
+                }
+            }
+            ra[i] = v;
+        }
+#pragma unroll
+        for (int i = 0; i < kWgB4; ++i) {
+            const int u = tid + i * kGradThreads;
+            const int cidx = u >> 4, mq = (u & 15) * 4;
+            const int pair = pc * kWgPT + (cidx >> 2), h = hc * kWgHT + (cidx & 3);
+            const int m = m0 + mq;
+            f32x4 v = {0.f, 0.f, 0.f, 0.f};
+            if (pair < p.pairs && h < p.o_h) {
+                const int n = (int)p.div_ow.div((uint32_t)pair), w = pair - n * p.o_w;
+                const float* src = p.G + (((int64_t)n * p.o_h + h) * p.o_w + w) * p.k_c + m;
+                if (p.gvec && m + 3 < p.k_c) {
+                    v = *reinterpret_cast<const f32x4*>(src);
+                } else {
+#pragma unroll
+                    for (int k = 0; k < 4; ++k)
+                        if (m + k < p.k_c) v[k] = src[k];
+                }
+            }
+            rb[i] = v;
+        }
+    };
+    auto store = [&]() {
+#pragma unroll
+        for (int i = 0; i < kWgA4; ++i) {
+            const int u = tid + i * kGradThreads;
+            *reinterpret_cast<f32x4*>(As + (u >> 5) * kWgJT + (u & 31) * 4) = ra[i];
+        }
+#pragma unroll
+        for (int i = 0; i < kWgB4; ++i) {
+            const int u = tid + i * kGradThreads;
+            *reinterpret_cast<f32x4*>(Bs + (u >> 4) * kWgMT + (u & 15) * 4) = rb[i];
+        }
+    };
+
+    floatx16 acc[2];
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[nb][v] = 0.f;
+    const int row = lane & 31, khalf = lane >> 5;
+
+    if (st_begin < st_end) {
+        load(st_begin);
+        store();
+        __syncthreads();
+        for (int st = st_begin; st < st_end; ++st) {
+            const bool more = st + 1 < st_end;
+            if (more) load(st + 1);  // in flight during the MFMAs below
+#pragma unroll 8
+            for (int kk = 0; kk < kWgC; kk += 2) {
+                const float af = As[(kk + khalf) * kWgJT + wave * 32 + row];
+#pragma unroll
+                for (int nb = 0; nb < 2; ++nb) {
+                    const float bf = Bs[(kk + khalf) * kWgMT + nb * 32 + row];
+                    acc[nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(af, bf, acc[nb], 0, 0, 0);
+                }
+            }
+            __syncthreads();  // every wave is done with this stage
+            if (more) {
+                store();
+                __syncthreads();
+            }
+        }
+    }
+
+    // lane holds C[j][m]: j = wave*32 + acc_row(v, lane), m = nb*32 + lane % 32
+    float* out = p.part + (int64_t)s * p.KD * p.k_c;
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+        const int m = m0 + nb * 32 + row;
+        if (m >= p.k_c) continue;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int j = j0 + wave * 32 + acc_row(v, lane);
+            if (j < p.KD) out[(int64_t)j * p.k_c + m] = acc[nb][v];
+        }
+    }
+}
+
+// dK[e] = sum over s of part[s][e], s increasing. V = 4 when E % 4 == 0 and
+// both buffers are 16-byte aligned.
+template <int V>
+__global__ __launch_bounds__(kGradThreads) void wgrad_reduce_kernel(const float* part, float* dK,
+                                                                    uint32_t units, uint32_t E,
+                                                                    int32_t splits) {
+    typedef float f32x4 __attribute__((ext_vector_type(4)));
+    const uint32_t stride = gridDim.x * kGradThreads;
+    for (uint32_t u = blockIdx.x * kGradThreads + threadIdx.x; u < units; u += stride) {
+        if (V == 4) {
+            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+            for (int s = 0; s < splits; ++s)
+                acc += *reinterpret_cast<const f32x4*>(part + (size_t)s * E + (size_t)u * 4);
+            *reinterpret_cast<f32x4*>(dK + (size_t)u * 4) = acc;
+        } else {
+            float acc = 0.f;
+            for (int s = 0; s < splits; ++s) acc += part[(size_t)s * E + u];
+            dK[u] = acc;
+        }
+    }
+}
+
+// ---------------------------------------------------------------- host side
+
+inline bool aligned16(const void* ptr) { return ((uintptr_t)ptr & 15u) == 0; }
+
+template <int KT, int MAXE>
+bool dgrad_config(const Shape& s, DgradParams& p) {
+    p.hspan = (int32_t)((kDgRT + s.k_h - 2) / s.s_h + 1);
+    p.gps = p.hspan * KT + 1;
+    p.gcount = kPairs * p.hspan * KT;
+    p.kbase = (kPairs * p.gps + 3) / 4 * 4;
+    p.kcount = (int32_t)(s.k_h * kDgJT * KT);
+    p.stage = p.kbase + (int32_t)(s.k_h * kDgJT * (KT + 1));
+    if ((int64_t)p.gcount + p.kcount > (int64_t)MAXE * kGradThreads) return false;
+    if ((size_t)p.stage * sizeof(float) > kGradLdsBudget) return false;
+    p.nbuf = (size_t)2 * p.stage * sizeof(float) <= kGradLdsBudget ? 2 : 1;
+    p.nchunks = (int32_t)((s.k_c + KT - 1) / KT);
+    p.div_hkt = FastDiv((uint32_t)(p.hspan * KT));
+    return true;
+}
+
+int64_t wgrad_tiles(const Shape& s) {
+    return ((s.k_h * s.R + kWgJT - 1) / kWgJT) * ((s.k_c + kWgMT - 1) / kWgMT);
+}
+
+int64_t wgrad_stages(const Shape& s) {
+    return ((s.pairs + kWgPT - 1) / kWgPT) * ((s.o_h + kWgHT - 1) / kWgHT);
+}
+
+}  // namespace
+
+bool dgrad_supported(const Shape& s) {
+    DgradParams p{};
+    if (s.R > (int64_t(1) << 26) || s.k_h > 4096) return false;
+    return dgrad_config<8, 16>(s, p) || dgrad_config<8, 32>(s, p) || dgrad_config<2, 32>(s, p);
+}
+
+hipError_t launch_dgrad_dl(const Shape& s, const float* G, const float* K, float* dL,
+                           hipStream_t stream) {
+    DgradParams p{};
+    p.G = G;
+    p.K = K;
+    p.dL = dL;
+    p.i_h = (int32_t)s.i_h;
+    p.o_h = (int32_t)s.o_h;
+    p.o_w = (int32_t)s.o_w;
+    p.k_h = (int32_t)s.k_h;
+    p.s_h = (int32_t)s.s_h;
+    p.k_c = (int32_t)s.k_c;
+    p.R = (int32_t)s.R;
+    p.pairs = (int32_t)s.pairs;
+    p.r_tiles = (int32_t)((s.i_h + kDgRT - 1) / kDgRT);
+    p.j_tiles = (int32_t)((s.R + kDgJT - 1) / kDgJT);
+    const int64_t ntiles = ((s.pairs + kPairs - 1) / kPairs) * p.r_tiles * p.j_tiles;
+    if (ntiles > 0x7fffffff) return hipErrorInvalidValue;
+    p.ntiles = (uint32_t)ntiles;
+    // the smallest prefetch that holds one stage: fewer registers, no spills
+#define MEC_DGRAD(KT, MAXE)                                                                   \
+    if (dgrad_config<KT, MAXE>(s, p)) {                                                       \
+        auto kern = dgrad_dl_kernel<KT, MAXE>;                                                \
+        hipLaunchKernelGGL(kern, dim3(p.ntiles), dim3(kGradThreads),                          \
+                           (size_t)p.nbuf * p.stage * sizeof(float), stream, p);              \
+        return hipGetLastError();                                                             \
+    }
+    MEC_DGRAD(8, 16)
+    MEC_DGRAD(8, 32)
+    MEC_DGRAD(2, 32)
+#undef MEC_DGRAD
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_fold(const Shape& s, const float* dL, float* dI, hipStream_t stream) {
+    FoldParams p{};
+    p.dL = dL;
+    p.dI = dI;
+    p.i_h = (uint32_t)s.i_h;
+    p.i_w = (uint32_t)s.i_w;
+    p.i_c = (uint32_t)s.i_c;
+    p.k_w = (uint32_t)s.k_w;
+    p.s_w = (uint32_t)s.s_w;
+    p.o_w = (uint32_t)s.o_w;
+    p.R = (uint32_t)s.R;
+    p.div_ic = FastDiv(p.i_c);
+    p.div_iw = FastDiv(p.i_w);
+    p.div_ih = FastDiv(p.i_h);
+    const int64_t elems = s.i_n * s.i_h * s.i_w * s.i_c;
+    const bool vec = s.i_c % 4 == 0 && aligned16(dL) && aligned16(dI);
+    p.units = (uint32_t)(vec ? elems / 4 : elems);
+    int64_t blocks = ((int64_t)p.units + kGradThreads - 1) / kGradThreads;
+    if (blocks > 65536) blocks = 65536;
+    if (blocks < 1) blocks = 1;
+    if (vec)
+        hipLaunchKernelGGL(fold_kernel<4>, dim3((uint32_t)blocks), dim3(kGradThreads), 0, stream, p);
+    else
+        hipLaunchKernelGGL(fold_kernel<1>, dim3((uint32_t)blocks), dim3(kGradThreads), 0, stream, p);
+    return hipGetLastError();
+}
+
+int64_t wgrad_splits(const Shape& s) {
+    // enough workgroups to fill the chip about four times over, at most one
+    // per stage, and partial sums within 256 MiB
+    const int64_t tiles = wgrad_tiles(s);
+    int64_t splits = (1024 + tiles - 1) / tiles;
+    const int64_t stages = wgrad_stages(s);
+    if (splits > stages) splits = stages;
+    const int64_t E = s.k_h * s.R * s.k_c;
+    const int64_t cap = (int64_t(64) << 20) / E;
+    if (splits > cap) splits = cap;
+    return splits < 1 ? 1 : splits;
+}
+
+int64_t wgrad_partial_bytes(const Shape& s) {
+    return wgrad_splits(s) * s.k_h * s.R * s.k_c * (int64_t)sizeof(float);
+}
+
+bool wgrad_supported(const Shape& s) {
+    const int64_t E = s.k_h * s.R * s.k_c;
+    return E < (int64_t(1) << 30) && s.k_h * s.R < (int64_t(1) << 30) &&
+           wgrad_stages(s) < (int64_t(1) << 30) && s.pairs < (int64_t(1) << 30) &&
+           wgrad_tiles(s) * wgrad_splits(s) < (int64_t(1) << 31);
+}
+
+hipError_t launch_wgrad(const Shape& s, const float* L, const float* G, float* part, float* dK,
+                        hipStream_t stream) {
+    WgradParams p{};
+    p.L = L;
+    p.G = G;
+    p.part = part;
+    p.i_h = (int32_t)s.i_h;
+    p.o_h = (int32_t)s.o_h;
+    p.o_w = (int32_t)s.o_w;
+    p.k_c = (int32_t)s.k_c;
+    p.s_h = (int32_t)s.s_h;
+    p.R = (int32_t)s.R;
+    p.KD = (int32_t)(s.k_h * s.R);
+    p.pairs = (int32_t)s.pairs;
+    p.h_chunks = (int32_t)((s.o_h + kWgHT - 1) / kWgHT);
+    p.nstages = (int32_t)wgrad_stages(s);
+    p.splits = (int32_t)wgrad_splits(s);
+    p.j_tiles = (int32_t)((p.KD + kWgJT - 1) / kWgJT);
+    p.m_tiles = (int32_t)((s.k_c + kWgMT - 1) / kWgMT);
+    p.ntiles = (uint32_t)((int64_t)p.j_tiles * p.m_tiles * p.splits);
+    p.lvec = s.R % 4 == 0 && aligned16(L);
+    p.gvec = s.k_c % 4 == 0 && aligned16(G);
+    p.div_ow = FastDiv((uint32_t)s.o_w);
+    hipLaunchKernelGGL(wgrad_kernel, dim3(p.ntiles), dim3(kGradThreads), 0, stream, p);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int64_t E = (int64_t)p.KD * s.k_c;
+    const bool vec = E % 4 == 0 && aligned16(part) && aligned16(dK);
+    const uint32_t units = (uint32_t)(vec ? E / 4 : E);
+    int64_t blocks = ((int64_t)units + kGradThreads - 1) / kGradThreads;
+    if (blocks > 65536) blocks = 65536;
+    if (vec)
+        hipLaunchKernelGGL(wgrad_reduce_kernel<4>, dim3((uint32_t)blocks), dim3(kGradThreads), 0,
+                           stream, part, dK, units, (uint32_t)E, p.splits);
+    else
+        hipLaunchKernelGGL(wgrad_reduce_kernel<1>, dim3((uint32_t)blocks), dim3(kGradThreads), 0,
+                           stream, part, dK, units, (uint32_t)E, p.splits);
+    return hipGetLastError();
+}
+
+}  // namespace mec

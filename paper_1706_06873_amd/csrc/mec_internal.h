@@ -98,6 +98,21 @@ bool gemm_supported(const Shape& s, int dtype);
 hipError_t launch_gemm_fixed(const Shape& s, const void* A, const void* K, float* O, int dtype,
                              bool fused, hipStream_t stream, bool dry_run);
 
+// ---------------------------------------------------------------- training passes
+// dL (fp32, L's layout) from G = dloss/dO and K, fp32.
+bool dgrad_supported(const Shape& s);
+hipError_t launch_dgrad_dl(const Shape& s, const float* G, const float* K, float* dL,
+                           hipStream_t stream);
+// dI from dL: the adjoint of the lowering.
+hipError_t launch_fold(const Shape& s, const float* dL, float* dI, hipStream_t stream);
+// dK from L and G: partial sums over shares of the reduction into `part`
+// (wgrad_partial_bytes), then their sum into dK.
+bool wgrad_supported(const Shape& s);
+int64_t wgrad_splits(const Shape& s);
+int64_t wgrad_partial_bytes(const Shape& s);
+hipError_t launch_wgrad(const Shape& s, const float* L, const float* G, float* part, float* dK,
+                        hipStream_t stream);
+
 }  // namespace mec
 
 #if defined(__HIP__)

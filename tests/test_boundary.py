@@ -247,3 +247,78 @@ int main() {
     out = subprocess.run([str(exe)], capture_output=True, text=True)
     assert out.returncode == 0, out.stdout
     assert " 0 wrong" in out.stdout
+
+
+# ---------------------------------------------------------------- training passes
+
+def test_grad_enums_match_header():
+    text = open(HEADER).read()
+    codes = dict((k, int(v)) for k, v in re.findall(r"(MEC_\w+)\s*=\s*(-?\d+)", text))
+    assert codes["MEC_GRAD_INPUT"] == mec.GRAD_INPUT
+    assert codes["MEC_GRAD_KERNEL"] == mec.GRAD_KERNEL
+    assert codes["MEC_GRAD_KERNEL_FROM_L"] == mec.GRAD_KERNEL_FROM_L
+
+
+@pytest.mark.parametrize("shape", SHAPES)
+def test_grad_workspace_sizes(orc, shape):
+    nL = orc.lowered_elems(*shape)
+    i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w = shape
+    if i_n * i_h * i_w * i_c >= 2 ** 31:
+        assert mec.lib.mec_grad_workspace_bytes(*shape, 0, 0) == -5
+        return
+    # dI: dL in fp32, exactly |L| * 4
+    assert mec.grad_workspace_bytes(*shape, grad_pass=mec.GRAD_INPUT) == nL * 4
+    # dK: whole partial-sum buffers of k_h*k_w*i_c*k_c floats, 1..1024 of them
+    part = mec.grad_workspace_bytes(*shape, grad_pass=mec.GRAD_KERNEL_FROM_L)
+    E = k_h * k_w * i_c * k_c * 4
+    assert part % E == 0 and 1 <= part // E <= 1024
+    # from I: L in fp32 (rounded up to 256 bytes), then the partial sums
+    assert mec.grad_workspace_bytes(*shape, grad_pass=mec.GRAD_KERNEL) == \
+        (nL * 4 + 255) // 256 * 256 + part
+
+
+def test_grad_rejects_bf16_and_bad_pass():
+    L = mec.lib
+    assert L.mec_grad_workspace_bytes(*GOOD, 1, 0) == -5
+    assert L.mec_grad_workspace_bytes(*GOOD, 2, 0) == -1
+    assert L.mec_grad_workspace_bytes(*GOOD, 0, 3) == -1
+    assert L.mec_dgrad_gemm(FAKE, FAKE, FAKE, *GOOD, 1, NULL) == -5
+    assert L.mec_conv2d_dgrad(FAKE, FAKE, FAKE, FAKE, 1 << 30, *GOOD, 1, NULL) == -5
+    assert L.mec_wgrad_gemm(FAKE, FAKE, FAKE, FAKE, 1 << 30, *GOOD, 1, NULL) == -5
+    assert L.mec_conv2d_wgrad(FAKE, FAKE, FAKE, FAKE, 1 << 30, *GOOD, 1, NULL) == -5
+
+
+@pytest.mark.parametrize("dims", BAD_DIMS)
+def test_grad_invalid_dims(dims):
+    L = mec.lib
+    assert L.mec_grad_workspace_bytes(*dims, 0, 0) == -1
+    assert L.mec_fold(FAKE, FAKE, *dims, NULL) == -1
+    assert L.mec_dgrad_gemm(FAKE, FAKE, FAKE, *dims, 0, NULL) == -1
+    assert L.mec_conv2d_dgrad(FAKE, FAKE, FAKE, FAKE, 1 << 40, *dims, 0, NULL) == -1
+    assert L.mec_wgrad_gemm(FAKE, FAKE, FAKE, FAKE, 1 << 40, *dims, 0, NULL) == -1
+    assert L.mec_conv2d_wgrad(FAKE, FAKE, FAKE, FAKE, 1 << 40, *dims, 0, NULL) == -1
+
+
+def test_grad_null_alignment_and_workspace():
+    L = mec.lib
+    big = 1 << 30
+    assert L.mec_fold(NULL, FAKE, *GOOD, NULL) == -1
+    assert L.mec_fold(FAKE, NULL, *GOOD, NULL) == -1
+    assert L.mec_fold(ODD, FAKE, *GOOD, NULL) == -3
+    for bad in ((NULL, FAKE, FAKE), (FAKE, NULL, FAKE), (FAKE, FAKE, NULL)):
+        assert L.mec_dgrad_gemm(*bad, *GOOD, 0, NULL) == -1
+        assert L.mec_conv2d_dgrad(*bad, FAKE, big, *GOOD, 0, NULL) == -1
+        assert L.mec_wgrad_gemm(*bad, FAKE, big, *GOOD, 0, NULL) == -1
+        assert L.mec_conv2d_wgrad(*bad, FAKE, big, *GOOD, 0, NULL) == -1
+    assert L.mec_dgrad_gemm(FAKE, ODD, FAKE, *GOOD, 0, NULL) == -3
+    assert L.mec_conv2d_dgrad(FAKE, FAKE, ODD, FAKE, big, *GOOD, 0, NULL) == -3
+    assert L.mec_wgrad_gemm(ODD, FAKE, FAKE, FAKE, big, *GOOD, 0, NULL) == -3
+    assert L.mec_conv2d_wgrad(FAKE, FAKE, FAKE, ODD, big, *GOOD, 0, NULL) == -3
+    need_i = mec.grad_workspace_bytes(*GOOD, grad_pass=mec.GRAD_INPUT)
+    need_k = mec.grad_workspace_bytes(*GOOD, grad_pass=mec.GRAD_KERNEL)
+    need_l = mec.grad_workspace_bytes(*GOOD, grad_pass=mec.GRAD_KERNEL_FROM_L)
+    assert L.mec_conv2d_dgrad(FAKE, FAKE, FAKE, FAKE, need_i - 4, *GOOD, 0, NULL) == -2
+    assert L.mec_conv2d_dgrad(FAKE, FAKE, FAKE, NULL, need_i, *GOOD, 0, NULL) == -2
+    assert L.mec_conv2d_wgrad(FAKE, FAKE, FAKE, FAKE, need_k - 4, *GOOD, 0, NULL) == -2
+    assert L.mec_wgrad_gemm(FAKE, FAKE, FAKE, FAKE, need_l - 4, *GOOD, 0, NULL) == -2
+    assert L.mec_wgrad_gemm(FAKE, FAKE, FAKE, NULL, need_l, *GOOD, 0, NULL) == -2
