@@ -36,12 +36,12 @@ namespace mec {
 namespace {
 
 constexpr int kGradThreads = 256;
-constexpr size_t kGradLdsBudget = 64 * 1024;
 
 // ---------------------------------------------------------------- dgrad: dL
 constexpr int kDgRT = 8;   // rows of dL per tile
 constexpr int kDgJT = 64;  // columns of dL per tile: two 32-wide MFMA blocks
 constexpr int kDgRW = 4;   // rows per wave; waves = 2 row groups x 2 column blocks
+constexpr size_t kDgLdsBudget = 80 * 1024;  // two workgroups per compute unit
 
 struct DgradParams {
     const float* G;
@@ -53,19 +53,25 @@ struct DgradParams {
     uint32_t ntiles;
     int32_t hspan;    // G rows a tile stages: (RT + k_h - 2) / s_h + 1
     int32_t nchunks;  // chunks of KT output channels
-    int32_t gps;      // LDS stride between pairs in the G stage: hspan*KT + 1
-    int32_t gcount;   // elements of the G stage: 32 * hspan * KT
+    int32_t gps;      // LDS stride between pairs in the G stage: hspan*KT + 1 (odd)
+    int32_t gunits;   // load units of the G stage: 32 * hspan * KT / VW
     int32_t kbase;    // LDS offset of the K stage
-    int32_t kcount;   // elements of the K stage: k_h * JT * KT
-    int32_t stage;    // LDS elements of one stage
+    int32_t kunits;   // load units of the K stage: k_h * JT * KT / VW
+    int32_t stage;    // LDS floats of one stage
     int32_t nbuf;     // stages in LDS: 2 (double-buffered) or 1
-    FastDiv div_hkt;  // by hspan * KT
+    FastDiv div_gu;   // by hspan * KT / VW (units per staged pair)
 };
 
-// KT: output channels per chunk. MAXE: stage elements one thread moves
-// (registers of the prefetch); the host checks (gcount + kcount) fits.
-template <int KT, int MAXE>
+// KT: output channels per chunk. VW: channels per global load (4: one
+// 16-byte load, k_c % 4 == 0 and G, K aligned; 1: one element). MAXU: load
+// units one thread moves per stage (the prefetch registers); the host checks
+// that a stage fits. LDS rows have odd strides, so the MFMA operand reads of
+// the 32 rows of a block hit 32 different banks; the staging therefore
+// writes LDS one element at a time.
+template <int KT, int VW, int MAXU>
 __global__ __launch_bounds__(kGradThreads) void dgrad_dl_kernel(DgradParams p) {
+    typedef float vec_t __attribute__((ext_vector_type(VW)));
+    constexpr int QU = KT / VW;  // load units per staged row
     extern __shared__ __align__(16) float dg_smem[];
     __shared__ int64_t gbase[kPairs];  // G offset of (n, 0, w, 0), or -1 past the last pair
     __shared__ int64_t lbase[kPairs];  // dL offset of pair row (n, w)
@@ -96,40 +102,41 @@ __global__ __launch_bounds__(kGradThreads) void dgrad_dl_kernel(DgradParams p) {
     }
     __syncthreads();
 
-    const int total = p.gcount + p.kcount;
-    // stage element e of the chunk starting at channel m0: its LDS offset and
-    // global source (nullptr where the stage holds zeros)
-    auto map = [&](int e, int m0, int& off) -> const float* {
-        if (e < p.gcount) {
-            const int pp = (int)p.div_hkt.div((uint32_t)e);
-            const int rem = e - pp * p.hspan * KT;
-            const int hh = rem / KT, mm = rem - (rem / KT) * KT;
-            off = pp * p.gps + hh * KT + mm;
-            const int h = h_min + hh, m = m0 + mm;
+    const int total = p.gunits + p.kunits;
+    // load unit u of the chunk starting at channel m0: its LDS offset and
+    // global source (nullptr where the stage holds zeros). With VW = 4 and
+    // k_c % 4 == 0 a unit is wholly inside or wholly past the k_c channels.
+    auto map = [&](int u, int m0, int& off) -> const float* {
+        if (u < p.gunits) {
+            const int pp = (int)p.div_gu.div((uint32_t)u);
+            const int rem = u - pp * p.hspan * QU;
+            const int hh = rem / QU, q = rem - (rem / QU) * QU;
+            off = pp * p.gps + hh * KT + q * VW;
+            const int h = h_min + hh, m = m0 + q * VW;
             const int64_t gb = gbase[pp];
             if (gb >= 0 && h < p.o_h && m < p.k_c) return p.G + gb + (int64_t)h * p.o_w * p.k_c + m;
             return nullptr;
         }
-        const int e2 = e - p.gcount;
-        const int a = e2 / (kDgJT * KT);
-        const int rem = e2 - a * (kDgJT * KT);
-        const int jj = rem / KT, mm = rem - (rem / KT) * KT;
-        off = p.kbase + (a * kDgJT + jj) * (KT + 1) + mm;
-        const int j = j0 + jj, m = m0 + mm;
+        const int u2 = u - p.gunits;
+        const int a = u2 / (kDgJT * QU);
+        const int rem = u2 - a * (kDgJT * QU);
+        const int jj = rem / QU, q = rem - (rem / QU) * QU;
+        off = p.kbase + (a * kDgJT + jj) * (KT + 1) + q * VW;
+        const int j = j0 + jj, m = m0 + q * VW;
         if (j < p.R && m < p.k_c) return p.K + ((int64_t)a * p.R + j) * p.k_c + m;
         return nullptr;
     };
 
-    float regs[MAXE];
+    vec_t regs[MAXU];
     auto load = [&](int rc) {
         int off;
 #pragma unroll
-        for (int i = 0; i < MAXE; ++i) {
-            const int e = tid + i * kGradThreads;
-            float v = 0.f;
-            if (e < total) {
-                const float* src = map(e, rc * KT, off);
-                if (src) v = *src;
+        for (int i = 0; i < MAXU; ++i) {
+            const int u = tid + i * kGradThreads;
+            vec_t v = {};
+            if (u < total) {
+                const float* src = map(u, rc * KT, off);
+                if (src) v = *reinterpret_cast<const vec_t*>(src);
             }
             regs[i] = v;
         }
@@ -137,11 +144,12 @@ __global__ __launch_bounds__(kGradThreads) void dgrad_dl_kernel(DgradParams p) {
     auto store = [&](float* st) {
         int off;
 #pragma unroll
-        for (int i = 0; i < MAXE; ++i) {
-            const int e = tid + i * kGradThreads;
-            if (e < total) {
-                (void)map(e, 0, off);
-                st[off] = regs[i];
+        for (int i = 0; i < MAXU; ++i) {
+            const int u = tid + i * kGradThreads;
+            if (u < total) {
+                (void)map(u, 0, off);
+#pragma unroll
+                for (int k = 0; k < VW; ++k) st[off + k] = regs[i][k];
             }
         }
     };
@@ -407,19 +415,19 @@ __global__ __launch_bounds__(kGradThreads) void wgrad_reduce_kernel(const float*
 
 inline bool aligned16(const void* ptr) { return ((uintptr_t)ptr & 15u) == 0; }
 
-template <int KT, int MAXE>
+template <int KT, int VW, int MAXU>
 bool dgrad_config(const Shape& s, DgradParams& p) {
     p.hspan = (int32_t)((kDgRT + s.k_h - 2) / s.s_h + 1);
     p.gps = p.hspan * KT + 1;
-    p.gcount = kPairs * p.hspan * KT;
-    p.kbase = (kPairs * p.gps + 3) / 4 * 4;
-    p.kcount = (int32_t)(s.k_h * kDgJT * KT);
+    p.gunits = kPairs * p.hspan * (KT / VW);
+    p.kbase = kPairs * p.gps;
+    p.kunits = (int32_t)(s.k_h * kDgJT * (KT / VW));
     p.stage = p.kbase + (int32_t)(s.k_h * kDgJT * (KT + 1));
-    if ((int64_t)p.gcount + p.kcount > (int64_t)MAXE * kGradThreads) return false;
-    if ((size_t)p.stage * sizeof(float) > kGradLdsBudget) return false;
-    p.nbuf = (size_t)2 * p.stage * sizeof(float) <= kGradLdsBudget ? 2 : 1;
+    if ((int64_t)p.gunits + p.kunits > (int64_t)MAXU * kGradThreads) return false;
+    if ((size_t)p.stage * sizeof(float) > kDgLdsBudget) return false;
+    p.nbuf = (size_t)2 * p.stage * sizeof(float) <= kDgLdsBudget ? 2 : 1;
     p.nchunks = (int32_t)((s.k_c + KT - 1) / KT);
-    p.div_hkt = FastDiv((uint32_t)(p.hspan * KT));
+    p.div_gu = FastDiv((uint32_t)(p.hspan * (KT / VW)));
     return true;
 }
 
@@ -436,7 +444,8 @@ int64_t wgrad_stages(const Shape& s) {
 bool dgrad_supported(const Shape& s) {
     DgradParams p{};
     if (s.R > (int64_t(1) << 26) || s.k_h > 4096) return false;
-    return dgrad_config<8, 16>(s, p) || dgrad_config<8, 32>(s, p) || dgrad_config<2, 32>(s, p);
+    return dgrad_config<16, 1, 32>(s, p) || dgrad_config<8, 1, 32>(s, p) ||
+           dgrad_config<2, 1, 32>(s, p);
 }
 
 hipError_t launch_dgrad_dl(const Shape& s, const float* G, const float* K, float* dL,
@@ -458,17 +467,28 @@ hipError_t launch_dgrad_dl(const Shape& s, const float* G, const float* K, float
     const int64_t ntiles = ((s.pairs + kPairs - 1) / kPairs) * p.r_tiles * p.j_tiles;
     if (ntiles > 0x7fffffff) return hipErrorInvalidValue;
     p.ntiles = (uint32_t)ntiles;
-    // the smallest prefetch that holds one stage: fewer registers, no spills
-#define MEC_DGRAD(KT, MAXE)                                                                   \
-    if (dgrad_config<KT, MAXE>(s, p)) {                                                       \
-        auto kern = dgrad_dl_kernel<KT, MAXE>;                                                \
-        hipLaunchKernelGGL(kern, dim3(p.ntiles), dim3(kGradThreads),                          \
-                           (size_t)p.nbuf * p.stage * sizeof(float), stream, p);              \
-        return hipGetLastError();                                                             \
+    // 16-byte loads when every chunk row starts on a 16-byte boundary; the
+    // smallest prefetch that holds one stage (fewer registers, no spills);
+    // double-buffered stages first, then single.
+    const bool vec = s.k_c % 4 == 0 && ((uintptr_t)G & 15u) == 0 && ((uintptr_t)K & 15u) == 0;
+#define MEC_DGRAD(KT, VW, MAXU)                                                                \
+    if (dgrad_config<KT, VW, MAXU>(s, p) && p.nbuf >= min_buf) {                               \
+        auto kern = dgrad_dl_kernel<KT, VW, MAXU>;                                             \
+        hipLaunchKernelGGL(kern, dim3(p.ntiles), dim3(kGradThreads),                           \
+                           (size_t)p.nbuf * p.stage * sizeof(float), stream, p);               \
+        return hipGetLastError();                                                              \
     }
-    MEC_DGRAD(8, 16)
-    MEC_DGRAD(8, 32)
-    MEC_DGRAD(2, 32)
+    for (int min_buf = 2; min_buf >= 1; --min_buf) {
+        if (vec) {
+            MEC_DGRAD(16, 4, 8)
+            MEC_DGRAD(16, 4, 16)
+            MEC_DGRAD(8, 4, 16)
+            MEC_DGRAD(4, 4, 16)
+        }
+        MEC_DGRAD(16, 1, 32)
+        MEC_DGRAD(8, 1, 32)
+        MEC_DGRAD(2, 1, 32)
+    }
 #undef MEC_DGRAD
     return hipErrorInvalidValue;
 }

@@ -3,12 +3,18 @@
     python -m paper_1706_06873_amd.suite table2 [--batch 32] [--dtype f32|bf16|both]
     python -m paper_1706_06873_amd.suite stride [--batch 32] [--dtype f32]
     python -m paper_1706_06873_amd.suite resnet101 [--batch 1] [--dtype f32]
+    python -m paper_1706_06873_amd.suite train [--layers resnet_mid,cv9,...] [--yardstick]
 
 ``table2`` runs the twelve layers of Table 2 (cv1-cv12), ``stride`` runs cv1
 (227x227x3 input, 11x11x96 kernel) with s_h = s_w = 1..10 as in Fig. 4(a),
 ``resnet101`` runs the five layers of Table 3 (cv4, cv9-cv12) and ends with a
 summary line weighing each layer by its count in ResNet-101, as Table 3 does:
-weighted workspace (MiB) and weighted time of MEC against im2col.
+weighted workspace (MiB) and weighted time of MEC against im2col. ``train``
+times the training passes (fp32) per layer: the input gradient (dL by the
+slab products against K, then the fold) and the kernel gradient (lowering,
+then the partial A_h^T G_h sums and their reduction), each kernel between
+HIP events; with ``--yardstick`` it also times torch's own convolution
+gradients (the vendor library) on the same shapes in NCHW, for context.
 For every layer it times MEC from L (compact lowering + slab products), MEC
 fused, and the im2col baseline (im2col lowering + one product through the
 same kernels), each kernel between HIP events on its stream, on seeded
@@ -18,6 +24,7 @@ against im2col. Parity of every one of these shapes with the CPU oracle is
 checked by the GPU tests, not here.
 """
 import argparse
+import dataclasses
 import json
 import sys
 
@@ -97,9 +104,71 @@ def _time_layer(layer, reps, warmup, sets):
                                                                        res["fused"]["us"]), 3)}
 
 
+def _time_train(layer, reps, warmup, yardstick):
+    i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w = layer.dims
+    o_h, o_w = mec.output_dims(i_h, i_w, k_h, k_w, s_h, s_w)
+    macs = i_n * o_h * o_w * k_c * k_h * k_w * i_c
+    dev = torch.device("cuda:0")
+    I0, K0 = wl.make_inputs(layer)
+    G0 = torch.rand((i_n, o_h, o_w, k_c), generator=torch.Generator().manual_seed(layer.seed + 7))
+    I, K, G = I0.to(dev), K0.to(dev), (G0 * 2 - 1).to(dev)
+    dI = torch.empty_like(I)
+    dK = torch.empty_like(K)
+    dL = torch.empty((i_n, o_w, i_h, k_w, i_c), dtype=torch.float32, device=dev)
+    L = torch.empty_like(dL)
+    part = torch.empty(mec.grad_workspace_bytes(*layer.dims, grad_pass=mec.GRAD_KERNEL_FROM_L),
+                       dtype=torch.uint8, device=dev)
+    stream = torch.cuda.Stream(device=dev)
+    steps = {
+        "dgrad_products": lambda: mec.dgrad_gemm(G, K, i_h, i_w, s_h, s_w, dL=dL, stream=stream),
+        "fold": lambda: mec.fold(dL, i_w, s_w, dI=dI, stream=stream),
+        "lower": lambda: mec.lower(I, k_h, k_w, k_c, s_h, s_w, L=L, stream=stream),
+        "wgrad_products": lambda: mec.wgrad_gemm(L, G, k_h, i_w, s_h, s_w, dK=dK, workspace=part,
+                                                 stream=stream),
+    }
+    if yardstick:
+        In = I.permute(0, 3, 1, 2).contiguous()
+        Kn = K.permute(3, 2, 0, 1).contiguous()
+        Gn = G.permute(0, 3, 1, 2).contiguous()
+        steps["vendor_dgrad"] = lambda: torch.nn.grad.conv2d_input(In.shape, Kn, Gn, stride=(s_h, s_w))
+        steps["vendor_wgrad"] = lambda: torch.nn.grad.conv2d_weight(In, Kn.shape, Gn, stride=(s_h, s_w))
+    times = {}
+    with torch.cuda.stream(stream):
+        for name, fn in steps.items():
+            for _ in range(warmup):
+                fn()
+            torch.cuda.synchronize()
+            ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                  for _ in range(reps)]
+            for a, b in ev:
+                a.record(stream)
+                fn()
+                b.record(stream)
+            torch.cuda.synchronize()
+            t = sorted(a.elapsed_time(b) * 1e3 for a, b in ev)
+            times[name] = round(t[len(t) // 2], 2)
+    tf = lambda us: round(2.0 * macs / (us * 1e-6) / 1e12, 2)
+    out = {"layer": layer.name, "dims": list(layer.dims), "gflop": round(2.0 * macs / 1e9, 3),
+           "us": times,
+           "dgrad_us": round(times["dgrad_products"] + times["fold"], 2),
+           "wgrad_us": round(times["lower"] + times["wgrad_products"], 2)}
+    out["dgrad_products_tflops"] = tf(times["dgrad_products"])
+    out["wgrad_products_tflops"] = tf(times["wgrad_products"])
+    out["dgrad_products_frac_fp32_mfma"] = round(out["dgrad_products_tflops"] / 157.3, 3)
+    out["wgrad_products_frac_fp32_mfma"] = round(out["wgrad_products_tflops"] / 157.3, 3)
+    fold_bytes = 4 * (dL.numel() + dI.numel())
+    out["fold_tbps"] = round(fold_bytes / (times["fold"] * 1e-6) / 1e12, 3)
+    if yardstick:
+        out["vendor_dgrad_tflops"] = tf(times["vendor_dgrad"])
+        out["vendor_wgrad_tflops"] = tf(times["vendor_wgrad"])
+    return out
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
-    ap.add_argument("which", choices=["table2", "stride", "resnet101"])
+    ap.add_argument("which", choices=["table2", "stride", "resnet101", "train"])
+    ap.add_argument("--yardstick", action="store_true",
+                    help="train: also time torch's convolution gradients")
     ap.add_argument("--batch", type=int, default=None,
                     help="images per layer (default 32; 1 for resnet101, as in Table 3)")
     ap.add_argument("--dtype", default="f32", choices=["f32", "bf16", "both"])
@@ -113,6 +182,16 @@ def main(argv=None):
         return 1
     dtypes = ["f32", "bf16"] if args.dtype == "both" else [args.dtype]
     batch = args.batch or (1 if args.which == "resnet101" else 32)
+    if args.which == "train":
+        names = args.layers.split(",") if args.layers else ["resnet_mid", "alexnet_conv1",
+                                                            "vgg_first"] + list(wl.TABLE2)
+        for name in names:
+            layer = wl.LAYERS[name] if name in wl.LAYERS else wl.table2_layer(name, batch)
+            if args.batch and name in wl.LAYERS:
+                layer = dataclasses.replace(layer, i_n=args.batch)
+            print(json.dumps(_time_train(layer, args.reps, args.warmup, args.yardstick)),
+                  flush=True)
+        return 0
     if args.which == "table2":
         names = args.layers.split(",") if args.layers else list(wl.TABLE2)
         layers = [wl.table2_layer(n, batch, d) for d in dtypes for n in names]
