@@ -3,8 +3,9 @@
 Each case copies the oracle's C source, makes one plausible mistake in it (a
 flipped or transposed kernel index, a swapped stride, a dropped term, a wrong
 lowering offset, a missing transpose, a narrower accumulator, a wrong bf16
-widening), builds the copy with gcc and runs the pin battery of
-test_oracle_pins.py against it. At least one pin must fail. Every mutant keeps
+widening, and in the training passes a flipped kernel row, a swapped stride,
+a fold or slab offset without its stride), builds the copy with gcc and runs
+the pin battery of test_oracle_pins.py and test_oracle_training.py against it. At least one pin must fail. Every mutant keeps
 all memory accesses in bounds, so a mutant can only give wrong values.
 """
 import os
@@ -15,6 +16,7 @@ import pytest
 
 import oracle
 import test_oracle_pins as pins
+import test_oracle_training as tpins
 
 SRC = os.path.join(os.path.dirname(oracle.__file__), "mec_oracle.c")
 
@@ -41,6 +43,18 @@ MUTANTS = {
     "bf16_widen_wrong": ("uint32_t bits = (uint32_t)((const uint16_t*)base)[idx] << 16;",
                          "uint32_t bits = (uint32_t)((const uint16_t*)base)[idx] << 15;"),
     "vanilla_ld_wrong": ("int64_t ld = i_h * k_w;", "int64_t ld = i_h * k_w - 1;"),
+    # training passes
+    "dgrad_kernel_flipped": ("g * elem(K, ((a * k_w + b) * i_c + c) * k_c + m, dtype);",
+                             "g * elem(K, (((k_h - 1 - a) * k_w + b) * i_c + c) * k_c + m, dtype);"),
+    "wgrad_rows_flipped": ("acc += elem(I, ((n * i_h + (y * s_h + a)) * i_w + (x * s_w + b)) * i_c + c, dtype) *",
+                           "acc += elem(I, ((n * i_h + (y * s_h + (k_h - 1 - a))) * i_w + (x * s_w + b)) * i_c + c, dtype) *"),
+    "wgrad_stride_swapped": ("acc += elem(I, ((n * i_h + (y * s_h + a)) * i_w + (x * s_w + b)) * i_c + c, dtype) *",
+                             "acc += elem(I, ((n * i_h + (y * s_h + a)) * i_w + (x * s_h + b) % i_w) * i_c + c, dtype) *"),
+    "fold_no_column_stride": ("d[(h * i_w + s_w * w + b) * i_c + c] +=",
+                              "d[(h * i_w + (w + b) % i_w) * i_c + c] +="),
+    "dL_slab_offset_without_stride": ("row[s_h * R * h + j] += acc;", "row[R * h + j] += acc;"),
+    "wgrad_lowered_offset_without_stride": ("acc += elem(L, p * LD + s_h * R * h + j, dtype) *",
+                                            "acc += elem(L, p * LD + R * h + j, dtype) *"),
 }
 
 
@@ -62,6 +76,13 @@ def battery():
         checks.append(lambda shape=shape: pins.test_against_torch_conv2d_f64(o, shape))
         checks.append(lambda shape=shape: pins.test_mec_equals_im2col(o, shape))
     checks.append(lambda: pins.test_delta_kernel_reproduces_shifted_input(o, (2, 3), (3, 3)))
+    # training passes
+    checks.append(lambda: tpins.test_worked_example_closed_forms(o))
+    for d in tpins.SHAPES[:4]:
+        checks.append(lambda d=d: tpins.test_adjoint_identities_exact(o, d))
+        checks.append(lambda d=d: tpins.test_mec_forms_equal_direct(o, d))
+        checks.append(lambda d=d: tpins.test_fold_is_adjoint_of_lowering(o, d))
+    checks.append(lambda: tpins.test_delta_gradients(o, (2, 12, 11, 3, 3, 4, 5, 2, 3)))
     return checks
 
 
