@@ -292,10 +292,37 @@ def cpu_baseline(layer, I, K, macs, seconds):
         reps += 1
         if reps >= 1000:
             break
-    return {"value": round(2.0 * macs * reps / t_total / 1e12, 6), "unit": "TFLOP/s",
-            "cores": oracle.num_threads(), "kind": "oracle",
-            "sample": "full %s layer (all %d images), direct fp64-accumulated convolution, "
-                      "%d repetition(s) in %.1f s" % (layer.name, layer.i_n, reps, t_total)}
+    out = {"value": round(2.0 * macs * reps / t_total / 1e12, 6), "unit": "TFLOP/s",
+           "cores": oracle.num_threads(), "kind": "oracle",
+           "sample": "full %s layer (all %d images), direct fp64-accumulated convolution, "
+                     "%d repetition(s) in %.1f s" % (layer.name, layer.i_n, reps, t_total),
+           "cpu_model": cpu_model()}
+    # the oracle's lowering (a plain copy loop): bytes of I read + L written per second, on
+    # all the cores above and on one
+    nbytes = Ia.nbytes * (1 + oracle.lowered_elems(*layer.dims) / Ia.size)
+    for key, threads in (("lowering_gbps_all_cores", out["cores"]), ("lowering_gbps_1_core", 1)):
+        oracle.set_num_threads(threads)
+        reps, t = 0, 0.0
+        while t < 0.5 or reps < 2:
+            t0 = time.perf_counter()
+            oracle.mec_lower(Ia, layer.k_h, layer.k_w, layer.k_c, layer.s_h, layer.s_w)
+            t += time.perf_counter() - t0
+            reps += 1
+        out[key] = round(nbytes * reps / t / 1e9, 2)
+    oracle.set_num_threads(out["cores"])
+    return out
+
+
+def cpu_model():
+    """The host CPU's model name, from /proc/cpuinfo."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 if __name__ == "__main__":

@@ -55,6 +55,8 @@ def _load(path):
         getattr(L, name).restype = None
     L.oracle_num_threads.argtypes = []
     L.oracle_num_threads.restype = ctypes.c_int
+    L.oracle_set_num_threads.argtypes = [ctypes.c_int]
+    L.oracle_set_num_threads.restype = None
     return L
 
 
@@ -267,3 +269,8 @@ def mec_fold(dL, i_w, s_w):
 
 def num_threads():
     return lib().oracle_num_threads()
+
+
+def set_num_threads(n):
+    """Thread count of the oracle's later parallel loops."""
+    lib().oracle_set_num_threads(int(n))

@@ -465,6 +465,9 @@ void oracle_mec_fold(const void* dL, double* dI,
 #ifdef _OPENMP
 #include <omp.h>
 int oracle_num_threads(void) { return omp_get_max_threads(); }
+/* Thread count of later parallel regions (n >= 1), for timing on one core. */
+void oracle_set_num_threads(int n) { omp_set_num_threads(n > 0 ? n : 1); }
 #else
 int oracle_num_threads(void) { return 0; }
+void oracle_set_num_threads(int n) { (void)n; }
 #endif
