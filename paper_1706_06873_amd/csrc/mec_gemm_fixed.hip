@@ -64,7 +64,13 @@ struct F32Cfg {
     static constexpr int NG = NT / 4;                   // 4-channel groups
     static constexpr int B_ITEMS = KH * KT * NG;        // (a, r, 4-channel group)
     static constexpr int BJ = (B_ITEMS + THREADS - 1) / THREADS;
-    static constexpr int EPI_WORDS = WAVES * 32 * 40;   // epilogue: one 32x40 block per wave
+    // Epilogue through LDS: a wave's NBW blocks of one output row side by side
+    // (rows EPI_LD floats apart) when that fits in the stage memory or in
+    // 40 KB; otherwise one 32x32 block at a time (rows 40 floats apart).
+    static constexpr int EPI_WIDE_WORDS = WAVES * 32 * (32 * NBW + 8);
+    static constexpr bool WIDE_EPI = EPI_WIDE_WORDS <= 2 * STAGE || EPI_WIDE_WORDS <= 10240;
+    static constexpr int EPI_LD = WIDE_EPI ? 32 * NBW + 8 : 40;
+    static constexpr int EPI_WORDS = WAVES * 32 * EPI_LD;
     static constexpr int LDS_WORDS = 2 * STAGE > EPI_WORDS ? 2 * STAGE : EPI_WORDS;
     static constexpr size_t LDS_BYTES = LDS_WORDS * sizeof(E);
     static_assert(WAVES % WAVES_H == 0 && HT % WAVES_H == 0 && NB % WAVES_N == 0, "wave split");
@@ -301,28 +307,39 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_kernel(FixedParams p
 
     const int64_t ostride_h = p.o_w * p.k_c;
     if (p.o_vec) {
-        // Through LDS (free since the loop's last barrier): each 32x32 block is
-        // written row-major (rows 40 floats apart), then read back as four
-        // 16-byte pieces per lane, so every lane stores 16 contiguous bytes of
-        // an O row and a store instruction covers 8 whole 128-byte row segments.
-        float* blk = reinterpret_cast<float*>(lds) + wave * (32 * 40);
-        const int rr = lane >> 3, cc = (lane & 7) * 4;
+        // Through LDS (free since the loop's last barrier): accumulator blocks
+        // are written row-major, rows EPI_LD floats apart, then read back as
+        // 16-byte pieces, so each lane stores 16 contiguous bytes of O. With
+        // WIDE_EPI a wave's NBW blocks of one output row sit side by side and a
+        // store instruction covers whole 32*NBW-channel row segments of several
+        // consecutive pairs; otherwise 128-byte segments of one block.
+        constexpr int LD = C::EPI_LD;
+        constexpr int NBS = C::WIDE_EPI ? NBW : 1;  // blocks per LDS pass
+        constexpr int Q = 8 * NBS;                  // 16-byte pieces per row segment
+        constexpr int RPI = 64 / Q;                 // rows per store instruction
+        float* blk = reinterpret_cast<float*>(lds) + wave * (32 * LD);
+        const int rr = lane / Q, cc = (lane % Q) * 4;
 #pragma unroll
         for (int hw = 0; hw < HW; ++hw) {
             const int64_t h = h0 + wh * HW + hw;
 #pragma unroll
-            for (int nb = 0; nb < NBW; ++nb) {
+            for (int nb0 = 0; nb0 < NBW; nb0 += NBS) {
 #pragma unroll
-                for (int v = 0; v < 16; ++v) blk[acc_row(v, lane) * 40 + row] = acc[hw][nb][v];
+                for (int nb = 0; nb < NBS; ++nb)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v)
+                        blk[acc_row(v, lane) * LD + nb * 32 + row] = acc[hw][nb0 + nb][v];
                 __syncthreads();
-                const int c = n0 + (wn * NBW + nb) * 32 + cc;
+                const int c = n0 + (wn * NBW + nb0) * 32 + cc;
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int r = rr + 8 * i;
-                    const float4 val = *reinterpret_cast<const float4*>(blk + r * 40 + cc);
-                    const int64_t ob = obase_s[r];
-                    if (h < p.o_h && c < p.k_c && ob >= 0)
-                        store_o4_nt(p.O + ob + h * ostride_h + c, val);
+                for (int i = 0; i < (32 + RPI - 1) / RPI; ++i) {
+                    const int r = rr + RPI * i;
+                    if (rr < RPI && r < 32) {
+                        const float4 val = *reinterpret_cast<const float4*>(blk + r * LD + cc);
+                        const int64_t ob = obase_s[r];
+                        if (h < p.o_h && c < p.k_c && ob >= 0)
+                            store_o4_nt(p.O + ob + h * ostride_h + c, val);
+                    }
                 }
                 __syncthreads();
             }
