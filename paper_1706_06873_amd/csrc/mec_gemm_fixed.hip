@@ -9,8 +9,9 @@
 // (h, a) pairs with h*s_h + a equal to that row, so the slab overlap is reused
 // in registers as well as in LDS. Staging offsets are computed once per tile,
 // relative to the tile's first pair so they fit 32-bit registers; the next
-// r-chunk's global loads are issued after the first MFMA k-step of the current
-// one, and their LDS stores go to the other of two stage buffers. O is written
+// r-chunk's global loads are issued during the current one (fp32: spread over
+// its first k-steps; bf16, two k-steps per chunk: before the first), and their
+// LDS stores go to the other of two stage buffers. O is written
 // n-h-w-c with non-temporal stores.
 #include <initializer_list>
 #include <type_traits>
@@ -560,6 +561,7 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_bf16_kernel(FixedParams 
     auto compute = [&](int buf, auto mid) {
         const uint16_t* As = lds + buf * STAGE + a_lane;
         const uint16_t* Bs = lds + buf * STAGE + b_lane;
+        mid();  // the next chunk's global loads, in flight during both k-steps
 #pragma unroll
         for (int kk = 0; kk < KT; kk += 16) {
             bf16x8 af[XW];
@@ -581,7 +583,6 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_bf16_kernel(FixedParams 
                     for (int nb = 0; nb < NBW; ++nb)
                         acc[hw][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[hw * SH + a], bf[a][nb],
                                                                            acc[hw][nb], 0, 0, 0);
-            if (kk == 0) mid();
         }
     };
 
