@@ -26,8 +26,9 @@
 //            workgroup computes a 128 x 64 tile of dK (rows j = a*R + b*i_c + c,
 //            columns m) over the stages in its share, a stage being 16 pairs x
 //            4 output rows, and writes the tile to its own partial buffer.
-//  reduce    dK = the partial buffers summed in increasing share order, so the
-//            result does not depend on scheduling.
+//  reduce    dK = the partial buffers summed in a fixed order (groups of
+//            consecutive shares, then the groups), so the result does not
+//            depend on scheduling.
 // Global loads of the next stage go to registers before the current stage's
 // MFMAs and to LDS after them.
 #include "mec_mfma.h"
@@ -389,23 +390,193 @@ __global__ __launch_bounds__(kGradThreads) void wgrad_kernel(WgradParams p) {
     }
 }
 
-// dK[e] = sum over s of part[s][e], s increasing. V = 4 when E % 4 == 0 and
-// both buffers are 16-byte aligned.
+// wgrad for the common kernel heights, reusing the slab overlap: a
+// workgroup computes every kernel row a < KH for 64 columns (b, c) and 64
+// output channels, i.e. the dK rows j = a*R + r for r in [r0, r0 + 64). A
+// stage is 16 pairs x 4 output rows as above, but it holds the union of the L
+// rows those output rows read -- hrows = 3*s_h + KH rows per pair, 64 columns
+// each -- and every staged row feeds each (h, a) with h*s_h + a equal to it:
+// KH MFMAs per G fragment instead of one. Wave w computes the 32-column block
+// w & 1 and the 32-channel block w >> 1 for all KH kernel rows. VEC: 16-byte
+// staging loads (R and k_c multiples of 4, L and G 16-byte aligned).
+constexpr int kWs = 64;     // columns r and channels m per tile
+constexpr int kWsRows = 8;  // LDS rows per staged pair: 3*s_h + KH <= 8 (host check)
+template <int KH, bool VEC>
+__global__ __launch_bounds__(kGradThreads) void wgrad_slab_kernel(WgradParams p) {
+    typedef float f32x4 __attribute__((ext_vector_type(4)));
+    constexpr int HR_MAX = kWsRows;
+    constexpr int A4 = kWgPT * HR_MAX * (kWs / 4) / kGradThreads;  // float4 per thread, max
+    constexpr int B4 = kWgC * kWs / 4 / kGradThreads;
+    __shared__ __align__(16) float As[kWgPT * HR_MAX * kWs];  // [pair][staged row][r]
+    __shared__ __align__(16) float Bs[kWgC * kWs];            // [combination][m]
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int hrows = (kWgHT - 1) * p.s_h + KH;
+    const int a_units = kWgPT * hrows * (kWs / 4);
+
+    const uint32_t t = xcd_remap(blockIdx.x, p.ntiles);
+    const int rt = (int)(t % (uint32_t)p.j_tiles);
+    const uint32_t rest = t / (uint32_t)p.j_tiles;
+    const int mt = (int)(rest % (uint32_t)p.m_tiles);
+    const int s = (int)(rest / (uint32_t)p.m_tiles);
+    const int r0 = rt * kWs, m0 = mt * kWs;
+    const int st_begin = (int)((int64_t)s * p.nstages / p.splits);
+    const int st_end = (int)((int64_t)(s + 1) * p.nstages / p.splits);
+
+    f32x4 ra[A4], rb[B4];
+    auto load = [&](int st) {
+        const int pc = st / p.h_chunks, hc = st - (st / p.h_chunks) * p.h_chunks;
+        const int x0 = hc * kWgHT * p.s_h;  // first staged input row
+#pragma unroll
+        for (int i = 0; i < A4; ++i) {
+            const int u = tid + i * kGradThreads;
+            f32x4 v = {0.f, 0.f, 0.f, 0.f};
+            if (u < a_units) {
+                const int pp = u / (hrows * (kWs / 4)), rem = u - pp * hrows * (kWs / 4);
+                const int x = rem / (kWs / 4), r = r0 + (rem - x * (kWs / 4)) * 4;
+                const int pair = pc * kWgPT + pp;
+                if (pair < p.pairs && x0 + x < p.i_h) {
+                    const float* src = p.L + ((int64_t)pair * p.i_h + x0 + x) * p.R + r;
+                    if (VEC) {
+                        if (r < p.R) v = *reinterpret_cast<const f32x4*>(src);
+                    } else {
+#pragma unroll
+                        for (int k = 0; k < 4; ++k)
+                            if (r + k < p.R) v[k] = src[k];
+                    }
+                }
+            }
+            ra[i] = v;
+        }
+#pragma unroll
+        for (int i = 0; i < B4; ++i) {
+            const int u = tid + i * kGradThreads;
+            const int cidx = u >> 4, m = m0 + (u & 15) * 4;
+            const int pair = pc * kWgPT + (cidx >> 2), h = hc * kWgHT + (cidx & 3);
+            f32x4 v = {0.f, 0.f, 0.f, 0.f};
+            if (pair < p.pairs && h < p.o_h) {
+                const int n = (int)p.div_ow.div((uint32_t)pair), w = pair - n * p.o_w;
+                const float* src = p.G + (((int64_t)n * p.o_h + h) * p.o_w + w) * p.k_c + m;
+                if (VEC) {
+                    if (m < p.k_c) v = *reinterpret_cast<const f32x4*>(src);
+                } else {
+#pragma unroll
+                    for (int k = 0; k < 4; ++k)
+                        if (m + k < p.k_c) v[k] = src[k];
+                }
+            }
+            rb[i] = v;
+        }
+    };
+    auto store = [&]() {
+#pragma unroll
+        for (int i = 0; i < A4; ++i) {
+            const int u = tid + i * kGradThreads;
+            if (u < a_units) {
+                const int pp = u / (hrows * (kWs / 4)), rem = u - pp * hrows * (kWs / 4);
+                const int x = rem / (kWs / 4), q = rem - x * (kWs / 4);
+                *reinterpret_cast<f32x4*>(As + (pp * HR_MAX + x) * kWs + q * 4) = ra[i];
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < B4; ++i) {
+            const int u = tid + i * kGradThreads;
+            *reinterpret_cast<f32x4*>(Bs + (u >> 4) * kWs + (u & 15) * 4) = rb[i];
+        }
+    };
+
+    floatx16 acc[KH];
+#pragma unroll
+    for (int a = 0; a < KH; ++a)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[a][v] = 0.f;
+    const int row = lane & 31, khalf = lane >> 5;
+    const int rblk = (wave & 1) * 32, mblk = (wave >> 1) * 32;
+
+    if (st_begin < st_end) {
+        load(st_begin);
+        store();
+        __syncthreads();
+        for (int st = st_begin; st < st_end; ++st) {
+            const bool more = st + 1 < st_end;
+            if (more) load(st + 1);  // in flight during the MFMAs below
+#pragma unroll 4
+            for (int kk = 0; kk < kWgC; kk += 2) {
+                const int c = kk + khalf;  // this lane's (pair, output row) combination
+                const int pp = c >> 2, hh = c & 3;
+                const float bf = Bs[c * kWs + mblk + row];
+                const float* ap = As + (pp * HR_MAX + hh * p.s_h) * kWs + rblk + row;
+#pragma unroll
+                for (int a = 0; a < KH; ++a)
+                    acc[a] = __builtin_amdgcn_mfma_f32_32x32x2f32(ap[a * kWs], bf, acc[a], 0, 0, 0);
+            }
+            __syncthreads();  // every wave is done with this stage
+            if (more) {
+                store();
+                __syncthreads();
+            }
+        }
+    }
+
+    // lane holds C[r][m] of kernel row a: r = r0 + rblk + acc_row(v, lane), m = m0 + mblk + lane % 32
+    float* out = p.part + (int64_t)s * p.KD * p.k_c;
+    const int m = m0 + mblk + row;
+    if (m >= p.k_c) return;
+#pragma unroll
+    for (int a = 0; a < KH; ++a)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int r = r0 + rblk + acc_row(v, lane);
+            if (r < p.R) out[((int64_t)a * p.R + r) * p.k_c + m] = acc[a][v];
+        }
+}
+
+// dK[e] = the sum over shares s of part[s][e], in two passes so that many
+// workgroups share the reading: pass 1 sums each group of consecutive shares
+// (group g = shares [g*S/NG, (g+1)*S/NG)) in increasing order and writes the
+// result over the group's first share; pass 2 sums the NG group results in
+// increasing order into dK. The order is fixed, so dK does not depend on
+// scheduling. V = 4 when E % 4 == 0 and both buffers are 16-byte aligned.
+template <int V>
+__global__ __launch_bounds__(kGradThreads) void wgrad_reduce_groups_kernel(float* part, uint32_t units,
+                                                                           uint32_t E, int32_t splits,
+                                                                           int32_t groups) {
+    typedef float f32x4 __attribute__((ext_vector_type(4)));
+    const uint32_t u = blockIdx.x * kGradThreads + threadIdx.x;
+    if (u >= units) return;
+    const int g = blockIdx.y;
+    const int s0 = (int)((int64_t)g * splits / groups), s1 = (int)((int64_t)(g + 1) * splits / groups);
+    if (V == 4) {
+        f32x4 acc = *reinterpret_cast<const f32x4*>(part + (size_t)s0 * E + (size_t)u * 4);
+        for (int s = s0 + 1; s < s1; ++s)
+            acc += *reinterpret_cast<const f32x4*>(part + (size_t)s * E + (size_t)u * 4);
+        *reinterpret_cast<f32x4*>(part + (size_t)s0 * E + (size_t)u * 4) = acc;
+    } else {
+        float acc = part[(size_t)s0 * E + u];
+        for (int s = s0 + 1; s < s1; ++s) acc += part[(size_t)s * E + u];
+        part[(size_t)s0 * E + u] = acc;
+    }
+}
+
 template <int V>
 __global__ __launch_bounds__(kGradThreads) void wgrad_reduce_kernel(const float* part, float* dK,
                                                                     uint32_t units, uint32_t E,
-                                                                    int32_t splits) {
+                                                                    int32_t splits, int32_t groups) {
     typedef float f32x4 __attribute__((ext_vector_type(4)));
     const uint32_t stride = gridDim.x * kGradThreads;
     for (uint32_t u = blockIdx.x * kGradThreads + threadIdx.x; u < units; u += stride) {
         if (V == 4) {
             f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-            for (int s = 0; s < splits; ++s)
-                acc += *reinterpret_cast<const f32x4*>(part + (size_t)s * E + (size_t)u * 4);
+            for (int g = 0; g < groups; ++g) {
+                const size_t s0 = (size_t)((int64_t)g * splits / groups);
+                acc += *reinterpret_cast<const f32x4*>(part + s0 * E + (size_t)u * 4);
+            }
             *reinterpret_cast<f32x4*>(dK + (size_t)u * 4) = acc;
         } else {
             float acc = 0.f;
-            for (int s = 0; s < splits; ++s) acc += part[(size_t)s * E + u];
+            for (int g = 0; g < groups; ++g) {
+                const size_t s0 = (size_t)((int64_t)g * splits / groups);
+                acc += part[s0 * E + u];
+            }
             dK[u] = acc;
         }
     }
@@ -520,15 +691,33 @@ hipError_t launch_fold(const Shape& s, const float* dL, float* dI, hipStream_t s
     return hipGetLastError();
 }
 
+// The slab-reuse kernel serves k_h = 1, 3 and 5 when R is a multiple of 4,
+// at least 48, and the staged rows fit its 8 LDS rows per pair; measured on
+// the benchmark layers it beats the plain tiles where rows are short (R <= 256)
+// or the kernel is 5 tall, and loses on long rows with few output tiles. The
+// choice depends on the shape only, so the workspace query and the launch agree.
+bool wgrad_slab_ok(const Shape& s) {
+    return (s.k_h == 1 || s.k_h == 3 || s.k_h == 5) && s.R % 4 == 0 && s.R >= 48 &&
+           (kWgHT - 1) * s.s_h + s.k_h <= kWsRows && (s.R <= 256 || s.k_h >= 5);
+}
+
 int64_t wgrad_splits(const Shape& s) {
-    // enough workgroups to fill the chip about four times over, at most one
-    // per stage, and partial sums within 256 MiB
-    const int64_t tiles = wgrad_tiles(s);
-    int64_t splits = (1024 + tiles - 1) / tiles;
     const int64_t stages = wgrad_stages(s);
-    if (splits > stages) splits = stages;
     const int64_t E = s.k_h * s.R * s.k_c;
-    const int64_t cap = (int64_t(64) << 20) / E;
+    int64_t splits, cap;
+    if (wgrad_slab_ok(s)) {
+        // about two workgroups per compute unit, partial sums within 32 MiB
+        const int64_t tiles = ((s.R + kWs - 1) / kWs) * ((s.k_c + kWs - 1) / kWs);
+        splits = (512 + tiles - 1) / tiles;
+        cap = (int64_t(8) << 20) / E;
+    } else {
+        // enough workgroups to fill the chip about four times over, partial
+        // sums within 256 MiB
+        const int64_t tiles = wgrad_tiles(s);
+        splits = (1024 + tiles - 1) / tiles;
+        cap = (int64_t(64) << 20) / E;
+    }
+    if (splits > stages) splits = stages;  // at most one share per stage
     if (splits > cap) splits = cap;
     return splits < 1 ? 1 : splits;
 }
@@ -561,26 +750,55 @@ hipError_t launch_wgrad(const Shape& s, const float* L, const float* G, float* p
     p.h_chunks = (int32_t)((s.o_h + kWgHT - 1) / kWgHT);
     p.nstages = (int32_t)wgrad_stages(s);
     p.splits = (int32_t)wgrad_splits(s);
-    p.j_tiles = (int32_t)((p.KD + kWgJT - 1) / kWgJT);
-    p.m_tiles = (int32_t)((s.k_c + kWgMT - 1) / kWgMT);
-    p.ntiles = (uint32_t)((int64_t)p.j_tiles * p.m_tiles * p.splits);
     p.lvec = s.R % 4 == 0 && aligned16(L);
     p.gvec = s.k_c % 4 == 0 && aligned16(G);
     p.div_ow = FastDiv((uint32_t)s.o_w);
-    hipLaunchKernelGGL(wgrad_kernel, dim3(p.ntiles), dim3(kGradThreads), 0, stream, p);
+    if (wgrad_slab_ok(s)) {
+        p.j_tiles = (int32_t)((s.R + kWs - 1) / kWs);
+        p.m_tiles = (int32_t)((s.k_c + kWs - 1) / kWs);
+        p.ntiles = (uint32_t)((int64_t)p.j_tiles * p.m_tiles * p.splits);
+        const bool vec = p.lvec && p.gvec;
+#define MEC_WGS(KH)                                                                            \
+    if (s.k_h == KH) {                                                                         \
+        auto kern = vec ? wgrad_slab_kernel<KH, true> : wgrad_slab_kernel<KH, false>;          \
+        hipLaunchKernelGGL(kern, dim3(p.ntiles), dim3(kGradThreads), 0, stream, p);            \
+    }
+        MEC_WGS(1) MEC_WGS(3) MEC_WGS(5)
+#undef MEC_WGS
+    } else {
+        p.j_tiles = (int32_t)((p.KD + kWgJT - 1) / kWgJT);
+        p.m_tiles = (int32_t)((s.k_c + kWgMT - 1) / kWgMT);
+        p.ntiles = (uint32_t)((int64_t)p.j_tiles * p.m_tiles * p.splits);
+        hipLaunchKernelGGL(wgrad_kernel, dim3(p.ntiles), dim3(kGradThreads), 0, stream, p);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int64_t E = (int64_t)p.KD * s.k_c;
     const bool vec = E % 4 == 0 && aligned16(part) && aligned16(dK);
     const uint32_t units = (uint32_t)(vec ? E / 4 : E);
-    int64_t blocks = ((int64_t)units + kGradThreads - 1) / kGradThreads;
+    const uint32_t ublocks = (units + kGradThreads - 1) / kGradThreads;
+    // groups of about 8 consecutive shares, at most 64 groups; with 8 shares
+    // or fewer every share is its own group and pass 1 is skipped
+    int32_t groups = p.splits <= 8 ? p.splits : (p.splits + 7) / 8;
+    if (groups > 64) groups = 64;
+    if (groups < p.splits) {
+        if (vec)
+            hipLaunchKernelGGL(wgrad_reduce_groups_kernel<4>, dim3(ublocks, groups), dim3(kGradThreads),
+                               0, stream, part, units, (uint32_t)E, p.splits, groups);
+        else
+            hipLaunchKernelGGL(wgrad_reduce_groups_kernel<1>, dim3(ublocks, groups), dim3(kGradThreads),
+                               0, stream, part, units, (uint32_t)E, p.splits, groups);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    int64_t blocks = ublocks;
     if (blocks > 65536) blocks = 65536;
     if (vec)
         hipLaunchKernelGGL(wgrad_reduce_kernel<4>, dim3((uint32_t)blocks), dim3(kGradThreads), 0,
-                           stream, part, dK, units, (uint32_t)E, p.splits);
+                           stream, part, dK, units, (uint32_t)E, p.splits, groups);
     else
         hipLaunchKernelGGL(wgrad_reduce_kernel<1>, dim3((uint32_t)blocks), dim3(kGradThreads), 0,
-                           stream, part, dK, units, (uint32_t)E, p.splits);
+                           stream, part, dK, units, (uint32_t)E, p.splits, groups);
     return hipGetLastError();
 }
 

@@ -31,6 +31,11 @@ SHAPES = [
     (35, 5, 5, 2, 2, 2, 3, 1, 1),       # pairs over several 32-pair tiles
     (8, 16, 16, 64, 3, 3, 130, 1, 1),   # dK tiles ragged in both directions
     (4, 21, 19, 16, 7, 7, 40, 2, 2),    # 7x7 stride 2
+    (3, 12, 11, 16, 3, 3, 70, 1, 1),    # slab wgrad, ragged channel tiles
+    (2, 15, 15, 16, 5, 5, 8, 1, 2),     # slab wgrad, 5x5
+    (3, 9, 9, 64, 1, 1, 40, 1, 1),      # slab wgrad, 1x1
+    (2, 13, 13, 64, 3, 3, 64, 3, 2),    # stride 3: too many staged rows for the slab wgrad
+    (2, 13, 13, 48, 1, 1, 64, 2, 2),    # slab wgrad, 1x1 stride 2
 ]
 
 
@@ -143,9 +148,9 @@ def test_wgrad_reuses_forward_workspace(orc):
     assert np.array_equal(dK.cpu().numpy(), ref.astype(np.float32))
 
 
-def test_unaligned_training_tensors(orc):
+@pytest.mark.parametrize("d", [(2, 13, 12, 8, 3, 3, 12, 1, 1), (2, 13, 12, 16, 3, 3, 12, 1, 1)])
+def test_unaligned_training_tensors(orc, d):
     """Tensors 4 bytes past a 16-byte boundary take the element-wise loads."""
-    d = (2, 13, 12, 8, 3, 3, 12, 1, 1)
     say("unaligned training", d)
     I, K, G = problem(5, d, "int")
     i_h, i_w, k_h, k_w = d[1], d[2], d[4], d[5]
