@@ -170,7 +170,11 @@ int mec_conv2d(const void* I, const void* K, float* O,
  * MEC_ERR_UNSUPPORTED); all tensors are fp32, 4-byte aligned.
  * ------------------------------------------------------------------------ */
 
-/* MEC_GRAD_INPUT: mec_conv2d_dgrad -- dL in fp32, |L| * 4 bytes exactly.
+/* MEC_GRAD_INPUT: mec_conv2d_dgrad -- for s_h = s_w = 1, k_h, k_w <= 3 and
+ *   i_c >= 32, the
+ *   zero-padded G' (i_n x (o_h + 2(k_h-1)) x (o_w + 2(k_w-1)) x k_c floats,
+ *   rounded up to 256 bytes) and the turned kernel K' (k_h*k_w*k_c*i_c
+ *   floats); otherwise dL in fp32, |L| * 4 bytes exactly.
  * MEC_GRAD_KERNEL: mec_conv2d_wgrad -- L (|L| * 4 bytes, rounded up to 256)
  *   followed by the partial sums of dK.
  * MEC_GRAD_KERNEL_FROM_L: mec_wgrad_gemm -- the partial sums of dK only:
@@ -201,10 +205,16 @@ int mec_dgrad_gemm(const float* G, const float* K, float* dL,
                    int k_h, int k_w, int k_c, int s_h, int s_w,
                    int dtype, void* stream);
 
-/* dI = dloss/dI: mec_dgrad_gemm into `workspace` (which then holds dL),
- * then mec_fold into dI. workspace_bytes must be at least
- * mec_grad_workspace_bytes(..., MEC_GRAD_INPUT). dI must not overlap G, K or
- * the workspace. Returns MEC_OK or a negative status. */
+/* dI = dloss/dI. With s_h = s_w = 1, k_h, k_w <= 3 and i_c >= 32 (where this is
+ * the faster path) the input gradient is itself
+ * a convolution: G zero-padded by k_h - 1 rows and k_w - 1 columns on every
+ * side (G'), correlated with the kernel turned by 180 degrees and transposed,
+ * K'[a, b, m, c] = K[k_h-1-a, k_w-1-b, c, m]; the library forms G' and K' in
+ * the workspace and runs MEC's fused slab products on them. Otherwise:
+ * mec_dgrad_gemm into `workspace` (which then holds dL), then mec_fold into
+ * dI. workspace_bytes must be at least mec_grad_workspace_bytes(...,
+ * MEC_GRAD_INPUT). dI must not overlap G, K or the workspace.
+ * Returns MEC_OK or a negative status. */
 int mec_conv2d_dgrad(const float* G, const void* K, float* dI,
                      void* workspace, size_t workspace_bytes,
                      int i_n, int i_h, int i_w, int i_c,

@@ -224,7 +224,7 @@ int64_t mec_grad_workspace_bytes(int i_n, int i_h, int i_w, int i_c, int k_h, in
     int rc = grad_shape(s, i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w, dtype);
     if (rc != MEC_OK) return rc;
     switch (pass) {
-        case MEC_GRAD_INPUT: return lowered_elems(s) * 4;
+        case MEC_GRAD_INPUT: return mec::dgrad_workspace_bytes(s);
         case MEC_GRAD_KERNEL: return wgrad_l_region(s) + mec::wgrad_partial_bytes(s);
         case MEC_GRAD_KERNEL_FROM_L: return mec::wgrad_partial_bytes(s);
         default: return MEC_ERR_INVALID_ARG;
@@ -262,13 +262,17 @@ int mec_conv2d_dgrad(const float* G, const void* K, float* dI, void* workspace,
     if (rc != MEC_OK) return rc;
     if (!G || !K || !dI) return MEC_ERR_INVALID_ARG;
     if (!aligned(G, 4) || !aligned(K, 4) || !aligned(dI, 4)) return MEC_ERR_ALIGNMENT;
-    if (!workspace || (uint64_t)workspace_bytes < (uint64_t)(lowered_elems(s) * 4))
+    if (!workspace || (uint64_t)workspace_bytes < (uint64_t)mec::dgrad_workspace_bytes(s))
         return MEC_ERR_WORKSPACE;
     if (!aligned(workspace, 4)) return MEC_ERR_ALIGNMENT;
-    if (!mec::dgrad_supported(s)) return MEC_ERR_UNSUPPORTED;
     const hipStream_t st = (hipStream_t)stream;
-    float* dL = static_cast<float*>(workspace);
     clear_stale_error();
+    if (mec::dgrad_transposed_ok(s))
+        return hip_status(mec::launch_dgrad_transposed(s, G, static_cast<const float*>(K), dI,
+                                                       workspace, st),
+                          "dgrad as a convolution of the padded gradient");
+    if (!mec::dgrad_supported(s)) return MEC_ERR_UNSUPPORTED;
+    float* dL = static_cast<float*>(workspace);
     rc = hip_status(mec::launch_dgrad_dl(s, G, static_cast<const float*>(K), dL, st),
                     "dgrad products");
     if (rc != MEC_OK) return rc;

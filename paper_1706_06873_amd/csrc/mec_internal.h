@@ -103,6 +103,13 @@ hipError_t launch_gemm_fixed(const Shape& s, const void* A, const void* K, float
 bool dgrad_supported(const Shape& s);
 hipError_t launch_dgrad_dl(const Shape& s, const float* G, const float* K, float* dL,
                            hipStream_t stream);
+// dI for stride 1 as a forward convolution of the zero-padded G with the
+// kernel turned by 180 degrees and transposed (fused slab products); G' and K'
+// go to the workspace (dgrad_workspace_bytes).
+bool dgrad_transposed_ok(const Shape& s);
+int64_t dgrad_workspace_bytes(const Shape& s);
+hipError_t launch_dgrad_transposed(const Shape& s, const float* G, const float* K, float* dI,
+                                   void* workspace, hipStream_t stream);
 // dI from dL: the adjoint of the lowering.
 hipError_t launch_fold(const Shape& s, const float* dL, float* dI, hipStream_t stream);
 // dK from L and G: partial sums over shares of the reduction into `part`

@@ -10,10 +10,11 @@
 ``resnet101`` runs the five layers of Table 3 (cv4, cv9-cv12) and ends with a
 summary line weighing each layer by its count in ResNet-101, as Table 3 does:
 weighted workspace (MiB) and weighted time of MEC against im2col. ``train``
-times the training passes (fp32) per layer: the input gradient (dL by the
-slab products against K, then the fold) and the kernel gradient (lowering,
-then the partial A_h^T G_h sums and their reduction), each kernel between
-HIP events; with ``--yardstick`` it also times torch's own convolution
+times the training passes (fp32) per layer, each call between HIP events:
+``conv2d_dgrad`` and ``conv2d_wgrad`` whole, and their parts -- the dL
+products against K and the fold (the input gradient's general path; stride-1
+layers with i_c >= 32 take a convolution of the padded gradient instead), the
+lowering and the partial A_h^T G_h sums with their reduction; with ``--yardstick`` it also times torch's own convolution
 gradients (the vendor library) on the same shapes in NCHW, for context.
 For every layer it times MEC from L (compact lowering + slab products), MEC
 fused, and the im2col baseline (im2col lowering + one product through the
@@ -118,8 +119,16 @@ def _time_train(layer, reps, warmup, yardstick):
     L = torch.empty_like(dL)
     part = torch.empty(mec.grad_workspace_bytes(*layer.dims, grad_pass=mec.GRAD_KERNEL_FROM_L),
                        dtype=torch.uint8, device=dev)
+    ws_i = torch.empty(mec.grad_workspace_bytes(*layer.dims, grad_pass=mec.GRAD_INPUT),
+                       dtype=torch.uint8, device=dev)
+    ws_k = torch.empty(mec.grad_workspace_bytes(*layer.dims, grad_pass=mec.GRAD_KERNEL),
+                       dtype=torch.uint8, device=dev)
     stream = torch.cuda.Stream(device=dev)
     steps = {
+        "conv2d_dgrad": lambda: mec.conv2d_dgrad(G, K, i_h, i_w, s_h, s_w, dI=dI, workspace=ws_i,
+                                                 stream=stream),
+        "conv2d_wgrad": lambda: mec.conv2d_wgrad(I, G, k_h, k_w, s_h, s_w, dK=dK, workspace=ws_k,
+                                                 stream=stream),
         "dgrad_products": lambda: mec.dgrad_gemm(G, K, i_h, i_w, s_h, s_w, dL=dL, stream=stream),
         "fold": lambda: mec.fold(dL, i_w, s_w, dI=dI, stream=stream),
         "lower": lambda: mec.lower(I, k_h, k_w, k_c, s_h, s_w, L=L, stream=stream),
@@ -150,8 +159,9 @@ def _time_train(layer, reps, warmup, yardstick):
     tf = lambda us: round(2.0 * macs / (us * 1e-6) / 1e12, 2)
     out = {"layer": layer.name, "dims": list(layer.dims), "gflop": round(2.0 * macs / 1e9, 3),
            "us": times,
-           "dgrad_us": round(times["dgrad_products"] + times["fold"], 2),
-           "wgrad_us": round(times["lower"] + times["wgrad_products"], 2)}
+           "dgrad_us": times["conv2d_dgrad"], "wgrad_us": times["conv2d_wgrad"],
+           "dgrad_tflops": tf(times["conv2d_dgrad"]), "wgrad_tflops": tf(times["conv2d_wgrad"]),
+           "dgrad_workspace": ws_i.numel(), "wgrad_workspace": ws_k.numel()}
     out["dgrad_products_tflops"] = tf(times["dgrad_products"])
     out["wgrad_products_tflops"] = tf(times["wgrad_products"])
     out["dgrad_products_frac_fp32_mfma"] = round(out["dgrad_products_tflops"] / 157.3, 3)

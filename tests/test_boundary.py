@@ -266,8 +266,15 @@ def test_grad_workspace_sizes(orc, shape):
     if i_n * i_h * i_w * i_c >= 2 ** 31:
         assert mec.lib.mec_grad_workspace_bytes(*shape, 0, 0) == -5
         return
-    # dI: dL in fp32, exactly |L| * 4
-    assert mec.grad_workspace_bytes(*shape, grad_pass=mec.GRAD_INPUT) == nL * 4
+    # dI: dL in fp32, exactly |L| * 4; or, for stride 1, k <= 3 and i_c >= 32, the padded
+    # G (rounded up to 256 bytes) and the turned kernel
+    wi = mec.grad_workspace_bytes(*shape, grad_pass=mec.GRAD_INPUT)
+    o_h, o_w = orc.out_dim(i_h, k_h, s_h), orc.out_dim(i_w, k_w, s_w)
+    gp = (i_n * (o_h + 2 * (k_h - 1)) * (o_w + 2 * (k_w - 1)) * k_c * 4 + 255) // 256 * 256
+    if s_h == s_w == 1 and i_c >= 32 and k_h <= 3 and k_w <= 3:
+        assert wi == gp + k_h * k_w * i_c * k_c * 4
+    else:
+        assert wi == nL * 4
     # dK: whole partial-sum buffers of k_h*k_w*i_c*k_c floats, 1..1024 of them
     part = mec.grad_workspace_bytes(*shape, grad_pass=mec.GRAD_KERNEL_FROM_L)
     E = k_h * k_w * i_c * k_c * 4

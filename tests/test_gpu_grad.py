@@ -36,6 +36,9 @@ SHAPES = [
     (3, 9, 9, 64, 1, 1, 40, 1, 1),      # slab wgrad, 1x1
     (2, 13, 13, 64, 3, 3, 64, 3, 2),    # stride 3: too many staged rows for the slab wgrad
     (2, 13, 13, 48, 1, 1, 64, 2, 2),    # slab wgrad, 1x1 stride 2
+    (3, 10, 11, 64, 3, 3, 32, 1, 1),    # dI as a convolution of the padded G (i_c >= 32)
+    (2, 12, 12, 40, 3, 2, 24, 1, 1),    # the same, 3x2, ragged channels
+    (2, 9, 9, 32, 1, 1, 8, 1, 1),       # the same, 1x1
 ]
 
 
@@ -76,14 +79,20 @@ def test_dgrad(orc, d, dist):
     dI = mec.conv2d_dgrad(Gd, Kd, i_h, i_w, s_h, s_w, workspace=ws)
     torch.cuda.synchronize()
     dL, dI = dL.cpu().numpy(), dI.cpu().numpy()
-    ws_dL = ws.cpu().numpy().view(np.float32).reshape(ref_dL.shape)
+    wsf = ws.cpu().numpy().view(np.float32)
+    if wsf.size == ref_dL.size:
+        # the dL path: the workspace holds dL
+        assert np.array_equal(wsf.reshape(ref_dL.shape), dL)
+    else:
+        # stride 1: the workspace starts with G zero-padded by k - 1 on every side
+        k_h, k_w = d[4], d[5]
+        Gp = np.pad(G.numpy(), ((0, 0), (k_h - 1, k_h - 1), (k_w - 1, k_w - 1), (0, 0)))
+        assert np.array_equal(wsf[:Gp.size].reshape(Gp.shape), Gp)
     if dist == "int":
         assert np.array_equal(dL, ref_dL.astype(np.float32))
-        assert np.array_equal(ws_dL, ref_dL.astype(np.float32))
         assert np.array_equal(dI, ref_dI.astype(np.float32))
     else:
         assert rel_l2(dL, ref_dL) <= TOL
-        assert np.array_equal(ws_dL, dL)
         assert rel_l2(dI, ref_dI) <= TOL
 
 
