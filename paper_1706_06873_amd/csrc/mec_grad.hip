@@ -22,10 +22,17 @@
 //  fold      dI[n, h, x, c] = sum over w with 0 <= x - s_w*w < k_w of
 //            dL[n, w, h, x - s_w*w, c], in increasing w: a gather, one thread
 //            per element (or per 4 channels), bound by HBM bandwidth.
+//  dI, stride 1  for kernels up to 3x3 the input gradient is itself a
+//            convolution: G zero-padded by k - 1 on every side, correlated with
+//            K turned by 180 degrees and transposed; pad_grad and flip_kernel
+//            form the two operands and the forward's fused slab products run.
 //  wgrad     a share of the reduction over (pair, output row) on fp32 MFMA: a
 //            workgroup computes a 128 x 64 tile of dK (rows j = a*R + b*i_c + c,
 //            columns m) over the stages in its share, a stage being 16 pairs x
-//            4 output rows, and writes the tile to its own partial buffer.
+//            4 output rows, and writes the tile to its own partial buffer;
+//            wgrad_slab, for short rows, takes all k_h kernel rows of 64
+//            columns at once and feeds each staged L row to every (h, a) that
+//            reads it.
 //  reduce    dK = the partial buffers summed in a fixed order (groups of
 //            consecutive shares, then the groups), so the result does not
 //            depend on scheduling.

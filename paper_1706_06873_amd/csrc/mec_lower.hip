@@ -14,11 +14,12 @@
 //         scattered through L (stride i_h*R); streaming them past the caches
 //         is what lets the write stream run near copy speed.
 //  strip  Short or unaligned runs (e.g. R = 33 fp32 for 11x11x3 kernels). A
-//         workgroup reads Hb consecutive input rows of one image (again one
-//         contiguous span of I) and, for every w, writes the chunk
-//         L[n, w, h0:h0+Hb, :] -- contiguous in L, Hb*R elements -- with
-//         aligned 16-byte non-temporal stores and element stores at the
-//         chunk's unaligned head and tail.
+//         workgroup reads Hb (+ a few) consecutive input rows of one image
+//         (again one contiguous span of I) and, for every w, writes the chunk
+//         L[n, w, h0:h0+Hb, :] -- contiguous in L, Hb*R elements. It owns the
+//         16-byte granules of L that start in its chunk, so every store inside
+//         a column is one whole non-temporal 16-byte vector; only granules
+//         that straddle two columns are written element by element.
 //  gather Fallback when an input row does not fit in LDS: each thread
 //         gathers 16 bytes of L straight from I.
 //
