@@ -53,17 +53,26 @@ def parse():
     return ap.parse_args()
 
 
+def _code_only(text):
+    """C/C++/HIP source with comments and whitespace removed (string literals
+    kept): edits to comments do not change the kernels."""
+    import re
+    pattern = re.compile(r'//[^\n]*|/\*.*?\*/|"(?:\\.|[^"\\])*"', re.S)
+    text = pattern.sub(lambda m: m.group(0) if m.group(0).startswith('"') else " ", text)
+    return "".join(text.split())
+
+
 def csrc_digest():
-    """sha256 over the native sources; a traffic figure taken from another
-    version of the kernels is not reported."""
+    """sha256 over the native sources without their comments; a traffic figure
+    taken from another version of the kernels is not reported."""
     import hashlib
     d = os.path.join(REPO, "paper_1706_06873_amd", "csrc")
     h = hashlib.sha256()
     for name in sorted(os.listdir(d)):
         if name.endswith((".hip", ".h", ".cpp")):
             h.update(name.encode())
-            with open(os.path.join(d, name), "rb") as f:
-                h.update(f.read())
+            with open(os.path.join(d, name), encoding="utf-8") as f:
+                h.update(_code_only(f.read()).encode())
     return h.hexdigest()
 
 
