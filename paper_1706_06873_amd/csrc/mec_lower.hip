@@ -72,7 +72,8 @@ __global__ __launch_bounds__(kRowsThreads) void lower_rows_kernel(RowsParams p) 
     const uint32_t blk = xcd_remap(blockIdx.x, p.nrows_in);  // input row n*i_h + h
     const uint32_t n = p.div_ih.div(blk), h = blk - n * p.i_h;
     const u32x4* __restrict__ I = reinterpret_cast<const u32x4*>(p.I) + (size_t)blk * p.rowv;
-    for (uint32_t i = threadIdx.x; i < p.rowv; i += kRowsThreads) row[i] = I[i];
+    // I is read once: streamed past the caches like the stores of L
+    for (uint32_t i = threadIdx.x; i < p.rowv; i += kRowsThreads) row[i] = __builtin_nontemporal_load(I + i);
     __syncthreads();
     u32x4* __restrict__ L = reinterpret_cast<u32x4*>(p.L);
     const uint32_t total = p.o_w * p.RV;
