@@ -405,6 +405,42 @@ def test_layer_full_size_sampled(orc, name):
     assert np.isfinite(g1).all()
 
 
+def test_lowered_tensor_beyond_2_31_elements(orc):
+    """A layer whose L has more than 2^31 elements (9.7 GB in fp32): the
+    lowering and the products index it with 64-bit offsets. The first and the
+    last image's L (the last starts past element 2^31) are compared with the
+    oracle's lowering bit for bit; O on sampled outputs of every image, and
+    LOWERED == FUSED there."""
+    dims = (12, 1024, 1026, 64, 3, 3, 16, 1, 1)
+    i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w = dims
+    assert orc.lowered_elems(*dims) > 2 ** 31
+    say("beyond 2^31", dims)
+    g = torch.Generator(device=DEV).manual_seed(12)
+    Id = torch.randint(-3, 4, (i_n, i_h, i_w, i_c), generator=g, device=DEV).float()
+    Kd = torch.randint(-3, 4, (k_h, k_w, i_c, k_c), generator=g, device=DEV).float()
+    ws = torch.empty(mec.workspace_bytes(*dims), dtype=torch.uint8, device=DEV)
+    O1 = mec.conv2d(Id, Kd, s_h, s_w, algo="lowered", workspace=ws)
+    O2 = mec.conv2d(Id, Kd, s_h, s_w, algo="fused")
+    torch.cuda.synchronize()
+    o_w = orc.out_dim(i_w, k_w, s_w)
+    L = ws.view(torch.float32).view(i_n, o_w, i_h, k_w, i_c)
+    I = Id.cpu().numpy()
+    K = Kd.cpu().numpy()
+    for n in (0, i_n - 1):
+        ref_L = orc.mec_lower(np.ascontiguousarray(I[n:n + 1]), k_h, k_w, k_c, s_h, s_w)
+        assert np.array_equal(L[n:n + 1].cpu().numpy(), ref_L), n
+        del ref_L
+    shape = tuple(O1.shape)
+    rng = np.random.default_rng(5)
+    idx = np.stack([rng.integers(0, d, 2000) for d in shape], axis=1)
+    idx[:12, 0] = np.arange(12)
+    ref = orc.conv2d_points(I, K, s_h, s_w, idx)
+    sel = tuple(torch.from_numpy(idx.T.copy()).to(DEV))
+    got1, got2 = O1[sel].cpu().numpy(), O2[sel].cpu().numpy()
+    assert np.array_equal(got1, ref.astype(np.float32))
+    assert np.array_equal(got1, got2)
+
+
 # ---------------------------------------------------------------- Table 2 and the stride sweep
 
 @pytest.mark.parametrize("name", list(wl.TABLE2))
