@@ -767,6 +767,39 @@ int pick_rows(const Shape& s, int nt, std::initializer_list<int> rows) {
     return best;
 }
 
+// fp32 3x3 stride 1, rows per tile (14, 4 or 2, the Wide, Wide4 and Wide2
+// configurations) by a cost model measured on this GPU: a tile's time is
+// nchunks x (t1 + (c - 1) * 1.31 * mfma) when c tiles share a compute unit,
+// with t1 = per-chunk overhead + MFMA cycles of one wave per chunk (overheads
+// 4600, 2300 and 1500 cycles; MFMA 1536 cycles per output row of a wave), and
+// at most w = 1, 3, 4 tiles resident per compute unit (LDS). Tiles beyond w
+// per compute unit run in further rounds. On ResNet/VGG layers of Table 2 it
+// picks the fastest of the three in every case measured (e.g. cv10 2 rows,
+// 21% faster than 4; cv9 4 rows, 13% faster than 14; resnet_mid 14).
+int pick_rows_f32_3x3(const Shape& s) {
+    struct Opt { int ht, w; double ovh; };
+    const Opt opts[3] = {{14, 1, 4600.0}, {4, 3, 2300.0}, {2, 4, 1500.0}};
+    const int64_t nchunks = (s.R + 15) / 16;
+    int best = 14;
+    double best_t = 0.0;
+    for (const Opt& o : opts) {
+        const int64_t tiles = ((s.pairs + kPairs - 1) / kPairs) * ((s.o_h + o.ht - 1) / o.ht) *
+                              ((s.k_c + 63) / 64);
+        const double mfma = 1536.0 * (o.ht / 2);
+        const int64_t per_cu = (tiles + 255) / 256;
+        double t = 0.0;
+        for (int64_t done = 0; done < per_cu; done += o.w) {
+            const int64_t c = per_cu - done < o.w ? per_cu - done : o.w;
+            t += (double)nchunks * (o.ovh + mfma + (double)(c - 1) * 1.31 * mfma);
+        }
+        if (best_t == 0.0 || t < best_t) {
+            best = o.ht;
+            best_t = t;
+        }
+    }
+    return best;
+}
+
 template <bool F>
 hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O, int dtype,
                           hipStream_t stream, bool dry_run) {
@@ -776,7 +809,7 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
     }
     if (dtype == 0) {
         if (s.R >= 32) {
-            const int ht = s.k_h == 3 && s.s_h == 1 ? pick_rows(s, 64, {14, 4, 2}) : 14;
+            const int ht = s.k_h == 3 && s.s_h == 1 ? pick_rows_f32_3x3(s) : 14;
             if (ht == 2) MEC_TRY_FIXED(F32K3S1Wide2<F>);
             if (ht == 4) MEC_TRY_FIXED(F32K3S1Wide4<F>);
             MEC_TRY_FIXED(F32K3S1Wide<F>);

@@ -68,7 +68,7 @@ SWEEP = [
     (33, 4, 4, 4, 2, 2, 33, 1, 1),       # pairs = 99
     (1, 5, 200, 64, 3, 3, 8, 1, 1),      # input rows wider than the lowering's LDS stage
     (2, 6, 130, 33, 3, 2, 5, 1, 3),      # wide odd rows
-    (16, 28, 28, 128, 3, 3, 128, 1, 1),  # 3x3 tiles of 4 output rows (many channel tiles)
+    (16, 28, 28, 128, 3, 3, 128, 1, 1),  # 3x3 tiles of 2 output rows (many channel tiles)
     (2, 21, 19, 16, 7, 7, 40, 2, 2),     # 7x7 s2, 16-byte rows, ragged channels
     (1, 23, 25, 3, 7, 7, 70, 2, 3),      # 7x7 s2, short rows, k_c not a multiple of 4
     (2, 14, 13, 32, 5, 5, 64, 1, 2),     # 5x5 s1, 16-byte rows
@@ -191,6 +191,21 @@ def test_lower_strip_offsets_and_guards(orc, dims, dtype, offs):
     out = lbuf.cpu()
     assert np.array_equal(host(out[guard + loff:guard + loff + nL]).reshape(ref.shape), ref)
     assert bool((out[:guard + loff] == -3.0).all()) and bool((out[guard + loff + nL:] == -3.0).all())
+
+
+# fp32 3x3 stride-1 layers whose tile cost model picks 4-row and 14-row tiles
+# (small layers pick 2-row tiles, e.g. (16, 28, 28, 128, ...) in the sweep).
+@pytest.mark.parametrize("dims", [
+    (8, 66, 66, 16, 3, 3, 192, 1, 1),    # 4 output rows per tile
+    (8, 58, 58, 16, 3, 3, 256, 1, 1),    # 14 output rows per tile
+])
+def test_row_tile_choices_bitwise(orc, dims):
+    say("row tiles", dims)
+    I, K = case(3 * sum(dims), dims, dist="int")
+    s_h, s_w = dims[7], dims[8]
+    ref = orc.conv2d_direct(host(I), host(K), s_h, s_w).astype(np.float32)
+    for algo in ("lowered", "fused"):
+        assert np.array_equal(run_conv(I, K, s_h, s_w, algo), ref), algo
 
 
 def im2col_ref(orc, I, k_h, k_w, s_h, s_w):
