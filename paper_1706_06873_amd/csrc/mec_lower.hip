@@ -17,9 +17,12 @@
 //         workgroup reads Hb (+ a few) consecutive input rows of one image
 //         (again one contiguous span of I) and, for every w, writes the chunk
 //         L[n, w, h0:h0+Hb, :] -- contiguous in L, Hb*R elements. It owns the
-//         16-byte granules of L that start in its chunk, so every store inside
-//         a column is one whole non-temporal 16-byte vector; only granules
-//         that straddle two columns are written element by element.
+//         128-byte lines of L that start in its chunk (16-byte vectors when
+//         chunks are short), so no line inside a column is written in two
+//         parts by two workgroups, and every store there is one whole
+//         non-temporal 16-byte vector; only the units that straddle two
+//         columns are written element by element. (Granule ownership left a
+//         quarter of the lines of 11x11x3 layers split, ~16% slower.)
 //  gather Fallback when an input row does not fit in LDS: each thread
 //         gathers 16 bytes of L straight from I.
 //
@@ -36,6 +39,8 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kRowsThreads = 256;
 constexpr int kStripThreads = 512;
+constexpr int kLineBytes = 128;           // cache line
+constexpr int64_t kStripLineMinChunk = 512;  // bytes of L per chunk for line ownership
 constexpr int kGatherThreads = 256;
 constexpr int kMaxRowsPerBlock = 1024;
 constexpr int64_t kTargetElemsPerBlock = 8192;
@@ -90,25 +95,28 @@ struct StripParams {
     const void* I;
     void* L;
     uint32_t i_h, o_w, rowlen, R, swic, Hb, hblocks, vpw, nblocks;
-    uint32_t extra;      // rows staged beyond the chunk: a granule may reach into them
+    uint32_t extra;      // rows staged beyond the chunk: an owned unit may reach into them
     int32_t in_total;    // elements of I (bound of the staging loads)
-    int32_t ioff, loff;  // elements from the 16-byte boundary below I and below L
+    int32_t ioff;        // elements from the 16-byte boundary below I
+    int32_t loff;        // elements from the unit-of-ownership boundary below L
     FastDiv div_hblocks, div_R, div_vpw;
 };
 
 // Chunk j of column (n, w) is written by workgroup (n, j). Ownership goes by
-// 16-byte granule of L: the workgroup writes every granule whose first
-// address lies in its chunk, L[n, w, h0 : h0+Hb, :], so no granule inside a
-// column is split between workgroups and every store there is one 16-byte
-// vector; only the granules that straddle two columns (or the ends of L) are
-// written element by element, each column's part by its own workgroup. A
-// granule starting near the chunk's end reaches into the next rows, so the
-// workgroup stages `extra` rows past its chunk. The staged rows are one
-// contiguous span of I, loaded as 16-byte granules of I, with element loads
-// for the granules that cross either end of I.
-template <typename E>
+// aligned units of OWN bytes of L (a cache line or a 16-byte vector): the
+// workgroup writes every unit whose first address lies in its chunk,
+// L[n, w, h0 : h0+Hb, :], so no unit inside a column is split between
+// workgroups and every store there is one 16-byte vector; only the units that
+// straddle two columns (or the ends of L) are written element by element,
+// each column's part by its own workgroup. A unit starting near the chunk's
+// end reaches into the next rows, so the workgroup stages `extra` rows past
+// its chunk. The staged rows are one contiguous span of I, loaded as 16-byte
+// granules of I, with element loads for the granules that cross either end
+// of I.
+template <typename E, int OWN>
 __global__ __launch_bounds__(kStripThreads) void lower_strip_kernel(StripParams p) {
     constexpr int VEC = Vec16<E>::N;
+    constexpr int LINE = OWN / sizeof(E);  // elements per unit of ownership
     extern __shared__ u32x4 strip4[];
     E* rows = reinterpret_cast<E*>(strip4);
     const uint32_t blk = xcd_remap(blockIdx.x, p.nblocks);
@@ -143,13 +151,14 @@ __global__ __launch_bounds__(kStripThreads) void lower_strip_kernel(StripParams 
         const uint32_t w = p.div_vpw.div(f);
         const uint32_t v = f - w * p.vpw;
         const int64_t base = ((int64_t)n * p.o_w + w) * col_len;  // column start in L
-        // granules of L start at k*VEC - loff; the first one of chunk 0 may
-        // start before the column
-        const int64_t from = base + (int64_t)h0 * p.R + (j == 0 ? 0 : VEC - 1);
-        const int64_t lo = ((from + p.loff) & ~(int64_t)(VEC - 1)) - p.loff;
-        const int64_t hi = base + (int64_t)hend * p.R;  // granule starts below hi
+        // units of L start at k*LINE - loff; the chunk's granules run from its
+        // first unit's start (chunk 0: the unit that starts before the column)
+        // to the end of the last unit that starts below hi
+        const int64_t from = base + (int64_t)h0 * p.R + (j == 0 ? 0 : LINE - 1);
+        const int64_t lo = ((from + p.loff) & ~(int64_t)(LINE - 1)) - p.loff;
+        const int64_t hi = base + (int64_t)hend * p.R;
         const int64_t gv = lo + (int64_t)v * VEC;
-        if (gv >= hi) continue;
+        if (((gv + p.loff) & ~(int64_t)(LINE - 1)) - p.loff >= hi) continue;
         const int e0 = (int)(gv - base);  // column index of the granule's first element
         const uint32_t ee = e0 < 0 ? 0u : (uint32_t)e0;
         const uint32_t r = p.div_R.div(ee);
@@ -247,25 +256,38 @@ hipError_t launch_rows(const Shape& s, const void* I, void* L, hipStream_t strea
     return hipGetLastError();
 }
 
-// Rows staged past a chunk so that every granule starting in it is covered.
-inline int64_t strip_extra(int64_t R, int VEC) { return (VEC - 2) / R + 1; }
+// Rows staged past a chunk so that every unit of `own` bytes starting in it
+// is covered.
+inline int64_t strip_extra(int64_t R, int64_t elem_bytes, int64_t own) {
+    return (own / elem_bytes - 2) / R + 1;
+}
 
-template <typename E>
-hipError_t launch_strip(const Shape& s, const void* I, void* L, hipStream_t stream) {
-    constexpr int VEC = Vec16<E>::N;
-    const int64_t es = sizeof(E);
+// Rows per chunk for an ownership unit of `own` bytes: chunks of about 1 KB of
+// L, enough workgroups to fill the chip (about 512, two per compute unit), and
+// the chunk plus its extra rows within the LDS limit; 0 if not even one row
+// fits.
+inline int64_t strip_rows(const Shape& s, int64_t es, int64_t own) {
     const int64_t row_bytes = s.i_w * s.i_c * es;
-    const int64_t extra = strip_extra(s.R, VEC);
-    // Hb rows per workgroup: chunks of about 1 KB of L, enough workgroups to
-    // fill the chip (about 512, two per compute unit), and Hb + extra rows
-    // within the LDS limit (the caller checked that Hb = 1 fits).
+    const int64_t extra = strip_extra(s.R, es, own);
+    const int64_t fit = (kStripLdsLimit - 2 * 16) / row_bytes - extra;
+    if (fit < 1) return 0;
     int64_t hb = (1024 + s.R * es - 1) / (s.R * es);
     const int64_t by_count = (s.i_n * s.i_h) / 512;
     if (hb > by_count) hb = by_count;
-    const int64_t fit = (kStripLdsLimit - 2 * 16) / row_bytes - extra;
     if (hb > fit) hb = fit;
     if (hb > s.i_h) hb = s.i_h;
     if (hb < 1) hb = 1;
+    return hb;
+}
+
+// OWN: bytes of L a workgroup owns as a unit (a 16-byte vector or a 128-byte
+// line).
+template <typename E, int OWN>
+hipError_t launch_strip(const Shape& s, int64_t hb, const void* I, void* L, hipStream_t stream) {
+    constexpr int VEC = Vec16<E>::N;
+    const int64_t es = sizeof(E);
+    const int64_t row_bytes = s.i_w * s.i_c * es;
+    const int64_t extra = strip_extra(s.R, es, OWN);
     StripParams p{};
     p.I = I;
     p.L = L;
@@ -278,9 +300,10 @@ hipError_t launch_strip(const Shape& s, const void* I, void* L, hipStream_t stre
     p.extra = (uint32_t)extra;
     p.in_total = (int32_t)(s.i_n * s.i_h * s.i_w * s.i_c);
     p.ioff = (int32_t)(((uintptr_t)I / es) % VEC);
-    p.loff = (int32_t)(((uintptr_t)L / es) % VEC);
+    p.loff = (int32_t)(((uintptr_t)L / es) % (OWN / es));
     p.hblocks = (uint32_t)((s.i_h + hb - 1) / hb);
-    p.vpw = (uint32_t)((hb * s.R + VEC - 1) / VEC + 2);
+    // granules from the first owned unit's start to the last one's end
+    p.vpw = (uint32_t)((hb * s.R + 2 * (OWN / es) + VEC - 1) / VEC);
     p.nblocks = (uint32_t)(s.i_n * p.hblocks);
     p.div_hblocks = FastDiv(p.hblocks);
     p.div_R = FastDiv(p.R);
@@ -288,7 +311,8 @@ hipError_t launch_strip(const Shape& s, const void* I, void* L, hipStream_t stre
     // staged rows plus up to one granule on each side of the span
     const int64_t staged = std::min<int64_t>(hb + extra, s.i_h);
     const size_t lds = (size_t)(staged * row_bytes + 2 * 16);
-    hipLaunchKernelGGL(lower_strip_kernel<E>, dim3(p.nblocks), dim3(kStripThreads), lds, stream, p);
+    hipLaunchKernelGGL((lower_strip_kernel<E, OWN>), dim3(p.nblocks), dim3(kStripThreads), lds, stream,
+                       p);
     return hipGetLastError();
 }
 
@@ -335,9 +359,18 @@ hipError_t launch_typed(const Shape& s, const void* I, void* L, hipStream_t stre
     // strip: 32-bit offsets into I and within a workgroup's o_w chunks, and at
     // least one chunk row plus its extra rows in LDS
     const bool strip_ok = small && s.i_n * s.i_h * s.i_w * s.i_c < (int64_t(1) << 31) &&
-                          s.o_w * (s.i_h * s.R / VEC + 3) < (int64_t(1) << 31) &&
-                          (1 + strip_extra(s.R, VEC)) * row_bytes + 2 * 16 <= kStripLdsLimit;
-    if (strip_ok) return launch_strip<E>(s, I, L, stream);
+                          s.o_w * (s.i_h * s.R / VEC + 18) < (int64_t(1) << 31);
+    if (strip_ok) {
+        // whole cache lines per workgroup when the chunks are long enough that
+        // the lines' extra rows and idle lanes cost less than lines written in
+        // two parts by two workgroups; 16-byte vectors otherwise
+        const int64_t es = sizeof(E);
+        const int64_t hb_line = strip_rows(s, es, kLineBytes);
+        if (hb_line > 0 && hb_line * s.R * es >= kStripLineMinChunk)
+            return launch_strip<E, kLineBytes>(s, hb_line, I, L, stream);
+        const int64_t hb_vec = strip_rows(s, es, 16);
+        if (hb_vec > 0) return launch_strip<E, 16>(s, hb_vec, I, L, stream);
+    }
     return launch_gather<E>(s, I, L, stream);
 }
 

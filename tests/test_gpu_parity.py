@@ -157,7 +157,8 @@ def test_lower_bitwise_sweep(orc, dims, dtype):
 
 # Short or unaligned runs take the strip lowering. Enough images x rows that a
 # workgroup owns chunks of several rows (the chunk height grows with
-# i_n * i_h), with I and L placed off their 16-byte boundaries.
+# i_n * i_h), with I and L placed off their 16-byte boundaries and at several
+# offsets from a 128-byte line (the unit a workgroup owns in L).
 STRIP_CASES = [
     (8, 150, 20, 3, 5, 5, 4, 1, 1),       # R = 15
     (16, 200, 21, 3, 11, 11, 4, 4, 4),    # R = 33, the 11x11 stride-4 layout
@@ -169,10 +170,10 @@ STRIP_CASES = [
 
 @pytest.mark.parametrize("dims", STRIP_CASES)
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("offs", [(0, 0), (1, 3), (3, 1), (2, 5)])
+@pytest.mark.parametrize("offs", [(0, 0), (1, 3), (3, 1), (2, 5), (1, 21)])
 def test_lower_strip_offsets_and_guards(orc, dims, dtype, offs):
     """L bit for bit, and nothing written outside it, for I and L starting
-    ioff and loff elements past a 16-byte boundary."""
+    ioff and loff (+ 24 guard) elements past a 256-byte boundary."""
     ioff, loff = offs
     say("lower strip", dtype, dims, offs)
     I, _ = case(31 * sum(dims) + ioff, dims, dtype=dtype)
