@@ -30,6 +30,7 @@ struct FixedParams {
     int32_t nchunks, h_tiles, n_tiles;
     uint32_t ntiles;
     int32_t o_vec;      // k_c % 4 == 0 and O 16-byte aligned: O rows stored 16 bytes per lane
+    FastDiv div_ow;     // pair -> image (streaming kernel; pairs < 2^31)
 };
 
 // ---------------------------------------------------------------- fp32 kernel
@@ -361,6 +362,250 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_kernel(FixedParams p
                 if (ob >= 0) __builtin_nontemporal_store(acc[hw][nb][v], p.O + ob + h * ostride_h + c);
             }
         }
+    }
+}
+
+// ---------------------------------------------------------------- fp32 streaming kernel
+// For layers whose whole reduction fits one stage (R <= KT: the 3x3x3 first
+// layers, 27 multiply-adds and 256 bytes of O per output pixel), whose time
+// goes to writing O. Run tile by tile, as above, such a layer proceeds in
+// lock-step rounds: every workgroup of a round stages and multiplies while HBM
+// idles, then all of them write their O tiles at once while the matrix cores
+// idle. Here a persistent workgroup walks the tiles b, b + G, b + 2G, ... and
+// issues the next tile's operand loads before the current tile's O stores.
+// Vector memory operations complete in issue order, so the loads it waits for
+// next are never queued behind its own stores, and those stores drain while
+// the next tile is multiplied. The O epilogue goes through a per-wave LDS
+// region of its own (no barrier), one 32x32 block at a time.
+template <class C>
+__global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_stream_kernel(FixedParams p) {
+    constexpr int KT = C::kKT, NT = C::NT, HW = C::HW, NBW = C::NBW, VA = C::kVA, VB = C::kVB;
+    constexpr int KH = C::kKH, SH = C::kSH, XW = C::XW, RG = C::RG, NG = C::NG;
+    constexpr int A_SIZE = C::A_SIZE, STAGE = C::STAGE, AJ = C::AJ, BJ = C::BJ;
+    // epilogue: a wave's NBW blocks of one output row side by side, rows LD
+    // floats apart, so a store instruction covers whole 32*NBW-channel row
+    // segments of consecutive pairs
+    constexpr int LD = 32 * NBW + 8;
+    constexpr int Q = 8 * NBW;     // 16-byte pieces per row segment
+    constexpr int RPI = 64 / Q;    // rows per store instruction
+    static_assert(64 % Q == 0, "row segments per store instruction");
+    __shared__ __align__(16) uint32_t lds[STAGE + C::kWaves * 32 * LD];
+    // per tile, for the three in flight (stores, stage, loads): each pair's
+    // source offset from the tile's first pair (-1: no such pair) and O offset
+    __shared__ int32_t src_s[3][kPairs];
+    __shared__ int64_t dst_s[3][kPairs];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wh = wave % (C::kWaves / C::WAVES_N), wn = wave / (C::kWaves / C::WAVES_N);
+    const int row = lane & 31;
+    const int kofs = lane >> 5;
+    const int a_lane = (wh * HW * SH) * KT * kPairs + kofs * kPairs + row;
+    const int b_lane = A_SIZE + kofs * NT + (wn * NBW) * 32 + row;
+    float* blk = reinterpret_cast<float*>(lds + STAGE) + wave * (32 * LD);
+    const int64_t ostride_h = p.o_w * p.k_c;
+
+    struct Tile {
+        int64_t pair0, h0, abase0;  // abase0: source element of the first pair
+        int n0;
+    };
+    // source element of a pair's slab (L row base, or I pixel for the fused form)
+    auto pair_base = [&](int64_t pair) -> int64_t {
+        if (!C::kFused) return pair * p.i_h * p.R;
+        const int64_t n = p.div_ow.div((uint32_t)pair), w = pair - n * p.o_w;
+        return ((n * p.i_h) * p.i_w + p.s_w * w) * p.i_c;
+    };
+    // tile i of the grid-stride walk; the host makes the grid a multiple of 8,
+    // so a workgroup's tiles stay on its XCD's share of xcd_remap
+    auto coords = [&](uint32_t i) {
+        const uint32_t t = xcd_remap(i, p.ntiles);
+        Tile c;
+        const uint32_t rest = t / (uint32_t)p.n_tiles;
+        c.n0 = (int)(t - rest * (uint32_t)p.n_tiles) * NT;
+        c.h0 = (int64_t)(rest % (uint32_t)p.h_tiles) * C::kHT;
+        c.pair0 = (int64_t)(rest / (uint32_t)p.h_tiles) * kPairs;
+        c.abase0 = pair_base(c.pair0);
+        return c;
+    };
+    auto write_offsets = [&](const Tile& c, int b) {
+        if (tid < kPairs) {
+            const int64_t pair = c.pair0 + tid;
+            if (pair < p.pairs) {
+                const int64_t n = p.div_ow.div((uint32_t)pair), w = pair - n * p.o_w;
+                src_s[b][tid] = (int32_t)(pair_base(pair) - c.abase0);
+                dst_s[b][tid] = (n * p.o_h * p.o_w + w) * p.k_c;
+            } else {
+                src_s[b][tid] = -1;
+                dst_s[b][tid] = -1;
+            }
+        }
+    };
+
+    VecN<VA, uint32_t> areg[AJ][4];
+    VecN<4, uint32_t> breg[BJ];
+    // global -> registers for a whole tile (one r-chunk), every entry predicated
+    auto load = [&](const Tile& c, int b) {
+        const uint32_t* __restrict__ Atile = reinterpret_cast<const uint32_t*>(p.A) + c.abase0;
+        const int32_t x0 = (int32_t)(c.h0 * SH);
+#pragma unroll
+        for (int j = 0; j < AJ; ++j) {
+            const int it = tid + j * C::THREADS;
+            const int pg = it % 8, t2 = it / 8;
+            const int rg = t2 % RG, x = t2 / RG;
+            const bool ok = it < C::A_ITEMS && rg * VA < p.R && x0 + x < p.i_h;
+            const uint32_t rofs = (uint32_t)((x0 + x) * (int32_t)p.a_xstride + rg * VA);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                areg[j][q].zero();
+                const int32_t sb = ok ? src_s[b][4 * pg + q] : -1;
+                if (sb >= 0) areg[j][q].load(Atile + ((uint32_t)sb + rofs));
+            }
+        }
+        const uint32_t* __restrict__ Kg = reinterpret_cast<const uint32_t*>(p.K);
+#pragma unroll
+        for (int j = 0; j < BJ; ++j) {
+            const int it = tid + j * C::THREADS;
+            const int ng = it % NG, t2 = it / NG;
+            const int r = t2 % KT, a = t2 / KT;
+            const int c0 = c.n0 + 4 * ng;
+            breg[j].zero();
+            if (it < C::B_ITEMS && r < p.R && c0 < p.k_c) {
+                const uint32_t off = (uint32_t)((a * (int32_t)p.R + r) * (int32_t)p.k_c + c0);
+                if (VB == 4) {
+                    breg[j].load(Kg + off);
+                } else {
+#pragma unroll
+                    for (int k = 0; k < 4; ++k)
+                        if (c0 + k < p.k_c) breg[j].e[k] = Kg[off + k];
+                }
+            }
+        }
+    };
+    auto store_stage = [&]() {
+#pragma unroll
+        for (int j = 0; j < AJ; ++j) {
+            const int it = tid + j * C::THREADS;
+            if (it < C::A_ITEMS) {
+                const int pg = it % 8, t2 = it / 8;
+                const int rg = t2 % RG, x = t2 / RG;
+                const int al = (x * KT + rg * VA) * kPairs + 4 * pg;
+#pragma unroll
+                for (int k = 0; k < VA; ++k)
+                    *reinterpret_cast<uint4*>(lds + al + k * kPairs) =
+                        make_uint4(areg[j][0].e[k], areg[j][1].e[k], areg[j][2].e[k], areg[j][3].e[k]);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < BJ; ++j) {
+            const int it = tid + j * C::THREADS;
+            if (it < C::B_ITEMS) {
+                const int ng = it % NG, t2 = it / NG;
+                const int r = t2 % KT, a = t2 / KT;
+                *reinterpret_cast<uint4*>(lds + A_SIZE + (a * KT + r) * NT + 4 * ng) =
+                    make_uint4(breg[j].e[0], breg[j].e[1], breg[j].e[2], breg[j].e[3]);
+            }
+        }
+    };
+
+    // Tile t is multiplied from the stage while tile t+1's operands are in
+    // registers (loaded one tile earlier) and tile t-1's O stores drain; then
+    // tile t+1 is staged, tile t+2's loads are issued, and only then tile t's
+    // stores. Waiting for a tile's operands thus waits for the stores issued
+    // before them one tile earlier, which had a whole tile of products to drain.
+    const uint64_t G = gridDim.x;
+    uint64_t i = blockIdx.x;
+    int b = 0;  // offsets buffer of tile t; t+1 uses b+1, t+2 b+2 (mod 3)
+    Tile cur = coords((uint32_t)i);
+    bool more1 = i + G < p.ntiles;
+    Tile nxt = more1 ? coords((uint32_t)(i + G)) : cur;
+    write_offsets(cur, 0);
+    if (more1) write_offsets(nxt, 1);
+    __syncthreads();
+    load(cur, 0);
+    store_stage();
+    if (more1) load(nxt, 1);
+    __syncthreads();
+    for (;;) {
+        floatx16 acc[HW][NBW];
+        // one k-step of the products; the first starts every accumulator from
+        // an MFMA with a zero addend (no zeroed registers kept around)
+        auto kstep = [&](int kk, auto first_tag) {
+            constexpr bool FIRST = decltype(first_tag)::value;
+            float af[XW];
+            float bf[KH][NBW];
+#pragma unroll
+            for (int x = 0; x < XW; ++x) af[x] = __builtin_bit_cast(float, lds[a_lane + (x * KT + kk) * kPairs]);
+#pragma unroll
+            for (int a = 0; a < KH; ++a)
+#pragma unroll
+                for (int nb = 0; nb < NBW; ++nb)
+                    bf[a][nb] = __builtin_bit_cast(float, lds[b_lane + (a * KT + kk) * NT + nb * 32]);
+#pragma unroll
+            for (int a = 0; a < KH; ++a)
+#pragma unroll
+                for (int h = 0; h < HW; ++h)
+#pragma unroll
+                    for (int nb = 0; nb < NBW; ++nb)
+                        acc[h][nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(
+                            af[h * SH + a], bf[a][nb], (FIRST && a == 0) ? floatx16{} : acc[h][nb], 0, 0, 0);
+        };
+        kstep(0, std::true_type{});
+#pragma unroll 1
+        for (int kk = 2; kk < KT; kk += 2) kstep(kk, std::false_type{});
+
+        const bool more2 = more1 && i + 2 * G < p.ntiles;
+        Tile nn = nxt;
+        const int b1 = b == 2 ? 0 : b + 1, b2 = b1 == 2 ? 0 : b1 + 1;
+        if (more2) {
+            nn = coords((uint32_t)(i + 2 * G));
+            write_offsets(nn, b2);
+        }
+        __syncthreads();  // the stage is free; tile t+2's offsets visible
+        if (more1) store_stage();  // tile t+1
+        if (more2) load(nn, b2);
+
+        if (p.o_vec) {
+            // each lane stores 16 contiguous bytes: rows rr, rr + RPI, ... of
+            // the wave's blocks, channels cc .. cc + 3 of the row segment
+            const int rr = lane / Q, cc = (lane % Q) * 4;
+            const int c = cur.n0 + wn * NBW * 32 + cc;
+#pragma unroll
+            for (int h = 0; h < HW; ++h) {
+                const int64_t oh = cur.h0 + wh * HW + h;
+#pragma unroll
+                for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) blk[acc_row(v, lane) * LD + nb * 32 + row] = acc[h][nb][v];
+#pragma unroll
+                for (int k = 0; k < 32 / RPI; ++k) {
+                    const float4 val = *reinterpret_cast<const float4*>(blk + (rr + RPI * k) * LD + cc);
+                    const int64_t ob = dst_s[b][rr + RPI * k];
+                    if (oh < p.o_h && c < p.k_c && ob >= 0) store_o4_nt(p.O + ob + oh * ostride_h + c, val);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int h = 0; h < HW; ++h) {
+                const int64_t oh = cur.h0 + wh * HW + h;
+                if (oh >= p.o_h) continue;
+#pragma unroll
+                for (int nb = 0; nb < NBW; ++nb) {
+                    const int c = cur.n0 + (wn * NBW + nb) * 32 + row;
+                    if (c >= p.k_c) continue;
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) {
+                        const int64_t ob = dst_s[b][acc_row(v, lane)];
+                        if (ob >= 0) __builtin_nontemporal_store(acc[h][nb][v], p.O + ob + oh * ostride_h + c);
+                    }
+                }
+            }
+        }
+        if (!more1) break;
+        __syncthreads();  // tile t+1's stage visible
+        i += G;
+        b = b1;
+        cur = nxt;
+        nxt = nn;
+        more1 = more2;
     }
 }
 
@@ -710,6 +955,56 @@ hipError_t run_fixed(const Shape& s, const void* A, const void* K, float* O, hip
     return hipGetLastError();
 }
 
+template <class C>
+bool stream_usable(const Shape& s, const void* A, const void* K) {
+    return usable<C>(s, A, K) && s.R <= C::kKT && s.pairs < (int64_t(1) << 31);
+}
+
+template <class C>
+hipError_t run_stream(const Shape& s, const void* A, const void* K, float* O, hipStream_t stream) {
+    FixedParams p{};
+    p.A = A;
+    p.K = K;
+    p.O = O;
+    p.i_h = s.i_h; p.i_w = s.i_w; p.i_c = s.i_c; p.k_c = s.k_c; p.s_w = s.s_w;
+    p.o_h = s.o_h; p.o_w = s.o_w; p.R = s.R; p.pairs = s.pairs;
+    p.a_xstride = C::kFused ? s.i_w * s.i_c : s.R;
+    p.nchunks = 1;
+    const int64_t pair_tiles = (s.pairs + kPairs - 1) / kPairs;
+    p.h_tiles = (int32_t)((s.o_h + C::kHT - 1) / C::kHT);
+    p.n_tiles = (int32_t)((s.k_c + C::NT - 1) / C::NT);
+    const int64_t ntiles = pair_tiles * p.h_tiles * p.n_tiles;
+    if (ntiles > 0x7fffffff) return hipErrorInvalidValue;
+    p.ntiles = (uint32_t)ntiles;
+    p.o_vec = s.k_c % 4 == 0 && ((uintptr_t)O & 15u) == 0;
+    p.div_ow = FastDiv((uint32_t)s.o_w);
+    // persistent grid: the workgroups every compute unit holds at once (LDS and
+    // registers), a multiple of 8 so each workgroup's tiles stay on its XCD
+    static const int per_cu = [] {
+        int b = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, slab_gemm_f32_stream_kernel<C>,
+                                                         C::THREADS, 0) != hipSuccess || b < 1)
+            b = 1;
+        return b;
+    }();
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+        cus = 1;
+    int64_t grid = (int64_t)per_cu * cus / 8 * 8;
+    if (grid < 8) grid = 8;
+    if (grid > ntiles) grid = ntiles;
+    hipLaunchKernelGGL(slab_gemm_f32_stream_kernel<C>, dim3((uint32_t)grid), dim3(C::THREADS), 0, stream,
+                       p);
+    return hipGetLastError();
+}
+
+// fp32, 3x3 stride 1, rows of at most 10 elements (3x3 kernels over 3 channels):
+// the streaming kernel, 32 pairs x 8 rows x 64 channels, the whole reduction
+// in one stage.
+template <bool F> using F32K3S1Stream = F32Cfg<8, 2, 4, 10, 3, 1, 1, 4, F>;
+template <bool F> using F32K3S1StreamScalar = F32Cfg<8, 2, 4, 10, 3, 1, 1, 1, F>;
+
 // fp32, 3x3 stride 1, long rows (R % 4 == 0): 32 pairs x 14 rows x 64 channels,
 // r-chunks of 16, 16-byte loads of L (or I) and K.
 template <bool F> using F32K3S1Wide = F32Cfg<14, 2, 2, 16, 3, 1, 4, 4, F>;
@@ -807,6 +1102,10 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
     if (usable<CFG>(s, A, K)) {                                             \
         return dry_run ? hipSuccess : run_fixed<CFG>(s, A, K, O, stream);   \
     }
+#define MEC_TRY_STREAM(CFG)                                                 \
+    if (stream_usable<CFG>(s, A, K)) {                                      \
+        return dry_run ? hipSuccess : run_stream<CFG>(s, A, K, O, stream);  \
+    }
     if (dtype == 0) {
         if (s.R >= 32) {
             const int ht = s.k_h == 3 && s.s_h == 1 ? pick_rows_f32_3x3(s) : 14;
@@ -814,6 +1113,8 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
             if (ht == 4) MEC_TRY_FIXED(F32K3S1Wide4<F>);
             MEC_TRY_FIXED(F32K3S1Wide<F>);
         }
+        MEC_TRY_STREAM(F32K3S1Stream<F>);
+        MEC_TRY_STREAM(F32K3S1StreamScalar<F>);
         MEC_TRY_FIXED(F32K3S1Narrow<F>);
         MEC_TRY_FIXED(F32K3S1NarrowScalar<F>);
         MEC_TRY_FIXED(F32K7S2Wide<F>);
@@ -840,6 +1141,7 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
         MEC_TRY_FIXED(BF16K1S1<F>);
     }
 #undef MEC_TRY_FIXED
+#undef MEC_TRY_STREAM
     return hipErrorNotSupported;
 }
 

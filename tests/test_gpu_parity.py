@@ -209,6 +209,48 @@ def test_row_tile_choices_bitwise(orc, dims):
         assert np.array_equal(run_conv(I, K, s_h, s_w, algo), ref), algo
 
 
+# 3x3 layers over 1-3 channels (R <= 10) take the streaming product kernel: a
+# persistent workgroup walks several tiles. Shapes with more tiles than the
+# ~768 resident workgroups, ragged pairs, rows and channel tiles, and k_c not
+# a multiple of 4 (element K loads, element O stores).
+STREAM_CASES = [
+    (16, 130, 130, 3, 3, 3, 64, 1, 1),   # 1024 tiles
+    (20, 100, 61, 3, 3, 3, 100, 1, 1),   # 962 tiles, every dimension ragged
+    (32, 90, 90, 3, 3, 3, 30, 1, 1),     # 968 tiles, k_c = 30
+    (8, 60, 60, 1, 3, 3, 64, 1, 2),      # R = 3, stride 2 along w
+    (6, 41, 47, 2, 3, 3, 36, 1, 1),      # R = 6
+]
+
+
+@pytest.mark.parametrize("dims", STREAM_CASES)
+def test_stream_products(orc, dims):
+    say("stream", dims)
+    s_h, s_w = dims[7], dims[8]
+    I, K = case(11 + sum(dims), dims)
+    ref = orc.conv2d_direct(host(I), host(K), s_h, s_w)
+    Ii, Ki = case(13 + sum(dims), dims, dist="int")
+    refi = orc.conv2d_direct(host(Ii), host(Ki), s_h, s_w)
+    assert np.abs(refi).max() < 2 ** 24
+    for algo in ("lowered", "fused"):
+        assert rel_l2(run_conv(I, K, s_h, s_w, algo), ref) <= TOL_F32, algo
+        assert np.array_equal(run_conv(Ii, Ki, s_h, s_w, algo), refi.astype(np.float32)), algo
+
+
+def test_stream_output_not_written_outside(orc):
+    dims = (20, 100, 61, 3, 3, 3, 100, 1, 1)
+    say("stream guard", dims)
+    I, K = case(17, dims)
+    ref = orc.conv2d_direct(host(I), host(K), 1, 1).astype(np.float32)
+    buf = torch.full((ref.size + 4096,), 7.0, dtype=torch.float32, device=DEV)
+    O = buf[1024:1024 + ref.size].view(ref.shape)
+    for algo in ("lowered", "fused"):
+        mec.conv2d(to_dev(I), to_dev(K), 1, 1, algo=algo, O=O)
+        torch.cuda.synchronize()
+        b = buf.cpu().numpy()
+        assert np.all(b[:1024] == 7.0) and np.all(b[1024 + ref.size:] == 7.0)
+        assert rel_l2(O.cpu().numpy(), ref) <= TOL_F32
+
+
 def im2col_ref(orc, I, k_h, k_w, s_h, s_w):
     """The oracle's im2col (rows n, y, x) reordered to the library's (n, x, y)."""
     i_n, i_h, i_w, i_c = I.shape
