@@ -12,7 +12,10 @@
 // r-chunk's global loads are issued during the current one (fp32: spread over
 // its first k-steps; bf16, two k-steps per chunk: before the first), and their
 // LDS stores go to the other of two stage buffers. O is written
-// n-h-w-c with non-temporal stores.
+// n-h-w-c with non-temporal stores. Layers whose whole reduction fits one stage
+// and whose time goes to writing O (3x3 over 1-3 channels) use a persistent
+// streaming variant that overlaps each tile's O stores with the next tile's
+// products.
 #include <initializer_list>
 #include <type_traits>
 

@@ -236,6 +236,31 @@ def test_stream_products(orc, dims):
         assert np.array_equal(run_conv(Ii, Ki, s_h, s_w, algo), refi.astype(np.float32)), algo
 
 
+@pytest.mark.parametrize("shift", [1, 3])
+def test_stream_unaligned(orc, shift):
+    """The streaming kernel with I, K, L and O off their 16-byte boundaries:
+    element K loads and element O stores."""
+    dims = (6, 41, 47, 3, 3, 3, 36, 1, 1)
+    say("stream unaligned", shift, dims)
+    I, K = case(23, dims, dist="int")
+    ref = orc.conv2d_direct(host(I), host(K), 1, 1).astype(np.float32)
+
+    def offset_copy(t):
+        buf = torch.zeros(t.numel() + 8, dtype=t.dtype, device=DEV)
+        v = buf[shift:shift + t.numel()].view(t.shape)
+        v.copy_(t.to(DEV))
+        return v
+
+    Id, Kd = offset_copy(I), offset_copy(K)
+    Od = torch.zeros(ref.size + 8, dtype=torch.float32, device=DEV)[shift:shift + ref.size].view(ref.shape)
+    ws = torch.zeros(mec.workspace_bytes(*dims) + 64, dtype=torch.uint8, device=DEV)[4 * shift:]
+    for algo in ("lowered", "fused"):
+        Od.zero_()
+        mec.conv2d(Id, Kd, 1, 1, algo=algo, O=Od, workspace=ws)
+        torch.cuda.synchronize()
+        assert np.array_equal(Od.cpu().numpy(), ref), algo
+
+
 def test_stream_output_not_written_outside(orc):
     dims = (20, 100, 61, 3, 3, 3, 100, 1, 1)
     say("stream guard", dims)
