@@ -31,7 +31,9 @@ struct FixedParams {
     int64_t i_h, i_w, i_c, k_c, s_w, o_h, o_w, R, pairs;
     int64_t a_xstride;  // elements between consecutive rows x of one pair's source
     int32_t nchunks, h_tiles, n_tiles;
-    uint32_t ntiles;
+    uint32_t ntiles;    // workgroups: tiles x ksplit
+    int32_t ksplit;     // fp32 kernel: 1, or 2 = each tile's r-chunks split between two
+                        // workgroups that add their partial sums into a zeroed O
     int32_t o_vec;      // k_c % 4 == 0 and O 16-byte aligned: O rows stored 16 bytes per lane
     FastDiv div_ow;     // pair -> image (streaming kernel; pairs < 2^31)
 };
@@ -96,7 +98,11 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_kernel(FixedParams p
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wh = wave % (C::kWaves / C::WAVES_N), wn = wave / (C::kWaves / C::WAVES_N);
 
-    const uint32_t t = xcd_remap(blockIdx.x, p.ntiles);
+    // the two halves of a split tile are neighbours, so they land on one XCD
+    const uint32_t tw = xcd_remap(blockIdx.x, p.ntiles);
+    const uint32_t t = tw / (uint32_t)p.ksplit, part = tw - t * (uint32_t)p.ksplit;
+    const int c_begin = (int)(part * (uint32_t)p.nchunks / (uint32_t)p.ksplit);
+    const int c_end = (int)((part + 1) * (uint32_t)p.nchunks / (uint32_t)p.ksplit);
     const int n_tile = (int)(t % (uint32_t)p.n_tiles);
     const uint32_t rest = t / (uint32_t)p.n_tiles;
     const int h_tile = (int)(rest % (uint32_t)p.h_tiles);
@@ -290,18 +296,19 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_kernel(FixedParams p
         }
     };
 
+    // r-chunks [c_begin, c_end): all of them, or this workgroup's half
     auto main_loop = [&](auto full_tag) {
-        load_stage(0, full_tag);
+        load_stage(c_begin, full_tag);
         store_stage(0);
         __syncthreads();
-        for (int rc = 0; rc < p.nchunks; ++rc) {
-            const bool more = rc + 1 < p.nchunks;
-            compute(rc & 1, [&](int pc0, int pc1) {
+        for (int rc = c_begin; rc < c_end; ++rc) {
+            const bool more = rc + 1 < c_end;
+            compute((rc - c_begin) & 1, [&](int pc0, int pc1) {
                 if (more)
 #pragma unroll
                     for (int pc = pc0; pc < pc1; ++pc) load_piece(rc + 1, full_tag, pc);
             });
-            if (more) store_stage((rc + 1) & 1);
+            if (more) store_stage((rc + 1 - c_begin) & 1);
             __syncthreads();
         }
     };
@@ -311,6 +318,9 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_kernel(FixedParams p
         main_loop(std::false_type{});
 
     const int64_t ostride_h = p.o_w * p.k_c;
+    // split tiles: exactly two partial sums added to +0 in either order give
+    // the same value, so O stays deterministic
+    const bool add = p.ksplit > 1;
     if (p.o_vec) {
         // Through LDS (free since the loop's last barrier): accumulator blocks
         // are written row-major, rows EPI_LD floats apart, then read back as
@@ -342,8 +352,17 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_kernel(FixedParams p
                     if (rr < RPI && r < 32) {
                         const float4 val = *reinterpret_cast<const float4*>(blk + r * LD + cc);
                         const int64_t ob = obase_s[r];
-                        if (h < p.o_h && c < p.k_c && ob >= 0)
-                            store_o4_nt(p.O + ob + h * ostride_h + c, val);
+                        if (h < p.o_h && c < p.k_c && ob >= 0) {
+                            float* dst = p.O + ob + h * ostride_h + c;
+                            if (add) {
+                                unsafeAtomicAdd(dst, val.x);
+                                unsafeAtomicAdd(dst + 1, val.y);
+                                unsafeAtomicAdd(dst + 2, val.z);
+                                unsafeAtomicAdd(dst + 3, val.w);
+                            } else {
+                                store_o4_nt(dst, val);
+                            }
+                        }
                     }
                 }
                 __syncthreads();
@@ -362,10 +381,23 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_kernel(FixedParams p
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 const int64_t ob = obase_s[acc_row(v, lane)];
-                if (ob >= 0) __builtin_nontemporal_store(acc[hw][nb][v], p.O + ob + h * ostride_h + c);
+                if (ob < 0) continue;
+                if (add)
+                    unsafeAtomicAdd(p.O + ob + h * ostride_h + c, acc[hw][nb][v]);
+                else
+                    __builtin_nontemporal_store(acc[hw][nb][v], p.O + ob + h * ostride_h + c);
             }
         }
     }
+}
+
+// O = 0 before the two halves of split tiles add into it (a kernel rather than
+// a memset so that the call stays safe to capture in a graph)
+__global__ __launch_bounds__(256) void zero_o_kernel(float* __restrict__ O, int64_t n) {
+    const int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+        if (i + k < n) __builtin_nontemporal_store(0.f, O + i + k);
 }
 
 // ---------------------------------------------------------------- fp32 streaming kernel
@@ -938,7 +970,8 @@ struct KernelOf<F32Cfg<HT, NB, WH, KT, KH, SH, VA, VB, F, W>> {
 };
 
 template <class C>
-hipError_t run_fixed(const Shape& s, const void* A, const void* K, float* O, hipStream_t stream) {
+hipError_t run_fixed(const Shape& s, const void* A, const void* K, float* O, hipStream_t stream,
+                     int ksplit = 1) {
     FixedParams p{};
     p.A = A;
     p.K = K;
@@ -950,10 +983,15 @@ hipError_t run_fixed(const Shape& s, const void* A, const void* K, float* O, hip
     const int64_t pair_tiles = (s.pairs + kPairs - 1) / kPairs;
     p.h_tiles = (int32_t)((s.o_h + C::kHT - 1) / C::kHT);
     p.n_tiles = (int32_t)((s.k_c + C::NT - 1) / C::NT);
-    const int64_t ntiles = pair_tiles * p.h_tiles * p.n_tiles;
+    const int64_t ntiles = pair_tiles * p.h_tiles * p.n_tiles * ksplit;
     if (ntiles > 0x7fffffff) return hipErrorInvalidValue;
     p.ntiles = (uint32_t)ntiles;
+    p.ksplit = ksplit;
     p.o_vec = s.k_c % 4 == 0 && ((uintptr_t)O & 15u) == 0;
+    if (ksplit > 1) {
+        const int64_t n = s.i_n * s.o_h * s.o_w * s.k_c;
+        hipLaunchKernelGGL(zero_o_kernel, dim3((uint32_t)((n + 1023) / 1024)), dim3(256), 0, stream, O, n);
+    }
     hipLaunchKernelGGL(KernelOf<C>::fn, dim3(p.ntiles), dim3(KernelOf<C>::threads), 0, stream, p);
     return hipGetLastError();
 }
@@ -1065,34 +1103,54 @@ int pick_rows(const Shape& s, int nt, std::initializer_list<int> rows) {
     return best;
 }
 
-// fp32 3x3 stride 1, rows per tile (14, 4 or 2, the Wide, Wide4 and Wide2
-// configurations) by a cost model measured on this GPU: a tile's time is
+// fp32 3x3 stride 1: rows per tile (14, 4 or 2, the Wide, Wide4 and Wide2
+// configurations) and whether to split each tile's r-chunks between two
+// workgroups, by a cost model measured on this GPU: a tile's time is
 // nchunks x (t1 + (c - 1) * 1.31 * mfma) when c tiles share a compute unit,
 // with t1 = per-chunk overhead + MFMA cycles of one wave per chunk (overheads
 // 4600, 2300 and 1500 cycles; MFMA 1536 cycles per output row of a wave), and
 // at most w = 1, 3, 4 tiles resident per compute unit (LDS). Tiles beyond w
-// per compute unit run in further rounds. On ResNet/VGG layers of Table 2 it
-// picks the fastest of the three in every case measured (e.g. cv10 2 rows,
-// 21% faster than 4; cv9 4 rows, 13% faster than 14; resnet_mid 14).
-int pick_rows_f32_3x3(const Shape& s) {
+// per compute unit run in further rounds. A split tile is two workgroups of
+// half the r-chunks each, plus zeroing O and adding both halves into it
+// (costed as a 4 us launch and three passes over O at 5 TB/s). On ResNet/VGG layers of Table 2
+// the unsplit choice is the fastest of the three row counts in every case
+// measured (e.g. cv10 2 rows, 21% faster than 4; cv9 4 rows, 13% faster than
+// 14; resnet_mid 14). A split is only considered where it shortens the
+// busiest compute unit's chunk count: layers whose tiles leave compute units
+// idle (cv11 12%, cv12 38% faster; the batch-1 layers).
+struct TileChoice {
+    int ht, ksplit;
+};
+TileChoice pick_tiles_f32_3x3(const Shape& s) {
     struct Opt { int ht, w; double ovh; };
     const Opt opts[3] = {{14, 1, 4600.0}, {4, 3, 2300.0}, {2, 4, 1500.0}};
     const int64_t nchunks = (s.R + 15) / 16;
-    int best = 14;
+    const double o_bytes = 4.0 * (double)(s.i_n * s.o_h * s.o_w * s.k_c);
+    TileChoice best{14, 1};
     double best_t = 0.0;
-    for (const Opt& o : opts) {
-        const int64_t tiles = ((s.pairs + kPairs - 1) / kPairs) * ((s.o_h + o.ht - 1) / o.ht) *
-                              ((s.k_c + 63) / 64);
-        const double mfma = 1536.0 * (o.ht / 2);
-        const int64_t per_cu = (tiles + 255) / 256;
-        double t = 0.0;
-        for (int64_t done = 0; done < per_cu; done += o.w) {
-            const int64_t c = per_cu - done < o.w ? per_cu - done : o.w;
-            t += (double)nchunks * (o.ovh + mfma + (double)(c - 1) * 1.31 * mfma);
-        }
-        if (best_t == 0.0 || t < best_t) {
-            best = o.ht;
-            best_t = t;
+    for (int split = 1; split <= 2; ++split) {
+        if (split == 2 && nchunks < 4) break;
+        const int64_t nch = (nchunks + split - 1) / split;
+        for (const Opt& o : opts) {
+            const int64_t tiles1 = ((s.pairs + kPairs - 1) / kPairs) * ((s.o_h + o.ht - 1) / o.ht) *
+                                   ((s.k_c + 63) / 64);
+            const int64_t tiles = tiles1 * split;
+            const double mfma = 1536.0 * (o.ht / 2);
+            const int64_t per_cu = (tiles + 255) / 256;
+            // split only where it shortens the busiest compute unit's r-chunks;
+            // otherwise it just doubles the tiles sharing each one (measured
+            // slower than the model says: cv6 122 -> 144 us)
+            if (split == 2 && per_cu * nch >= ((tiles1 + 255) / 256) * nchunks) continue;
+            // split: the zeroing launch (~4 us) and three passes over O
+            double t = split == 1 ? 0.0 : 9600.0 + 3.0 * o_bytes / 5.0e12 * 2.4e9;
+            for (int64_t done = 0; done < per_cu; done += o.w) {
+                const int64_t c = per_cu - done < o.w ? per_cu - done : o.w;
+                t += (double)nch * (o.ovh + mfma + (double)(c - 1) * 1.31 * mfma);
+            }
+            if (best_t == 0.0 || t < best_t) {
+                best = {o.ht, split};
+                best_t = t;
+            }
         }
     }
     return best;
@@ -1105,16 +1163,20 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
     if (usable<CFG>(s, A, K)) {                                             \
         return dry_run ? hipSuccess : run_fixed<CFG>(s, A, K, O, stream);   \
     }
+#define MEC_TRY_FIXED_SPLIT(CFG, KSPLIT)                                            \
+    if (usable<CFG>(s, A, K)) {                                                     \
+        return dry_run ? hipSuccess : run_fixed<CFG>(s, A, K, O, stream, KSPLIT);   \
+    }
 #define MEC_TRY_STREAM(CFG)                                                 \
     if (stream_usable<CFG>(s, A, K)) {                                      \
         return dry_run ? hipSuccess : run_stream<CFG>(s, A, K, O, stream);  \
     }
     if (dtype == 0) {
         if (s.R >= 32) {
-            const int ht = s.k_h == 3 && s.s_h == 1 ? pick_rows_f32_3x3(s) : 14;
-            if (ht == 2) MEC_TRY_FIXED(F32K3S1Wide2<F>);
-            if (ht == 4) MEC_TRY_FIXED(F32K3S1Wide4<F>);
-            MEC_TRY_FIXED(F32K3S1Wide<F>);
+            const TileChoice tc = s.k_h == 3 && s.s_h == 1 ? pick_tiles_f32_3x3(s) : TileChoice{14, 1};
+            if (tc.ht == 2) MEC_TRY_FIXED_SPLIT(F32K3S1Wide2<F>, tc.ksplit);
+            if (tc.ht == 4) MEC_TRY_FIXED_SPLIT(F32K3S1Wide4<F>, tc.ksplit);
+            MEC_TRY_FIXED_SPLIT(F32K3S1Wide<F>, tc.ksplit);
         }
         MEC_TRY_STREAM(F32K3S1Stream<F>);
         MEC_TRY_STREAM(F32K3S1StreamScalar<F>);
@@ -1145,6 +1207,7 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
     }
 #undef MEC_TRY_FIXED
 #undef MEC_TRY_STREAM
+#undef MEC_TRY_FIXED_SPLIT
     return hipErrorNotSupported;
 }
 

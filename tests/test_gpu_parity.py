@@ -276,6 +276,48 @@ def test_stream_output_not_written_outside(orc):
         assert rel_l2(O.cpu().numpy(), ref) <= TOL_F32
 
 
+# fp32 3x3 layers with few tiles and long reductions split each tile's r-chunks
+# between two workgroups that add into a zeroed O (cv11/cv12-like shapes).
+SPLIT_CASES = [
+    (4, 14, 14, 256, 3, 3, 256, 1, 1),
+    (2, 7, 7, 512, 3, 3, 512, 1, 1),
+    (3, 16, 15, 64, 3, 3, 100, 1, 1),    # ragged channel tile
+]
+
+
+@pytest.mark.parametrize("dims", SPLIT_CASES)
+@pytest.mark.parametrize("algo", ["lowered", "fused"])
+def test_split_reduction(orc, dims, algo):
+    """Within tolerance on floats, bit for bit on small integers, and the same
+    bits on a second run (two partial sums onto +0 commute exactly)."""
+    say("split", algo, dims)
+    s_h, s_w = dims[7], dims[8]
+    I, K = case(29 + sum(dims), dims)
+    ref = orc.conv2d_direct(host(I), host(K), s_h, s_w)
+    O1 = run_conv(I, K, s_h, s_w, algo)
+    assert rel_l2(O1, ref) <= TOL_F32
+    assert np.array_equal(run_conv(I, K, s_h, s_w, algo), O1)
+    Ii, Ki = case(31 + sum(dims), dims, dist="int")
+    refi = orc.conv2d_direct(host(Ii), host(Ki), s_h, s_w)
+    assert np.array_equal(run_conv(Ii, Ki, s_h, s_w, algo), refi.astype(np.float32))
+
+
+def test_split_reduction_unaligned_o(orc):
+    """O off its 16-byte boundary: element atomics, nothing written outside O."""
+    dims = SPLIT_CASES[0]
+    say("split unaligned", dims)
+    I, K = case(37, dims, dist="int")
+    ref = orc.conv2d_direct(host(I), host(K), 1, 1).astype(np.float32)
+    buf = torch.full((ref.size + 64,), 7.0, dtype=torch.float32, device=DEV)
+    O = buf[33:33 + ref.size].view(ref.shape)
+    for algo in ("lowered", "fused"):
+        mec.conv2d(to_dev(I), to_dev(K), 1, 1, algo=algo, O=O)
+        torch.cuda.synchronize()
+        b = buf.cpu().numpy()
+        assert np.all(b[:33] == 7.0) and np.all(b[33 + ref.size:] == 7.0)
+        assert np.array_equal(O.cpu().numpy(), ref), algo
+
+
 def im2col_ref(orc, I, k_h, k_w, s_h, s_w):
     """The oracle's im2col (rows n, y, x) reordered to the library's (n, x, y)."""
     i_n, i_h, i_w, i_c = I.shape
