@@ -713,7 +713,11 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_bf16_kernel(FixedParams 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wh = wave % (C::kWaves / C::WAVES_N), wn = wave / (C::kWaves / C::WAVES_N);
 
-    const uint32_t t = xcd_remap(blockIdx.x, p.ntiles);
+    // the two halves of a split tile are neighbours, so they land on one XCD
+    const uint32_t tw = xcd_remap(blockIdx.x, p.ntiles);
+    const uint32_t t = tw / (uint32_t)p.ksplit, part = tw - t * (uint32_t)p.ksplit;
+    const int c_begin = (int)(part * (uint32_t)p.nchunks / (uint32_t)p.ksplit);
+    const int c_end = (int)((part + 1) * (uint32_t)p.nchunks / (uint32_t)p.ksplit);
     const int n_tile = (int)(t % (uint32_t)p.n_tiles);
     const uint32_t rest = t / (uint32_t)p.n_tiles;
     const int h_tile = (int)(rest % (uint32_t)p.h_tiles);
@@ -866,16 +870,17 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_bf16_kernel(FixedParams 
         }
     };
 
+    // r-chunks [c_begin, c_end): all of them, or this workgroup's half
     auto main_loop = [&](auto full_tag) {
-        load_stage(0, full_tag);
+        load_stage(c_begin, full_tag);
         store_stage(0);
         __syncthreads();
-        for (int rc = 0; rc < p.nchunks; ++rc) {
-            const bool more = rc + 1 < p.nchunks;
-            compute(rc & 1, [&] {
+        for (int rc = c_begin; rc < c_end; ++rc) {
+            const bool more = rc + 1 < c_end;
+            compute((rc - c_begin) & 1, [&] {
                 if (more) load_stage(rc + 1, full_tag);
             });
-            if (more) store_stage((rc + 1) & 1);
+            if (more) store_stage((rc + 1 - c_begin) & 1);
             __syncthreads();
         }
     };
@@ -885,6 +890,7 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_bf16_kernel(FixedParams 
         main_loop(std::false_type{});
 
     const int64_t ostride_h = p.o_w * p.k_c;
+    const bool add = p.ksplit > 1;  // split tile: add into the zeroed O, as in the fp32 kernel
     if (p.o_vec) {
         // 16-byte O stores through LDS, as in the fp32 kernel
         float* blk = reinterpret_cast<float*>(lds) + wave * (32 * 40);
@@ -903,8 +909,17 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_bf16_kernel(FixedParams 
                     const int r = rr + 8 * i;
                     const float4 val = *reinterpret_cast<const float4*>(blk + r * 40 + cc);
                     const int64_t ob = obase_s[r];
-                    if (h < p.o_h && c < p.k_c && ob >= 0)
-                        store_o4_nt(p.O + ob + h * ostride_h + c, val);
+                    if (h < p.o_h && c < p.k_c && ob >= 0) {
+                        float* dst = p.O + ob + h * ostride_h + c;
+                        if (add) {
+                            unsafeAtomicAdd(dst, val.x);
+                            unsafeAtomicAdd(dst + 1, val.y);
+                            unsafeAtomicAdd(dst + 2, val.z);
+                            unsafeAtomicAdd(dst + 3, val.w);
+                        } else {
+                            store_o4_nt(dst, val);
+                        }
+                    }
                 }
                 __syncthreads();
             }
@@ -922,7 +937,11 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_bf16_kernel(FixedParams 
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 const int64_t ob = obase_s[acc_row(v, lane)];
-                if (ob >= 0) __builtin_nontemporal_store(acc[hw][nb][v], p.O + ob + h * ostride_h + c);
+                if (ob < 0) continue;
+                if (add)
+                    unsafeAtomicAdd(p.O + ob + h * ostride_h + c, acc[hw][nb][v]);
+                else
+                    __builtin_nontemporal_store(acc[hw][nb][v], p.O + ob + h * ostride_h + c);
             }
         }
     }
@@ -1103,6 +1122,17 @@ int pick_rows(const Shape& s, int nt, std::initializer_list<int> rows) {
     return best;
 }
 
+// bf16 3x3 tiles (one workgroup per compute unit): split a tile's r-chunks
+// between two workgroups only where that shortens the busiest compute unit's
+// chunk count and each half keeps at least 4 chunks (the small deep layers,
+// e.g. cv12: 60 tiles of 48 chunks on 256 compute units).
+bool split_shortens(const Shape& s, int ht, int nt, int kt) {
+    const int64_t nchunks = (s.R + kt - 1) / kt;
+    if (nchunks < 8) return false;
+    const int64_t tiles = ((s.pairs + kPairs - 1) / kPairs) * ((s.o_h + ht - 1) / ht) * ((s.k_c + nt - 1) / nt);
+    return ((2 * tiles + 255) / 256) * ((nchunks + 1) / 2) < ((tiles + 255) / 256) * nchunks;
+}
+
 // fp32 3x3 stride 1: rows per tile (14, 4 or 2, the Wide, Wide4 and Wide2
 // configurations) and whether to split each tile's r-chunks between two
 // workgroups, by a cost model measured on this GPU: a tile's time is
@@ -1199,9 +1229,10 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
     } else {
         {
             const int ht = s.k_h == 3 && s.s_h == 1 ? pick_rows(s, 128, {14, 4, 2}) : 14;
-            if (ht == 2) MEC_TRY_FIXED(BF16K3S1R2<F>);
-            if (ht == 4) MEC_TRY_FIXED(BF16K3S1R4<F>);
-            MEC_TRY_FIXED(BF16K3S1<F>);
+            const int ks = split_shortens(s, ht, 128, 32) ? 2 : 1;
+            if (ht == 2) MEC_TRY_FIXED_SPLIT(BF16K3S1R2<F>, ks);
+            if (ht == 4) MEC_TRY_FIXED_SPLIT(BF16K3S1R4<F>, ks);
+            MEC_TRY_FIXED_SPLIT(BF16K3S1<F>, ks);
         }
         MEC_TRY_FIXED(BF16K1S1<F>);
     }

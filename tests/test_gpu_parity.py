@@ -302,6 +302,30 @@ def test_split_reduction(orc, dims, algo):
     assert np.array_equal(run_conv(Ii, Ki, s_h, s_w, algo), refi.astype(np.float32))
 
 
+# bf16 3x3 layers with few tiles split their reduction the same way.
+SPLIT_CASES_BF16 = [
+    (2, 7, 7, 512, 3, 3, 512, 1, 1),     # 12 tiles of 48 r-chunks
+    (3, 9, 8, 256, 3, 3, 136, 1, 1),     # ragged channel tile
+]
+
+
+@pytest.mark.parametrize("dims", SPLIT_CASES_BF16)
+@pytest.mark.parametrize("algo", ["lowered", "fused"])
+def test_split_reduction_bf16(orc, dims, algo):
+    say("split bf16", algo, dims)
+    s_h, s_w = dims[7], dims[8]
+    I32, K32 = case(41 + sum(dims), dims, dtype="f32")
+    I, K = I32.to(torch.bfloat16), K32.to(torch.bfloat16)
+    ref = orc.conv2d_direct(host(I), host(K), s_h, s_w)
+    O1 = run_conv(I, K, s_h, s_w, algo)
+    assert rel_l2(O1, ref) <= TOL_F32
+    assert np.array_equal(run_conv(I, K, s_h, s_w, algo), O1)
+    Ii, Ki = case(43 + sum(dims), dims, dtype="bf16", dist="int")
+    refi = orc.conv2d_direct(host(Ii), host(Ki), s_h, s_w)
+    assert np.abs(refi).max() < 2 ** 24
+    assert np.array_equal(run_conv(Ii, Ki, s_h, s_w, algo), refi.astype(np.float32))
+
+
 def test_split_reduction_unaligned_o(orc):
     """O off its 16-byte boundary: element atomics, nothing written outside O."""
     dims = SPLIT_CASES[0]
