@@ -174,11 +174,14 @@ int mec_conv2d(const void* I, const void* K, float* O,
  * MEC_ERR_UNSUPPORTED); all tensors are fp32, 4-byte aligned.
  * ------------------------------------------------------------------------ */
 
-/* MEC_GRAD_INPUT: mec_conv2d_dgrad -- for s_h = s_w = 1, k_h, k_w <= 3 and
- *   i_c >= 32, the
- *   zero-padded G' (i_n x (o_h + 2(k_h-1)) x (o_w + 2(k_w-1)) x k_c floats,
- *   rounded up to 256 bytes) and the turned kernel K' (k_h*k_w*k_c*i_c
- *   floats); otherwise dL in fp32, |L| * 4 bytes exactly.
+/* MEC_GRAD_INPUT: mec_conv2d_dgrad -- on the sub-pixel phase path (see
+ *   mec_conv2d_dgrad): 12 bytes of alignment slack, the largest phase's
+ *   zero-padded G' (i_n x (Ny + J - 1) x (Nx + I - 1) x k_c floats, rounded
+ *   up to 256 bytes) and the largest phase kernel K' (J*I*k_c*i_c floats),
+ *   where phase (py, px) has J = ceil((k_h - py)/s_h), I = ceil((k_w - px)/s_w),
+ *   Ny = ceil((i_h - py)/s_h), Nx = ceil((i_w - px)/s_w) (stride 1: one phase,
+ *   G' of (o_h + 2(k_h-1)) x (o_w + 2(k_w-1)) pixels); otherwise dL in fp32,
+ *   |L| * 4 bytes exactly.
  * MEC_GRAD_KERNEL: mec_conv2d_wgrad -- L (|L| * 4 bytes, rounded up to 256)
  *   followed by the partial sums of dK.
  * MEC_GRAD_KERNEL_FROM_L: mec_wgrad_gemm -- the partial sums of dK only:
@@ -209,14 +212,22 @@ int mec_dgrad_gemm(const float* G, const float* K, float* dL,
                    int k_h, int k_w, int k_c, int s_h, int s_w,
                    int dtype, void* stream);
 
-/* dI = dloss/dI. With s_h = s_w = 1, k_h, k_w <= 3 and i_c >= 32 (where this is
- * the faster path) the input gradient is itself
- * a convolution: G zero-padded by k_h - 1 rows and k_w - 1 columns on every
- * side (G'), correlated with the kernel turned by 180 degrees and transposed,
- * K'[a, b, m, c] = K[k_h-1-a, k_w-1-b, c, m]; the library forms G' and K' in
- * the workspace and runs MEC's fused slab products on them. Otherwise:
- * mec_dgrad_gemm into `workspace` (which then holds dL), then mec_fold into
- * dI. workspace_bytes must be at least mec_grad_workspace_bytes(...,
+/* dI = dloss/dI. The pixels of one sub-pixel phase (py, px),
+ * dI[n, s_h*Y + py, s_w*X + px, :], receive G only through the kernel taps
+ * a = py + s_h*j, b = px + s_w*i, so each phase is itself a stride-1
+ * convolution: G zero-padded by J - 1 rows above and I - 1 columns to the left
+ * (G'), correlated with K'[j, i, m, c] = K[py + s_h(J-1-j), px + s_w(I-1-i), c, m]
+ * (the taps turned by 180 degrees, input and output channels swapped); at
+ * stride 1 there is one phase, G padded by k - 1 on every side. The library
+ * forms G' and K' in the workspace, one phase after another, and runs MEC's
+ * fused slab products on them, writing straight into the phase's pixels. This
+ * path is taken for i_c >= 32 and, at stride 1, kernels up to 3x3 (where it is
+ * the faster one); at larger strides for s_h <= k_h, s_w <= k_w, k_c and i_c
+ * multiples of 4, phase kernel heights up to 5, at most 4 phases and
+ * k_h*k_w >= 10*s_h*s_w (the phases run one after another; smaller ones lose
+ * to the dL path). Otherwise: mec_dgrad_gemm
+ * into `workspace` (which then holds dL), then mec_fold into dI.
+ * workspace_bytes must be at least mec_grad_workspace_bytes(...,
  * MEC_GRAD_INPUT). dI must not overlap G, K or the workspace.
  * Returns MEC_OK or a negative status. */
 int mec_conv2d_dgrad(const float* G, const void* K, float* dI,

@@ -307,7 +307,8 @@ def dgrad_gemm(G, K, i_h, i_w, s_h=1, s_w=1, dL=None, stream=None):
 
 
 def conv2d_dgrad(G, K, i_h, i_w, s_h=1, s_w=1, dI=None, workspace=None, stream=None):
-    """dI = dloss/dI (I's shape, float32); the workspace then holds dL."""
+    """dI = dloss/dI (I's shape, float32); on the dL path the workspace then
+    holds dL, on the sub-pixel phase path the last phase's padded G and kernel."""
     import torch
     d = _grad_dims(G, K, i_h, i_w, s_h, s_w)
     if dI is None:

@@ -267,10 +267,10 @@ int mec_conv2d_dgrad(const float* G, const void* K, float* dI, void* workspace,
     if (!aligned(workspace, 4)) return MEC_ERR_ALIGNMENT;
     const hipStream_t st = (hipStream_t)stream;
     clear_stale_error();
-    if (mec::dgrad_transposed_ok(s))
-        return hip_status(mec::launch_dgrad_transposed(s, G, static_cast<const float*>(K), dI,
-                                                       workspace, st),
-                          "dgrad as a convolution of the padded gradient");
+    if (mec::dgrad_phases_ok(s))
+        return hip_status(mec::launch_dgrad_phases(s, G, static_cast<const float*>(K), dI,
+                                                   workspace, st),
+                          "dgrad as sub-pixel phases of the padded gradient");
     if (!mec::dgrad_supported(s)) return MEC_ERR_UNSUPPORTED;
     float* dL = static_cast<float*>(workspace);
     rc = hip_status(mec::launch_dgrad_dl(s, G, static_cast<const float*>(K), dL, st),

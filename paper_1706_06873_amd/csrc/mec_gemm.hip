@@ -447,10 +447,11 @@ bool gemm_supported(const Shape& s, int dtype) {
 }
 
 hipError_t launch_gemm(const Shape& s, const void* A, const void* K, float* O, int dtype,
-                       bool fused, hipStream_t stream) {
-    // kernels specialised for this kernel height and stride first
-    const hipError_t e = launch_gemm_fixed(s, A, K, O, dtype, fused, stream, false);
-    if (e != hipErrorNotSupported) return e;
+                       bool fused, hipStream_t stream, const OutLayout* layout) {
+    // kernels specialised for this kernel height and stride first; only they
+    // take a strided output layout
+    const hipError_t e = launch_gemm_fixed(s, A, K, O, dtype, fused, stream, false, layout);
+    if (e != hipErrorNotSupported || layout) return e;
     if (fused) return dispatch<true>(s, A, K, O, dtype, stream, false);
     return dispatch<false>(s, A, K, O, dtype, stream, false);
 }

@@ -36,6 +36,8 @@ struct FixedParams {
                         // workgroups that add their partial sums into a zeroed O
     int32_t o_vec;      // k_c % 4 == 0 and O 16-byte aligned: O rows stored 16 bytes per lane
     FastDiv div_ow;     // pair -> image (streaming kernel; pairs < 2^31)
+    // fp32 kernels: O element (n, h, w, c) at n*o_img + h*o_row + w*o_col + o_off + c
+    int64_t o_img, o_row, o_col, o_off;
 };
 
 // ---------------------------------------------------------------- fp32 kernel
@@ -116,7 +118,7 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_kernel(FixedParams p
         if (pair < p.pairs) {
             const int64_t n = pair / p.o_w, w = pair % p.o_w;
             abase_s[tid] = C::kFused ? ((n * p.i_h) * p.i_w + p.s_w * w) * p.i_c : pair * p.i_h * p.R;
-            obase_s[tid] = (n * p.o_h * p.o_w + w) * p.k_c;
+            obase_s[tid] = n * p.o_img + w * p.o_col + p.o_off;
         } else {
             abase_s[tid] = -1;
             obase_s[tid] = -1;
@@ -317,7 +319,7 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_kernel(FixedParams p
     else
         main_loop(std::false_type{});
 
-    const int64_t ostride_h = p.o_w * p.k_c;
+    const int64_t ostride_h = p.o_row;
     // split tiles: exactly two partial sums added to +0 in either order give
     // the same value, so O stays deterministic
     const bool add = p.ksplit > 1;
@@ -437,7 +439,7 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_stream_kernel(FixedP
     const int a_lane = (wh * HW * SH) * KT * kPairs + kofs * kPairs + row;
     const int b_lane = A_SIZE + kofs * NT + (wn * NBW) * 32 + row;
     float* blk = reinterpret_cast<float*>(lds + STAGE) + wave * (32 * LD);
-    const int64_t ostride_h = p.o_w * p.k_c;
+    const int64_t ostride_h = p.o_row;
 
     struct Tile {
         int64_t pair0, h0, abase0;  // abase0: source element of the first pair
@@ -467,7 +469,7 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_stream_kernel(FixedP
             if (pair < p.pairs) {
                 const int64_t n = p.div_ow.div((uint32_t)pair), w = pair - n * p.o_w;
                 src_s[b][tid] = (int32_t)(pair_base(pair) - c.abase0);
-                dst_s[b][tid] = (n * p.o_h * p.o_w + w) * p.k_c;
+                dst_s[b][tid] = n * p.o_img + w * p.o_col + p.o_off;
             } else {
                 src_s[b][tid] = -1;
                 dst_s[b][tid] = -1;
@@ -988,9 +990,28 @@ struct KernelOf<F32Cfg<HT, NB, WH, KT, KH, SH, VA, VB, F, W>> {
     static constexpr int threads = 64 * W;
 };
 
+// Output layout fields and the 16-byte store test: dense n-h-w-c unless a
+// layout is given (fp32 kernels only).
+inline void set_layout(FixedParams& p, const Shape& s, float* O, const OutLayout* layout) {
+    if (layout) {
+        p.o_img = layout->img;
+        p.o_row = layout->row;
+        p.o_col = layout->col;
+        p.o_off = layout->off;
+    } else {
+        p.o_img = s.o_h * s.o_w * s.k_c;
+        p.o_row = s.o_w * s.k_c;
+        p.o_col = s.k_c;
+        p.o_off = 0;
+    }
+    p.o_vec = s.k_c % 4 == 0 && ((uintptr_t)O & 15u) == 0 &&
+              ((p.o_img | p.o_row | p.o_col | p.o_off) & 3) == 0;
+}
+
 template <class C>
 hipError_t run_fixed(const Shape& s, const void* A, const void* K, float* O, hipStream_t stream,
-                     int ksplit = 1) {
+                     int ksplit = 1, const OutLayout* layout = nullptr) {
+    if (layout) ksplit = 1;  // the zeroing would clear other parts of a strided O
     FixedParams p{};
     p.A = A;
     p.K = K;
@@ -1006,7 +1027,7 @@ hipError_t run_fixed(const Shape& s, const void* A, const void* K, float* O, hip
     if (ntiles > 0x7fffffff) return hipErrorInvalidValue;
     p.ntiles = (uint32_t)ntiles;
     p.ksplit = ksplit;
-    p.o_vec = s.k_c % 4 == 0 && ((uintptr_t)O & 15u) == 0;
+    set_layout(p, s, O, layout);
     if (ksplit > 1) {
         const int64_t n = s.i_n * s.o_h * s.o_w * s.k_c;
         hipLaunchKernelGGL(zero_o_kernel, dim3((uint32_t)((n + 1023) / 1024)), dim3(256), 0, stream, O, n);
@@ -1021,7 +1042,8 @@ bool stream_usable(const Shape& s, const void* A, const void* K) {
 }
 
 template <class C>
-hipError_t run_stream(const Shape& s, const void* A, const void* K, float* O, hipStream_t stream) {
+hipError_t run_stream(const Shape& s, const void* A, const void* K, float* O, hipStream_t stream,
+                      const OutLayout* layout = nullptr) {
     FixedParams p{};
     p.A = A;
     p.K = K;
@@ -1036,7 +1058,7 @@ hipError_t run_stream(const Shape& s, const void* A, const void* K, float* O, hi
     const int64_t ntiles = pair_tiles * p.h_tiles * p.n_tiles;
     if (ntiles > 0x7fffffff) return hipErrorInvalidValue;
     p.ntiles = (uint32_t)ntiles;
-    p.o_vec = s.k_c % 4 == 0 && ((uintptr_t)O & 15u) == 0;
+    set_layout(p, s, O, layout);
     p.div_ow = FastDiv((uint32_t)s.o_w);
     // persistent grid: the workgroups every compute unit holds at once (LDS and
     // registers), a multiple of 8 so each workgroup's tiles stay on its XCD
@@ -1085,6 +1107,11 @@ using F32K11S4 = typename std::conditional<F, F32Cfg<8, 3, 8, 2, 11, 4, 1, VB, t
 template <bool F> using F32K7S2Wide = F32Cfg<8, 2, 2, 8, 7, 2, 4, 4, F>;
 template <bool F> using F32K7S2Narrow = F32Cfg<8, 2, 4, 4, 7, 2, 1, 4, F>;
 template <bool F> using F32K7S2Scalar = F32Cfg<8, 2, 4, 4, 7, 2, 1, 1, F>;
+// fp32, 2x2 and 4x4 (any k_w) stride 1, 16-byte rows: 32 pairs x 8 rows x 64
+// channels (the sub-pixel phases of stride-2 input gradients: 3x3 -> 2x2,
+// 7x7 -> 4x4 and 3x3 kernels).
+template <bool F> using F32K2S1Wide = F32Cfg<8, 2, 2, 16, 2, 1, 4, 4, F>;
+template <bool F> using F32K4S1Wide = F32Cfg<8, 2, 2, 16, 4, 1, 4, 4, F>;
 // fp32, 5x5 stride 1: 32 pairs x 4 rows (8 staged rows) x 64 channels.
 template <bool F> using F32K5S1Wide = F32Cfg<4, 2, 2, 16, 5, 1, 4, 4, F>;
 template <bool F> using F32K5S1Narrow = F32Cfg<4, 2, 2, 4, 5, 1, 1, 4, F>;
@@ -1124,12 +1151,14 @@ int pick_rows(const Shape& s, int nt, std::initializer_list<int> rows) {
 
 // bf16 3x3 tiles (one workgroup per compute unit): split a tile's r-chunks
 // between two workgroups only where that shortens the busiest compute unit's
-// chunk count and each half keeps at least 4 chunks (the small deep layers,
-// e.g. cv12: 60 tiles of 48 chunks on 256 compute units).
+// chunk count, the tiles are 2-row tiles at most two per compute unit
+// unsplit, and each half keeps at least 4 chunks (the small deep layers, e.g.
+// cv12: 60 tiles of 48 chunks on 256 compute units).
 bool split_shortens(const Shape& s, int ht, int nt, int kt) {
     const int64_t nchunks = (s.R + kt - 1) / kt;
     if (nchunks < 8) return false;
     const int64_t tiles = ((s.pairs + kPairs - 1) / kPairs) * ((s.o_h + ht - 1) / ht) * ((s.k_c + nt - 1) / nt);
+    if (ht != 2 || tiles > 512) return false;  // measured on 2-row tiles only
     return ((2 * tiles + 255) / 256) * ((nchunks + 1) / 2) < ((tiles + 255) / 256) * nchunks;
 }
 
@@ -1146,8 +1175,9 @@ bool split_shortens(const Shape& s, int ht, int nt, int kt) {
 // the unsplit choice is the fastest of the three row counts in every case
 // measured (e.g. cv10 2 rows, 21% faster than 4; cv9 4 rows, 13% faster than
 // 14; resnet_mid 14). A split is only considered where it shortens the
-// busiest compute unit's chunk count: layers whose tiles leave compute units
-// idle (cv11 12%, cv12 38% faster; the batch-1 layers).
+// busiest compute unit's chunk count, for 2-row tiles at most two per compute
+// unit unsplit: layers whose tiles leave compute units idle (cv11 12%, cv12
+// 38% faster; the batch-1 layers).
 struct TileChoice {
     int ht, ksplit;
 };
@@ -1167,10 +1197,16 @@ TileChoice pick_tiles_f32_3x3(const Shape& s) {
             const int64_t tiles = tiles1 * split;
             const double mfma = 1536.0 * (o.ht / 2);
             const int64_t per_cu = (tiles + 255) / 256;
-            // split only where it shortens the busiest compute unit's r-chunks;
-            // otherwise it just doubles the tiles sharing each one (measured
-            // slower than the model says: cv6 122 -> 144 us)
-            if (split == 2 && per_cu * nch >= ((tiles1 + 255) / 256) * nchunks) continue;
+            // split only where it shortens the busiest compute unit's r-chunks
+            // and the unsplit tiles are at most two per compute unit; otherwise
+            // it mostly multiplies the tiles sharing each one (measured slower
+            // than the model says: cv6 122 -> 144 us; the input-gradient
+            // convolution of cv10, 784 tiles, 113 -> 176 us)
+            // (and on 2-row tiles only: split 14-row tiles measured far off the
+            // model, cv10's input gradient 156 us against ~104 unsplit)
+            const int64_t per_cu1 = (tiles1 + 255) / 256;
+            if (split == 2 && (o.ht != 2 || per_cu1 > 2 || per_cu * nch >= per_cu1 * nchunks))
+                continue;
             // split: the zeroing launch (~4 us) and three passes over O
             double t = split == 1 ? 0.0 : 9600.0 + 3.0 * o_bytes / 5.0e12 * 2.4e9;
             for (int64_t done = 0; done < per_cu; done += o.w) {
@@ -1188,18 +1224,18 @@ TileChoice pick_tiles_f32_3x3(const Shape& s) {
 
 template <bool F>
 hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O, int dtype,
-                          hipStream_t stream, bool dry_run) {
-#define MEC_TRY_FIXED(CFG)                                                  \
-    if (usable<CFG>(s, A, K)) {                                             \
-        return dry_run ? hipSuccess : run_fixed<CFG>(s, A, K, O, stream);   \
-    }
-#define MEC_TRY_FIXED_SPLIT(CFG, KSPLIT)                                            \
+                          hipStream_t stream, bool dry_run, const OutLayout* layout) {
+#define MEC_TRY_FIXED(CFG)                                                          \
     if (usable<CFG>(s, A, K)) {                                                     \
-        return dry_run ? hipSuccess : run_fixed<CFG>(s, A, K, O, stream, KSPLIT);   \
+        return dry_run ? hipSuccess : run_fixed<CFG>(s, A, K, O, stream, 1, layout); \
     }
-#define MEC_TRY_STREAM(CFG)                                                 \
-    if (stream_usable<CFG>(s, A, K)) {                                      \
-        return dry_run ? hipSuccess : run_stream<CFG>(s, A, K, O, stream);  \
+#define MEC_TRY_FIXED_SPLIT(CFG, KSPLIT)                                                  \
+    if (usable<CFG>(s, A, K)) {                                                           \
+        return dry_run ? hipSuccess : run_fixed<CFG>(s, A, K, O, stream, KSPLIT, layout); \
+    }
+#define MEC_TRY_STREAM(CFG)                                                         \
+    if (stream_usable<CFG>(s, A, K)) {                                              \
+        return dry_run ? hipSuccess : run_stream<CFG>(s, A, K, O, stream, layout);  \
     }
     if (dtype == 0) {
         if (s.R >= 32) {
@@ -1216,6 +1252,8 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
         MEC_TRY_FIXED(F32K7S2Narrow<F>);
         MEC_TRY_FIXED(F32K7S2Scalar<F>);
         MEC_TRY_FIXED(F32K5S1Wide<F>);
+        MEC_TRY_FIXED(F32K2S1Wide<F>);
+        MEC_TRY_FIXED(F32K4S1Wide<F>);
         MEC_TRY_FIXED(F32K5S1Narrow<F>);
         MEC_TRY_FIXED(F32K5S1Scalar<F>);
         using K11V4 = F32K11S4<F, 4>;
@@ -1227,6 +1265,7 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
         MEC_TRY_FIXED(F32K1S1Narrow<F>);
         MEC_TRY_FIXED(F32K1S1Scalar<F>);
     } else {
+        if (layout) return hipErrorNotSupported;  // dense O only
         {
             const int ht = s.k_h == 3 && s.s_h == 1 ? pick_rows(s, 128, {14, 4, 2}) : 14;
             const int ks = split_shortens(s, ht, 128, 32) ? 2 : 1;
@@ -1245,9 +1284,9 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
 }  // namespace
 
 hipError_t launch_gemm_fixed(const Shape& s, const void* A, const void* K, float* O, int dtype,
-                             bool fused, hipStream_t stream, bool dry_run) {
-    if (fused) return dispatch_fixed<true>(s, A, K, O, dtype, stream, dry_run);
-    return dispatch_fixed<false>(s, A, K, O, dtype, stream, dry_run);
+                             bool fused, hipStream_t stream, bool dry_run, const OutLayout* layout) {
+    if (fused) return dispatch_fixed<true>(s, A, K, O, dtype, stream, dry_run, layout);
+    return dispatch_fixed<false>(s, A, K, O, dtype, stream, dry_run, layout);
 }
 
 }  // namespace mec

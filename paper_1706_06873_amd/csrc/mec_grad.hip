@@ -600,8 +600,8 @@ struct PadParams {
     float* Gp;
     uint32_t units;          // 4-channel groups (or elements) of G'
     uint32_t o_h, o_w, k_c;  // G's shape
-    uint32_t ph, pw;         // padding: k_h - 1, k_w - 1
-    uint32_t hp, wp;         // G' rows and columns: o_h + 2*ph, o_w + 2*pw
+    uint32_t ph, pw;         // zero rows above and columns left of G in G'
+    uint32_t hp, wp;         // G' rows and columns (G's rows and columns past them unused)
     FastDiv div_kc, div_wp, div_hp;
 };
 
@@ -622,17 +622,25 @@ __global__ __launch_bounds__(kGradThreads) void pad_grad_kernel(PadParams p) {
     }
 }
 
-// K'[a, b, m, c] = K[k_h-1-a, k_w-1-b, c, m]; one thread per element of K'.
-__global__ __launch_bounds__(kGradThreads) void flip_kernel_kernel(const float* K, float* Kp,
-                                                                   uint32_t total, uint32_t k_h,
-                                                                   uint32_t k_w, uint32_t i_c,
-                                                                   uint32_t k_c) {
+// The sub-kernel of sub-pixel phase (py, px) of the input gradient:
+// K'[j, i, m, c] = K[py + s_h*(J-1-j), px + s_w*(I-1-i), c, m] for j < J, i < I
+// (the kernel taps that reach the phase, turned by 180 degrees, with input and
+// output channels swapped). Stride 1: K turned by 180 degrees and transposed.
+// One thread per element of K'.
+struct PhaseKernelParams {
+    const float* K;
+    float* Kp;
+    uint32_t total, J, I, i_c, k_c, k_w, py, px, s_h, s_w;
+};
+
+__global__ __launch_bounds__(kGradThreads) void phase_kernel_kernel(PhaseKernelParams p) {
     const uint32_t stride = gridDim.x * kGradThreads;
-    for (uint32_t e = blockIdx.x * kGradThreads + threadIdx.x; e < total; e += stride) {
-        const uint32_t c = e % i_c, t = e / i_c;
-        const uint32_t m = t % k_c, t2 = t / k_c;
-        const uint32_t b = t2 % k_w, a = t2 / k_w;
-        Kp[e] = K[(((k_h - 1 - a) * k_w + (k_w - 1 - b)) * i_c + c) * k_c + m];
+    for (uint32_t e = blockIdx.x * kGradThreads + threadIdx.x; e < p.total; e += stride) {
+        const uint32_t c = e % p.i_c, t = e / p.i_c;
+        const uint32_t m = t % p.k_c, t2 = t / p.k_c;
+        const uint32_t i = t2 % p.I, j = t2 / p.I;
+        const uint32_t a = p.py + p.s_h * (p.J - 1 - j), bb = p.px + p.s_w * (p.I - 1 - i);
+        p.Kp[e] = p.K[((a * p.k_w + bb) * p.i_c + c) * p.k_c + m];
     }
 }
 
@@ -856,81 +864,175 @@ hipError_t launch_wgrad(const Shape& s, const float* L, const float* G, float* p
     return hipGetLastError();
 }
 
-Shape dgrad_transposed_shape(const Shape& s) {
-    Shape t{};
+// Sub-pixel phase (py, px) of the input gradient: the pixels
+// dI[n, s_h*Y + py, s_w*X + px, :] receive G through the kernel taps
+// a = py + s_h*j (j < J) and b = px + s_w*i (i < I) only:
+//   dI[n, s_h*Y+py, s_w*X+px, c] = sum_{j,i,m} G[n, Y-j, X-i, m] K[py+s_h*j, px+s_w*i, c, m]
+// (G zero outside its o_h x o_w), which is a stride-1 correlation of G
+// zero-padded by J-1 rows above and I-1 columns to the left with the
+// sub-kernel K' of phase_kernel_kernel. Stride 1 has one phase: G padded by
+// k-1 on every side, K turned by 180 degrees and transposed.
+struct Phase {
+    Shape t;          // the phase's stride-1 convolution
+    int64_t py, px;   // which phase
+    int64_t gp_elems; // padded G
+};
+
+Phase dgrad_phase(const Shape& s, int64_t py, int64_t px) {
+    Phase ph{};
+    ph.py = py;
+    ph.px = px;
+    const int64_t J = (s.k_h - py + s.s_h - 1) / s.s_h, I = (s.k_w - px + s.s_w - 1) / s.s_w;
+    const int64_t Ny = (s.i_h - py + s.s_h - 1) / s.s_h, Nx = (s.i_w - px + s.s_w - 1) / s.s_w;
+    Shape& t = ph.t;
     t.i_n = s.i_n;
-    t.i_h = s.o_h + 2 * (s.k_h - 1);
-    t.i_w = s.o_w + 2 * (s.k_w - 1);
+    t.i_h = Ny + J - 1;
+    t.i_w = Nx + I - 1;
     t.i_c = s.k_c;
-    t.k_h = s.k_h;
-    t.k_w = s.k_w;
+    t.k_h = J;
+    t.k_w = I;
     t.k_c = s.i_c;
     t.s_h = t.s_w = 1;
-    t.o_h = t.i_h - t.k_h + 1;  // = i_h
-    t.o_w = t.i_w - t.k_w + 1;  // = i_w
+    t.o_h = Ny;
+    t.o_w = Nx;
     t.R = t.k_w * t.i_c;
     t.pairs = t.i_n * t.o_w;
-    return t;
+    ph.gp_elems = t.i_n * t.i_h * t.i_w * t.i_c;
+    return ph;
 }
 
-// Taken for stride 1, kernels up to 3x3 and i_c >= 32 (the transposed
-// convolution's output channels): measured on the benchmark layers it beats
-// the dL path there (cv9 1.4x, cv8 1.26x, resnet_mid 1.2x) and loses on 5x5
-// kernels (cv5) and on few-channel outputs.
-bool dgrad_transposed_ok(const Shape& s) {
-    if (s.s_h != 1 || s.s_w != 1 || s.i_c < 32 || s.k_h > 3 || s.k_w > 3) return false;
-    if (s.k_h * s.k_w * s.i_c * s.k_c >= (int64_t(1) << 31)) return false;
-    const Shape t = dgrad_transposed_shape(s);
-    if (t.i_n * t.i_h * t.i_w * t.i_c >= (int64_t(1) << 31)) return false;
-    if (t.R > (int64_t(1) << 26)) return false;
-    return gemm_supported(t, 0);
+// Where phase (py, px) writes in dI (nullptr: dense, stride 1).
+OutLayout phase_layout(const Shape& s, const Phase& ph) {
+    OutLayout o{};
+    o.img = s.i_h * s.i_w * s.i_c;
+    o.row = s.s_h * s.i_w * s.i_c;
+    o.col = s.s_w * s.i_c;
+    o.off = (ph.py * s.i_w + ph.px) * s.i_c;
+    return o;
 }
+
+// Taken for i_c >= 32 (the phases' output channels) and, at stride 1, kernels
+// up to 3x3: measured on the benchmark layers it beats the dL path there (cv9
+// 1.4x, cv8 1.26x, resnet_mid 1.2x) and loses on 5x5 kernels (cv5) and on
+// few-channel outputs. Strided (s <= k, every phase reaches some tap): k_c and
+// i_c multiples of 4 and phase kernel heights up to 5, so that every phase has
+// a fixed kernel with 16-byte rows that takes a strided output layout, and at
+// most 4 phases of at least 10 taps each on average: the phases run one after
+// another as small convolutions, and measured faster than the dL path for
+// 7x7 stride 2 (cv4: 4.85 -> 1.77 ms, workspace 1.3 GB -> 104 MB) but slower
+// for 3x3 (1.0-1.7x) and 5x5 (2.9x) stride 2.
+bool dgrad_phases_ok(const Shape& s) {
+    if (s.i_c < 32) return false;
+    if (s.k_h * s.k_w * s.i_c * s.k_c >= (int64_t(1) << 31)) return false;
+    const bool unit = s.s_h == 1 && s.s_w == 1;
+    if (unit && (s.k_h > 3 || s.k_w > 3)) return false;
+    if (!unit && (s.s_h > s.k_h || s.s_w > s.k_w || s.k_c % 4 || s.i_c % 4 ||
+                  (s.k_h + s.s_h - 1) / s.s_h > 5))
+        return false;  // phase kernels with 16-byte rows, heights 1-5
+    if (!unit && (s.k_h * s.k_w < 10 * s.s_h * s.s_w || s.s_h * s.s_w > 4))
+        return false;  // phases too small: one small launch each
+    if (s.i_n * s.i_h * s.i_w * s.i_c >= (int64_t(1) << 31)) return false;
+    for (int64_t py = 0; py < s.s_h; ++py)
+        for (int64_t px = 0; px < s.s_w; ++px) {
+            const Phase ph = dgrad_phase(s, py, px);
+            if (ph.gp_elems >= (int64_t(1) << 31) || ph.t.R > (int64_t(1) << 26)) return false;
+            if (unit) {
+                if (!gemm_supported(ph.t, 0)) return false;
+            } else {
+                const OutLayout o = phase_layout(s, ph);
+                if (launch_gemm_fixed(ph.t, nullptr, nullptr, nullptr, 0, true, nullptr, true, &o) !=
+                    hipSuccess)
+                    return false;
+            }
+        }
+    return true;
+}
+
+namespace {
+// workspace: from its first 16-byte boundary (the caller guarantees 4-byte
+// alignment), the largest phase's padded G (rounded to 256 bytes), then the
+// largest K'
+int64_t phases_gp_bytes(const Shape& s) {
+    int64_t gp = 0;
+    for (int64_t py = 0; py < s.s_h; ++py)
+        for (int64_t px = 0; px < s.s_w; ++px) {
+            const int64_t e = dgrad_phase(s, py, px).gp_elems;
+            if (e > gp) gp = e;
+        }
+    return (gp * 4 + 255) / 256 * 256;
+}
+}  // namespace
 
 int64_t dgrad_workspace_bytes(const Shape& s) {
-    if (!dgrad_transposed_ok(s)) return s.i_n * s.o_w * s.i_h * s.k_w * s.i_c * 4;  // dL
-    const Shape t = dgrad_transposed_shape(s);
-    const int64_t gp = (t.i_n * t.i_h * t.i_w * t.i_c * 4 + 255) / 256 * 256;
-    return gp + s.k_h * s.k_w * s.i_c * s.k_c * 4;
+    if (!dgrad_phases_ok(s)) return s.i_n * s.o_w * s.i_h * s.k_w * s.i_c * 4;  // dL
+    int64_t kp = 0;
+    for (int64_t py = 0; py < s.s_h; ++py)
+        for (int64_t px = 0; px < s.s_w; ++px) {
+            const Shape& t = dgrad_phase(s, py, px).t;
+            if (t.k_h * t.k_w * t.i_c * t.k_c > kp) kp = t.k_h * t.k_w * t.i_c * t.k_c;
+        }
+    return 12 + phases_gp_bytes(s) + kp * 4;
 }
 
-hipError_t launch_dgrad_transposed(const Shape& s, const float* G, const float* K, float* dI,
-                                   void* workspace, hipStream_t stream) {
-    const Shape t = dgrad_transposed_shape(s);
-    float* Gp = static_cast<float*>(workspace);
-    const int64_t gp_bytes = (t.i_n * t.i_h * t.i_w * t.i_c * 4 + 255) / 256 * 256;
-    float* Kp = reinterpret_cast<float*>(static_cast<char*>(workspace) + gp_bytes);
-    PadParams p{};
-    p.G = G;
-    p.Gp = Gp;
-    p.o_h = (uint32_t)s.o_h;
-    p.o_w = (uint32_t)s.o_w;
-    p.k_c = (uint32_t)s.k_c;
-    p.ph = (uint32_t)(s.k_h - 1);
-    p.pw = (uint32_t)(s.k_w - 1);
-    p.hp = (uint32_t)t.i_h;
-    p.wp = (uint32_t)t.i_w;
-    p.div_kc = FastDiv(p.k_c);
-    p.div_wp = FastDiv(p.wp);
-    p.div_hp = FastDiv(p.hp);
-    const int64_t elems = t.i_n * t.i_h * t.i_w * t.i_c;
-    const bool vec = s.k_c % 4 == 0 && aligned16(G) && aligned16(Gp);
-    p.units = (uint32_t)(vec ? elems / 4 : elems);
-    int64_t blocks = ((int64_t)p.units + kGradThreads - 1) / kGradThreads;
-    if (blocks > 65536) blocks = 65536;
-    if (vec)
-        hipLaunchKernelGGL(pad_grad_kernel<4>, dim3((uint32_t)blocks), dim3(kGradThreads), 0, stream, p);
-    else
-        hipLaunchKernelGGL(pad_grad_kernel<1>, dim3((uint32_t)blocks), dim3(kGradThreads), 0, stream, p);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    const uint32_t ktot = (uint32_t)(s.k_h * s.k_w * s.i_c * s.k_c);
-    int64_t kblocks = ((int64_t)ktot + kGradThreads - 1) / kGradThreads;
-    if (kblocks > 65536) kblocks = 65536;
-    hipLaunchKernelGGL(flip_kernel_kernel, dim3((uint32_t)kblocks), dim3(kGradThreads), 0, stream, K,
-                       Kp, ktot, (uint32_t)s.k_h, (uint32_t)s.k_w, (uint32_t)s.i_c, (uint32_t)s.k_c);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    return launch_gemm(t, Gp, Kp, dI, 0, true, stream);
+hipError_t launch_dgrad_phases(const Shape& s, const float* G, const float* K, float* dI,
+                               void* workspace, hipStream_t stream) {
+    char* base = static_cast<char*>(workspace) + ((16 - ((uintptr_t)workspace & 15u)) & 15u);
+    float* Gp = reinterpret_cast<float*>(base);
+    float* Kp = reinterpret_cast<float*>(base + phases_gp_bytes(s));
+    const bool unit = s.s_h == 1 && s.s_w == 1;
+    for (int64_t py = 0; py < s.s_h; ++py)
+        for (int64_t px = 0; px < s.s_w; ++px) {
+            const Phase ph = dgrad_phase(s, py, px);
+            const Shape& t = ph.t;
+            PadParams p{};
+            p.G = G;
+            p.Gp = Gp;
+            p.o_h = (uint32_t)s.o_h;
+            p.o_w = (uint32_t)s.o_w;
+            p.k_c = (uint32_t)s.k_c;
+            p.ph = (uint32_t)(t.k_h - 1);
+            p.pw = (uint32_t)(t.k_w - 1);
+            p.hp = (uint32_t)t.i_h;
+            p.wp = (uint32_t)t.i_w;
+            p.div_kc = FastDiv(p.k_c);
+            p.div_wp = FastDiv(p.wp);
+            p.div_hp = FastDiv(p.hp);
+            const bool vec = s.k_c % 4 == 0 && aligned16(G) && aligned16(Gp);
+            p.units = (uint32_t)(vec ? ph.gp_elems / 4 : ph.gp_elems);
+            int64_t blocks = ((int64_t)p.units + kGradThreads - 1) / kGradThreads;
+            if (blocks > 65536) blocks = 65536;
+            if (vec)
+                hipLaunchKernelGGL(pad_grad_kernel<4>, dim3((uint32_t)blocks), dim3(kGradThreads), 0,
+                                   stream, p);
+            else
+                hipLaunchKernelGGL(pad_grad_kernel<1>, dim3((uint32_t)blocks), dim3(kGradThreads), 0,
+                                   stream, p);
+            hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return e;
+            PhaseKernelParams q{};
+            q.K = K;
+            q.Kp = Kp;
+            q.total = (uint32_t)(t.k_h * t.k_w * t.i_c * t.k_c);
+            q.J = (uint32_t)t.k_h;
+            q.I = (uint32_t)t.k_w;
+            q.i_c = (uint32_t)s.i_c;
+            q.k_c = (uint32_t)s.k_c;
+            q.k_w = (uint32_t)s.k_w;
+            q.py = (uint32_t)py;
+            q.px = (uint32_t)px;
+            q.s_h = (uint32_t)s.s_h;
+            q.s_w = (uint32_t)s.s_w;
+            int64_t kblocks = ((int64_t)q.total + kGradThreads - 1) / kGradThreads;
+            if (kblocks > 65536) kblocks = 65536;
+            hipLaunchKernelGGL(phase_kernel_kernel, dim3((uint32_t)kblocks), dim3(kGradThreads), 0,
+                               stream, q);
+            e = hipGetLastError();
+            if (e != hipSuccess) return e;
+            const OutLayout o = phase_layout(s, ph);
+            e = launch_gemm(t, Gp, Kp, dI, 0, true, stream, unit ? nullptr : &o);
+            if (e != hipSuccess) return e;
+        }
+    return hipSuccess;
 }
 
 }  // namespace mec

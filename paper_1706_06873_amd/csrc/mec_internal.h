@@ -83,33 +83,49 @@ struct GemmParams {
     uint32_t ntiles;
 };
 
+struct OutLayout;
+
 // Enqueue the slab products. fused selects the I-sourced variant.
 // Returns hipErrorInvalidValue when the shape exceeds the kernels' on-chip
-// limits (see gemm_supported), else the launch status.
+// limits (see gemm_supported), else the launch status. A strided output
+// layout (fp32 only) is taken by the fixed kernels alone: hipErrorNotSupported
+// when none of them matches.
 hipError_t launch_gemm(const Shape& s, const void* A, const void* K, float* O, int dtype,
-                       bool fused, hipStream_t stream);
+                       bool fused, hipStream_t stream, const OutLayout* layout = nullptr);
 
 // Whether the slab-product kernels can run this shape (LDS limits).
 bool gemm_supported(const Shape& s, int dtype);
 
+// Where the fp32 kernels of mec_gemm_fixed.hip write output element
+// (n, h, w, c): O + n*img + h*row + w*col + off + c. The default (nullptr)
+// is dense n-h-w-c; a strided layout lets one sub-pixel phase of the input
+// gradient write straight into its positions of dI.
+struct OutLayout {
+    int64_t img, row, col, off;
+};
+
 // The kernels specialised for a compile-time kernel height and stride.
 // Returns hipErrorNotSupported when none matches the shape (or the pointers'
-// alignment); with dry_run, only reports whether one matches.
+// alignment, or a non-default layout with dtype bf16); with dry_run, only
+// reports whether one matches.
 hipError_t launch_gemm_fixed(const Shape& s, const void* A, const void* K, float* O, int dtype,
-                             bool fused, hipStream_t stream, bool dry_run);
+                             bool fused, hipStream_t stream, bool dry_run,
+                             const OutLayout* layout = nullptr);
 
 // ---------------------------------------------------------------- training passes
 // dL (fp32, L's layout) from G = dloss/dO and K, fp32.
 bool dgrad_supported(const Shape& s);
 hipError_t launch_dgrad_dl(const Shape& s, const float* G, const float* K, float* dL,
                            hipStream_t stream);
-// dI for stride 1 as a forward convolution of the zero-padded G with the
-// kernel turned by 180 degrees and transposed (fused slab products); G' and K'
-// go to the workspace (dgrad_workspace_bytes).
-bool dgrad_transposed_ok(const Shape& s);
+// dI as s_h*s_w sub-pixel phases, each a stride-1 forward convolution of the
+// zero-padded G with the taps of K that reach it, turned by 180 degrees and
+// transposed (fused slab products, written straight into the phase's pixels
+// of dI); the padded G and K' go to the workspace (dgrad_workspace_bytes),
+// one phase after the other.
+bool dgrad_phases_ok(const Shape& s);
 int64_t dgrad_workspace_bytes(const Shape& s);
-hipError_t launch_dgrad_transposed(const Shape& s, const float* G, const float* K, float* dI,
-                                   void* workspace, hipStream_t stream);
+hipError_t launch_dgrad_phases(const Shape& s, const float* G, const float* K, float* dI,
+                               void* workspace, hipStream_t stream);
 // dI from dL: the adjoint of the lowering.
 hipError_t launch_fold(const Shape& s, const float* dL, float* dI, hipStream_t stream);
 // dK from L and G: partial sums over shares of the reduction into `part`

@@ -259,22 +259,32 @@ def test_grad_enums_match_header():
     assert codes["MEC_GRAD_KERNEL_FROM_L"] == mec.GRAD_KERNEL_FROM_L
 
 
-@pytest.mark.parametrize("shape", SHAPES)
+GRAD_SHAPES = SHAPES + [
+    (2, 17, 15, 32, 3, 3, 40, 2, 2),    # 3x3 s2: phases too small, dL path
+    (2, 21, 19, 32, 7, 7, 36, 2, 2),    # 7x7 s2: phases of 4x4 .. 3x3 taps
+    (2, 21, 20, 32, 7, 5, 36, 2, 1),    # 7x5, strides 2 and 1
+    (2, 19, 18, 32, 5, 5, 40, 1, 2),    # 5x5, strides 1 and 2
+    (2, 15, 16, 32, 3, 5, 16, 2, 3),    # unequal strides, too small
+    (2, 23, 23, 64, 11, 11, 64, 2, 2),  # phase kernels of 6 rows: dL path
+    (2, 17, 15, 32, 3, 3, 42, 2, 2),    # k_c not a multiple of 4: dL path
+    (2, 17, 15, 32, 1, 1, 40, 2, 2),    # s > k: dL path
+    (2, 17, 15, 32, 5, 5, 40, 1, 1),    # stride 1, 5x5: dL path
+]
+
+
+@pytest.mark.parametrize("shape", GRAD_SHAPES)
 def test_grad_workspace_sizes(orc, shape):
     nL = orc.lowered_elems(*shape)
     i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w = shape
     if i_n * i_h * i_w * i_c >= 2 ** 31:
         assert mec.lib.mec_grad_workspace_bytes(*shape, 0, 0) == -5
         return
-    # dI: dL in fp32, exactly |L| * 4; or, for stride 1, k <= 3 and i_c >= 32, the padded
-    # G (rounded up to 256 bytes) and the turned kernel
+    # dI: dL in fp32, exactly |L| * 4; or, on the sub-pixel phase path, 12 bytes of
+    # alignment slack, the largest phase's padded G (rounded up to 256 bytes) and the
+    # largest phase kernel
     wi = mec.grad_workspace_bytes(*shape, grad_pass=mec.GRAD_INPUT)
-    o_h, o_w = orc.out_dim(i_h, k_h, s_h), orc.out_dim(i_w, k_w, s_w)
-    gp = (i_n * (o_h + 2 * (k_h - 1)) * (o_w + 2 * (k_w - 1)) * k_c * 4 + 255) // 256 * 256
-    if s_h == s_w == 1 and i_c >= 32 and k_h <= 3 and k_w <= 3:
-        assert wi == gp + k_h * k_w * i_c * k_c * 4
-    else:
-        assert wi == nL * 4
+    expect = dgrad_phase_workspace(shape)
+    assert wi == (expect if expect is not None else nL * 4)
     # dK: whole partial-sum buffers of k_h*k_w*i_c*k_c floats, 1..1024 of them
     part = mec.grad_workspace_bytes(*shape, grad_pass=mec.GRAD_KERNEL_FROM_L)
     E = k_h * k_w * i_c * k_c * 4
@@ -282,6 +292,30 @@ def test_grad_workspace_sizes(orc, shape):
     # from I: L in fp32 (rounded up to 256 bytes), then the partial sums
     assert mec.grad_workspace_bytes(*shape, grad_pass=mec.GRAD_KERNEL) == \
         (nL * 4 + 255) // 256 * 256 + part
+
+
+def dgrad_phase_workspace(shape):
+    """Workspace of the sub-pixel phase path for this shape, or None where the
+    library takes the dL path (its stated rule)."""
+    i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w = shape
+    unit = s_h == s_w == 1
+    if i_c < 32 or (unit and (k_h > 3 or k_w > 3)):
+        return None
+    if not unit and (s_h > k_h or s_w > k_w or k_c % 4 or i_c % 4 or -(-k_h // s_h) > 5):
+        return None
+    if not unit and (k_h * k_w < 10 * s_h * s_w or s_h * s_w > 4):
+        return None
+    gp = kp = 0
+    for py in range(s_h):
+        for px in range(s_w):
+            J, I = -(-(k_h - py) // s_h), -(-(k_w - px) // s_w)
+            Ny, Nx = -(-(i_h - py) // s_h), -(-(i_w - px) // s_w)
+            gp = max(gp, i_n * (Ny + J - 1) * (Nx + I - 1) * k_c)
+            kp = max(kp, J * I * k_c * i_c)
+    if unit:  # one phase: G padded by k - 1 on every side
+        o_h, o_w = i_h - k_h + 1, i_w - k_w + 1
+        assert gp == i_n * (o_h + 2 * (k_h - 1)) * (o_w + 2 * (k_w - 1)) * k_c
+    return 12 + (gp * 4 + 255) // 256 * 256 + kp * 4
 
 
 def test_grad_rejects_bf16_and_bad_pass():

@@ -39,6 +39,12 @@ SHAPES = [
     (3, 10, 11, 64, 3, 3, 32, 1, 1),    # dI as a convolution of the padded G (i_c >= 32)
     (2, 12, 12, 40, 3, 2, 24, 1, 1),    # the same, 3x2, ragged channels
     (2, 9, 9, 32, 1, 1, 8, 1, 1),       # the same, 1x1
+    (2, 21, 19, 32, 7, 7, 36, 2, 2),    # dI as sub-pixel phases: 7x7 s2 (4x4 .. 3x3 taps)
+    (2, 21, 20, 32, 7, 5, 36, 2, 1),    # 7x5, strides 2 and 1 (4x5 and 3x5 taps)
+    (2, 19, 18, 32, 5, 5, 40, 1, 2),    # 5x5, strides 1 and 2 (5x3 and 5x2 taps)
+    (2, 17, 15, 32, 3, 3, 40, 2, 2),    # 3x3 s2: phases too small, dL path
+    (2, 13, 12, 32, 5, 5, 24, 2, 2),    # 5x5 s2: dL path
+    (1, 30, 31, 32, 11, 11, 32, 4, 4),  # 11x11 s4: sixteen phases, dL path
 ]
 
 
@@ -65,6 +71,34 @@ def problem(seed, d, dist):
     return I, K, G
 
 
+def last_phase_padded_g(G, d):
+    """G zero-padded as the library pads it for its last sub-pixel phase
+    (py, px) = (s_h - 1, s_w - 1): J - 1 rows above, I - 1 columns left,
+    Ny + J - 1 rows and Nx + I - 1 columns in all."""
+    i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w = d
+    py, px = s_h - 1, s_w - 1
+    J, I = -(-(k_h - py) // s_h), -(-(k_w - px) // s_w)
+    Ny, Nx = -(-(i_h - py) // s_h), -(-(i_w - px) // s_w)
+    out = np.zeros((G.shape[0], Ny + J - 1, Nx + I - 1, G.shape[3]), np.float32)
+    rows, cols = min(G.shape[1], Ny), min(G.shape[2], Nx)
+    out[:, J - 1:J - 1 + rows, I - 1:I - 1 + cols] = G[:, :rows, :cols]
+    return out
+
+
+@pytest.mark.parametrize("d", [(2, 21, 19, 32, 7, 7, 36, 2, 2), (3, 10, 11, 64, 3, 3, 32, 1, 1)])
+def test_dgrad_phases_unaligned_workspace(orc, d):
+    """The phase path with a workspace that is only 4-byte aligned."""
+    say("dgrad unaligned ws", d)
+    I, K, G = problem(47 + sum(d), d, "int")
+    i_h, i_w, s_h, s_w = d[1], d[2], d[7], d[8]
+    ref = orc.conv2d_dgrad(G.numpy(), K.numpy(), i_h, i_w, s_h, s_w)
+    need = mec.grad_workspace_bytes(*d)
+    ws = torch.zeros(need + 4, dtype=torch.uint8, device=DEV)[4:]
+    dI = mec.conv2d_dgrad(G.to(DEV), K.to(DEV), i_h, i_w, s_h, s_w, workspace=ws)
+    torch.cuda.synchronize()
+    assert np.array_equal(dI.cpu().numpy(), ref.astype(np.float32))
+
+
 @pytest.mark.parametrize("d", SHAPES)
 @pytest.mark.parametrize("dist", ["int", "u11"])
 def test_dgrad(orc, d, dist):
@@ -84,9 +118,9 @@ def test_dgrad(orc, d, dist):
         # the dL path: the workspace holds dL
         assert np.array_equal(wsf.reshape(ref_dL.shape), dL)
     else:
-        # stride 1: the workspace starts with G zero-padded by k - 1 on every side
-        k_h, k_w = d[4], d[5]
-        Gp = np.pad(G.numpy(), ((0, 0), (k_h - 1, k_h - 1), (k_w - 1, k_w - 1), (0, 0)))
+        # sub-pixel phases: the workspace starts with the last phase's padded G
+        # (stride 1: the only phase, G zero-padded by k - 1 on every side)
+        Gp = last_phase_padded_g(G.numpy(), d)
         assert np.array_equal(wsf[:Gp.size].reshape(Gp.shape), Gp)
     if dist == "int":
         assert np.array_equal(dL, ref_dL.astype(np.float32))

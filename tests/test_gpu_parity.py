@@ -73,6 +73,9 @@ SWEEP = [
     (1, 23, 25, 3, 7, 7, 70, 2, 3),      # 7x7 s2, short rows, k_c not a multiple of 4
     (2, 14, 13, 32, 5, 5, 64, 1, 2),     # 5x5 s1, 16-byte rows
     (2, 14, 13, 32, 5, 5, 66, 1, 1),     # 5x5 s1, k_c not a multiple of 4
+    (2, 15, 14, 16, 2, 2, 40, 1, 1),     # 2x2 s1, 16-byte rows
+    (2, 17, 16, 8, 4, 4, 64, 1, 1),      # 4x4 s1, 16-byte rows
+    (3, 12, 13, 32, 4, 3, 36, 1, 2),     # 4x3, s_w = 2
 ]
 
 SWEEP_BF16 = [
