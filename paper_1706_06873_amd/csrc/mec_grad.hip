@@ -22,10 +22,13 @@
 //  fold      dI[n, h, x, c] = sum over w with 0 <= x - s_w*w < k_w of
 //            dL[n, w, h, x - s_w*w, c], in increasing w: a gather, one thread
 //            per element (or per 4 channels), bound by HBM bandwidth.
-//  dI, stride 1  for kernels up to 3x3 the input gradient is itself a
-//            convolution: G zero-padded by k - 1 on every side, correlated with
-//            K turned by 180 degrees and transposed; pad_grad and flip_kernel
-//            form the two operands and the forward's fused slab products run.
+//  dI as sub-pixel phases  the pixels dI[n, s_h*Y + py, s_w*X + px, :] of
+//            one phase receive G only through the taps a = py + s_h*j,
+//            b = px + s_w*i, so each phase is a stride-1 convolution: G zero-
+//            padded by J-1 rows and I-1 columns, correlated with those taps
+//            turned by 180 degrees and transposed (stride 1: one phase, padding
+//            k-1). pad_grad and phase_kernel form the operands; the forward's
+//            fused slab products write each phase straight into its pixels.
 //  wgrad     a share of the reduction over (pair, output row) on fp32 MFMA: a
 //            workgroup computes a 128 x 64 tile of dK (rows j = a*R + b*i_c + c,
 //            columns m) over the stages in its share, a stage being 16 pairs x
