@@ -1,7 +1,7 @@
 // MEC's slab products (Section 3.3, Algorithm 2, product phase) for kernel
 // heights and strides fixed at compile time: in fp32 3x3 stride 1, 5x5 stride
-// 1, 7x7 stride 2, 11x11 stride 4 and k_h = 1; in bf16 3x3 stride 1 and
-// k_h = 1 (the shapes of the paper's benchmark layers, Table 2). Same tiling as mec_gemm.hip -- a tile of 32
+// 1, 7x7 stride 2, 11x11 stride 4 and k_h = 1; in bf16 3x3 and 5x5 stride 1,
+// 7x7 stride 2 and k_h = 1 (the shapes of the paper's benchmark layers, Table 2). Same tiling as mec_gemm.hip -- a tile of 32
 // (n, w) pairs x HT output rows x NT channels stages the union of the slab rows
 // it needs, hrows = (HT-1)*s_h + k_h, once per r-chunk -- but with k_h and s_h
 // known the reduction over the kernel rows is fully unrolled: each wave loads
@@ -1129,6 +1129,10 @@ template <bool F> using BF16K1S1 = BF16Cfg<7, 8, 1, 32, 1, 1, F, 8>;
 template <bool F> using BF16K3S1 = BF16Cfg<14, 4, 2, 32, 3, 1, F, 8>;
 template <bool F> using BF16K3S1R4 = BF16Cfg<4, 4, 2, 32, 3, 1, F, 8>;
 template <bool F> using BF16K3S1R2 = BF16Cfg<2, 4, 2, 32, 3, 1, F, 8>;
+// bf16, 5x5 stride 1 (8 staged rows, r-chunks of 32) and 7x7 stride 2 (13
+// staged rows, r-chunks of 16): 32 pairs x 4 rows x 128 channels.
+template <bool F> using BF16K5S1 = BF16Cfg<4, 4, 2, 32, 5, 1, F, 8>;
+template <bool F> using BF16K7S2 = BF16Cfg<4, 4, 2, 16, 7, 2, F, 8>;
 
 // Of tiles that differ only in their number of output rows, the one that
 // minimises (rounds of tiles over the 256 compute units) x (input rows each
@@ -1273,6 +1277,8 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
             if (ht == 4) MEC_TRY_FIXED_SPLIT(BF16K3S1R4<F>, ks);
             MEC_TRY_FIXED_SPLIT(BF16K3S1<F>, ks);
         }
+        MEC_TRY_FIXED(BF16K5S1<F>);
+        MEC_TRY_FIXED(BF16K7S2<F>);
         MEC_TRY_FIXED(BF16K1S1<F>);
     }
 #undef MEC_TRY_FIXED

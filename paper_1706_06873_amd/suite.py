@@ -1,6 +1,6 @@
 """Timing suite over the paper's benchmark layers on one MI355X.
 
-    python -m paper_1706_06873_amd.suite table2 [--batch 32] [--dtype f32|bf16|both]
+    python -m paper_1706_06873_amd.suite table2 [--batch 32] [--dtype f32|bf16|both] [--yardstick]
     python -m paper_1706_06873_amd.suite stride [--batch 32] [--dtype f32]
     python -m paper_1706_06873_amd.suite resnet101 [--batch 1] [--dtype f32]
     python -m paper_1706_06873_amd.suite train [--layers resnet_mid,cv9,...] [--yardstick]
@@ -12,10 +12,13 @@ summary line weighing each layer by its count in ResNet-101, as Table 3 does:
 weighted workspace (MiB) and weighted time of MEC against im2col. ``train``
 times the training passes (fp32) per layer, each call between HIP events:
 ``conv2d_dgrad`` and ``conv2d_wgrad`` whole, and their parts -- the dL
-products against K and the fold (the input gradient's general path; stride-1
-layers with i_c >= 32 take a convolution of the padded gradient instead), the
-lowering and the partial A_h^T G_h sums with their reduction; with ``--yardstick`` it also times torch's own convolution
-gradients (the vendor library) on the same shapes in NCHW, for context.
+products against K and the fold (the input gradient's general path; layers
+taking the sub-pixel phases of the padded gradient run those instead), the
+lowering and the partial A_h^T G_h sums with their reduction; with
+``--yardstick`` it also times torch's own convolution gradients (the vendor
+library) on the same shapes in NCHW, for context. ``table2 --yardstick`` (and
+the other forward modes) also times the vendor GEMM (hipBLASLt through torch)
+on the same im2col matrix, for context: im2col + vendor GEMM.
 For every layer it times MEC from L (compact lowering + slab products), MEC
 fused, and the im2col baseline (im2col lowering + one product through the
 same kernels), each kernel between HIP events on its stream, on seeded
@@ -35,7 +38,7 @@ import paper_1706_06873_amd as mec
 from paper_1706_06873_amd import workloads as wl
 
 
-def _time_layer(layer, reps, warmup, sets):
+def _time_layer(layer, reps, warmup, sets, yardstick=False):
     i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w = layer.dims
     o_h, o_w = mec.output_dims(i_h, i_w, k_h, k_w, s_h, s_w)
     dt = mec.BF16 if layer.dtype == "bf16" else mec.F32
@@ -92,6 +95,23 @@ def _time_layer(layer, reps, warmup, sets):
         if algo != "fused":
             res[algo]["lower_us"] = round(med(low), 2)
             res[algo]["product_us"] = round(med(prod), 2)
+        if algo == "im2col" and yardstick:
+            # context only: the vendor GEMM (hipBLASLt through torch) on the same
+            # im2col matrix, rows (n, x, y); its result is not in O's layout
+            Mv, Kv = bufs[0]["W"].view(-1, P), bufs[0]["K"].view(P, k_c)
+            with torch.cuda.stream(stream):
+                for _ in range(warmup):
+                    torch.matmul(Mv, Kv)
+                torch.cuda.synchronize()
+                gev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(reps)]
+                for r in range(reps):
+                    gev[r][0].record(stream)
+                    torch.matmul(Mv, Kv)
+                    gev[r][1].record(stream)
+                torch.cuda.synchronize()
+            g = med(sorted(e[0].elapsed_time(e[1]) * 1e3 for e in gev))
+            res["im2col"]["vendor_gemm_us"] = round(g, 2)
+            res["im2col"]["im2col_plus_vendor_gemm_us"] = round(med(low) + g, 2)
         for b in bufs:
             b.pop("W", None)
         torch.cuda.empty_cache()
@@ -178,7 +198,8 @@ def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("which", choices=["table2", "stride", "resnet101", "train"])
     ap.add_argument("--yardstick", action="store_true",
-                    help="train: also time torch's convolution gradients")
+                    help="train: also time torch's convolution gradients; forward modes: "
+                         "the vendor GEMM on the im2col matrix")
     ap.add_argument("--batch", type=int, default=None,
                     help="images per layer (default 32; 1 for resnet101, as in Table 3)")
     ap.add_argument("--dtype", default="f32", choices=["f32", "bf16", "both"])
@@ -213,7 +234,7 @@ def main(argv=None):
         layers = [wl.table2_layer("cv1", batch, d, stride=s) for d in dtypes for s in strides]
     rows = []
     for layer in layers:
-        rows.append(_time_layer(layer, args.reps, args.warmup, args.sets))
+        rows.append(_time_layer(layer, args.reps, args.warmup, args.sets, args.yardstick))
         print(json.dumps(rows[-1]), flush=True)
     if args.which == "resnet101":
         for d in dtypes:

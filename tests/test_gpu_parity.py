@@ -88,6 +88,8 @@ SWEEP_BF16 = [
     (1, 4, 400, 64, 3, 3, 16, 1, 1),     # wide rows (gather lowering)
     (3, 18, 16, 40, 3, 3, 136, 1, 1),    # bf16 3x3: two channel tiles, the second ragged
     (2, 9, 40, 24, 3, 3, 8, 1, 2),       # bf16 3x3, R not a multiple of the r-chunk
+    (2, 14, 13, 32, 5, 5, 136, 1, 1),    # bf16 5x5 s1: two channel tiles, the second ragged
+    (2, 21, 19, 16, 7, 7, 40, 2, 2),     # bf16 7x7 s2, ragged channels
 ]
 
 
