@@ -654,11 +654,16 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_stream_kernel(FixedP
 //        thread loads an 8 (r) x 8 (channel) block with eight 16-byte loads and
 //        transposes it in registers into eight 16-byte LDS stores.
 // The padding puts the 8 rows of each 128-byte LDS access phase in distinct banks.
-template <int HT, int NB, int WAVES_H, int KT, int KH, int SH, bool FUSED, int WAVES = 4>
+// VECA = false: rows whose length R is not a multiple of 8 (e.g. 11x11x3):
+// the A pieces are gathered element by element and each row of a K block is
+// bounded by R on its own.
+template <int HT, int NB, int WAVES_H, int KT, int KH, int SH, bool FUSED, int WAVES = 4,
+          bool VECA = true>
 struct BF16Cfg {
     using T = TraitsBF16;
     using E = uint16_t;
-    static constexpr int kHT = HT, kKT = KT, kKH = KH, kSH = SH, kVA = 8, kVB = 8;
+    static constexpr int kHT = HT, kKT = KT, kKH = KH, kSH = SH, kVA = VECA ? 8 : 1, kVB = 8;
+    static constexpr bool kVecA = VECA;
     static constexpr bool kFused = FUSED;
     static constexpr int kWaves = WAVES;
     static constexpr int NT = 32 * NB;
@@ -796,22 +801,37 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_bf16_kernel(FixedParams 
         const uint32_t r0 = (uint32_t)(rc * KT);
 #pragma unroll
         for (int j = 0; j < AJ; ++j) {
-            if (FULL && (j + 1) * C::THREADS <= C::A_ITEMS) {
+            if (C::kVecA && FULL && (j + 1) * C::THREADS <= C::A_ITEMS) {
                 areg[j] = *reinterpret_cast<const uint4*>(Atile + (ag[j] + r0));
             } else {
                 areg[j] = make_uint4(0, 0, 0, 0);
-                if (ag[j] != 0xffffffffu && (int64_t)r0 + ar[j] < p.R)
-                    areg[j] = *reinterpret_cast<const uint4*>(Atile + (ag[j] + r0));
+                if (ag[j] != 0xffffffffu && (int64_t)r0 + ar[j] < p.R) {
+                    if (C::kVecA) {
+                        areg[j] = *reinterpret_cast<const uint4*>(Atile + (ag[j] + r0));
+                    } else {
+                        // element by element, each bounded by R
+                        uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+                        for (int k = 0; k < 8; ++k)
+                            if ((int64_t)r0 + ar[j] + k < p.R)
+                                w[k >> 1] |= (uint32_t)Atile[ag[j] + r0 + k] << (16 * (k & 1));
+                        areg[j] = make_uint4(w[0], w[1], w[2], w[3]);
+                    }
+                }
             }
         }
 #pragma unroll
         for (int j = 0; j < BJ; ++j) {
             const uint32_t off = bg[j] + (uint32_t)rc * kstep;
-            const bool ok = (FULL && (j + 1) * C::THREADS <= C::B_ITEMS) ||
+            const bool ok = (C::kVecA && FULL && (j + 1) * C::THREADS <= C::B_ITEMS) ||
                             (bg[j] != 0xffffffffu && (int64_t)r0 + br[j] < p.R);
 #pragma unroll
-            for (int i = 0; i < 8; ++i)
-                breg[j][i] = ok ? *reinterpret_cast<const uint4*>(Kg + (off + i * krow)) : make_uint4(0, 0, 0, 0);
+            for (int i = 0; i < 8; ++i) {
+                // rows past R belong to the next kernel row: zero (R % 8 != 0 only)
+                const bool row_ok = ok && (C::kVecA || (int64_t)r0 + br[j] + i < p.R);
+                breg[j][i] = row_ok ? *reinterpret_cast<const uint4*>(Kg + (off + i * krow))
+                                    : make_uint4(0, 0, 0, 0);
+            }
         }
     };
     auto store_stage = [&](int buf) {
@@ -979,9 +999,9 @@ bool usable(const Shape& s, const void* A, const void* K) {
 
 template <class C>
 struct KernelOf;
-template <int HT, int NB, int WH, int KT, int KH, int SH, bool F, int W>
-struct KernelOf<BF16Cfg<HT, NB, WH, KT, KH, SH, F, W>> {
-    static constexpr auto fn = slab_gemm_bf16_kernel<BF16Cfg<HT, NB, WH, KT, KH, SH, F, W>>;
+template <int HT, int NB, int WH, int KT, int KH, int SH, bool F, int W, bool V>
+struct KernelOf<BF16Cfg<HT, NB, WH, KT, KH, SH, F, W, V>> {
+    static constexpr auto fn = slab_gemm_bf16_kernel<BF16Cfg<HT, NB, WH, KT, KH, SH, F, W, V>>;
     static constexpr int threads = 64 * W;
 };
 template <int HT, int NB, int WH, int KT, int KH, int SH, int VA, int VB, bool F, int W>
@@ -1133,6 +1153,9 @@ template <bool F> using BF16K3S1R2 = BF16Cfg<2, 4, 2, 32, 3, 1, F, 8>;
 // staged rows, r-chunks of 16): 32 pairs x 4 rows x 128 channels.
 template <bool F> using BF16K5S1 = BF16Cfg<4, 4, 2, 32, 5, 1, F, 8>;
 template <bool F> using BF16K7S2 = BF16Cfg<4, 4, 2, 16, 7, 2, F, 8>;
+// bf16, 11x11 stride 4 over few channels (rows of 33 elements, gathered element
+// by element): 32 pairs x 2 rows (15 staged rows) x 96 channels, r-chunks of 16.
+template <bool F> using BF16K11S4 = BF16Cfg<2, 3, 2, 16, 11, 4, F, 6, false>;
 
 // Of tiles that differ only in their number of output rows, the one that
 // minimises (rounds of tiles over the 256 compute units) x (input rows each
@@ -1279,6 +1302,7 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
         }
         MEC_TRY_FIXED(BF16K5S1<F>);
         MEC_TRY_FIXED(BF16K7S2<F>);
+        MEC_TRY_FIXED(BF16K11S4<F>);
         MEC_TRY_FIXED(BF16K1S1<F>);
     }
 #undef MEC_TRY_FIXED

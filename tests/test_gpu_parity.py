@@ -90,6 +90,8 @@ SWEEP_BF16 = [
     (2, 9, 40, 24, 3, 3, 8, 1, 2),       # bf16 3x3, R not a multiple of the r-chunk
     (2, 14, 13, 32, 5, 5, 136, 1, 1),    # bf16 5x5 s1: two channel tiles, the second ragged
     (2, 21, 19, 16, 7, 7, 40, 2, 2),     # bf16 7x7 s2, ragged channels
+    (2, 35, 33, 3, 11, 11, 104, 4, 3),   # bf16 11x11 s4, rows of 33 gathered by element, two channel tiles
+    (1, 27, 29, 5, 11, 11, 40, 4, 4),    # the same, rows of 55
 ]
 
 
