@@ -92,6 +92,7 @@ SWEEP_BF16 = [
     (2, 21, 19, 16, 7, 7, 40, 2, 2),     # bf16 7x7 s2, ragged channels
     (2, 35, 33, 3, 11, 11, 104, 4, 3),   # bf16 11x11 s4, rows of 33 gathered by element, two channel tiles
     (1, 27, 29, 5, 11, 11, 40, 4, 4),    # the same, rows of 55
+    (1, 23, 25, 3, 7, 7, 72, 2, 3),      # bf16 7x7 s2, rows of 21: the generic kernel
 ]
 
 
