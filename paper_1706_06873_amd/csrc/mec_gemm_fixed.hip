@@ -1213,7 +1213,7 @@ bool split_shortens(const Shape& s, int ht, int nt, int kt) {
 struct TileChoice {
     int ht, ksplit;
 };
-TileChoice pick_tiles_f32_3x3(const Shape& s) {
+TileChoice pick_tiles_f32_3x3(const Shape& s, bool allow_split) {
     struct Opt { int ht, w; double ovh; };
     const Opt opts[3] = {{14, 1, 4600.0}, {4, 3, 2300.0}, {2, 4, 1500.0}};
     const int64_t nchunks = (s.R + 15) / 16;
@@ -1221,7 +1221,7 @@ TileChoice pick_tiles_f32_3x3(const Shape& s) {
     TileChoice best{14, 1};
     double best_t = 0.0;
     for (int split = 1; split <= 2; ++split) {
-        if (split == 2 && nchunks < 4) break;
+        if (split == 2 && (nchunks < 4 || !allow_split)) break;
         const int64_t nch = (nchunks + split - 1) / split;
         for (const Opt& o : opts) {
             const int64_t tiles1 = ((s.pairs + kPairs - 1) / kPairs) * ((s.o_h + o.ht - 1) / o.ht) *
@@ -1271,7 +1271,9 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
     }
     if (dtype == 0) {
         if (s.R >= 32) {
-            const TileChoice tc = s.k_h == 3 && s.s_h == 1 ? pick_tiles_f32_3x3(s) : TileChoice{14, 1};
+            // no split into a strided layout: zeroing O would clear other pixels
+            const TileChoice tc =
+                s.k_h == 3 && s.s_h == 1 ? pick_tiles_f32_3x3(s, layout == nullptr) : TileChoice{14, 1};
             if (tc.ht == 2) {
                 const int64_t wgs = ((s.pairs + kPairs - 1) / kPairs) * ((s.o_h + 1) / 2) *
                                     ((s.k_c + 63) / 64) * tc.ksplit;
