@@ -99,6 +99,28 @@ def test_dgrad_phases_unaligned_workspace(orc, d):
     assert np.array_equal(dI.cpu().numpy(), ref.astype(np.float32))
 
 
+@pytest.mark.parametrize("d", [(2, 21, 19, 32, 7, 7, 36, 2, 2), (2, 19, 18, 32, 5, 5, 40, 1, 2),
+                               (3, 10, 11, 64, 3, 3, 32, 1, 1)])
+def test_dgrad_phases_unaligned_g_and_di(orc, d):
+    """The phase path with G and dI one element off a 16-byte boundary: element
+    padding of G and element stores into the phase's pixels; nothing written
+    outside dI."""
+    say("dgrad unaligned G/dI", d)
+    I, K, G = problem(53 + sum(d), d, "int")
+    i_n, i_h, i_w, i_c, s_h, s_w = d[0], d[1], d[2], d[3], d[7], d[8]
+    ref = orc.conv2d_dgrad(G.numpy(), K.numpy(), i_h, i_w, s_h, s_w).astype(np.float32)
+    gbuf = torch.zeros(G.numel() + 8, device=DEV)
+    Gd = gbuf[1:1 + G.numel()].view(G.shape)
+    Gd.copy_(G.to(DEV))
+    obuf = torch.full((ref.size + 64,), 7.0, device=DEV)
+    dI = obuf[33:33 + ref.size].view(ref.shape)
+    mec.conv2d_dgrad(Gd, K.to(DEV), i_h, i_w, s_h, s_w, dI=dI)
+    torch.cuda.synchronize()
+    b = obuf.cpu().numpy()
+    assert np.all(b[:33] == 7.0) and np.all(b[33 + ref.size:] == 7.0)
+    assert np.array_equal(dI.cpu().numpy(), ref)
+
+
 @pytest.mark.parametrize("d", SHAPES)
 @pytest.mark.parametrize("dist", ["int", "u11"])
 def test_dgrad(orc, d, dist):
