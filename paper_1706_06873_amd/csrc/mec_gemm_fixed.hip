@@ -56,6 +56,7 @@ struct F32Cfg {
     using E = uint32_t;
     static constexpr int kHT = HT, kKT = KT, kKH = KH, kSH = SH, kVA = VA, kVB = VB;
     static constexpr bool kFused = FUSED;
+    static constexpr bool kDMA = false;
     static constexpr int NT = 32 * NB;
     static constexpr int kWaves = WAVES;
     static constexpr int THREADS = 64 * WAVES;
@@ -657,13 +658,22 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_stream_kernel(FixedP
 // VECA = false: rows whose length R is not a multiple of 8 (e.g. 11x11x3):
 // the A pieces are gathered element by element and each row of a K block is
 // bounded by R on its own.
+// DMA = true: A and B go from global memory straight into LDS (16 bytes per
+// lane, no registers): A two r-chunks ahead through three stages, B one
+// chunk ahead through two. Stages are unpadded and their 16-byte granules
+// permuted so that fragment reads spread over the banks:
+//   A [x][pair][32 r]      granule g of row q at g ^ ((q >> 2) & 3)
+//   B [a][32 r][channel]   K's own layout; granule g of row r at g ^ (r & 8 ? 4 : 0)
+// A B fragment (8 consecutive r of one channel) is gathered by 16-bit reads.
+// Needs R % 32 == 0, so that no chunk holds a partial row.
 template <int HT, int NB, int WAVES_H, int KT, int KH, int SH, bool FUSED, int WAVES = 4,
-          bool VECA = true>
+          bool VECA = true, bool DMA = false>
 struct BF16Cfg {
     using T = TraitsBF16;
     using E = uint16_t;
     static constexpr int kHT = HT, kKT = KT, kKH = KH, kSH = SH, kVA = VECA ? 8 : 1, kVB = 8;
     static constexpr bool kVecA = VECA;
+    static constexpr bool kDMA = DMA;
     static constexpr bool kFused = FUSED;
     static constexpr int kWaves = WAVES;
     static constexpr int NT = 32 * NB;
@@ -674,19 +684,25 @@ struct BF16Cfg {
     static constexpr int HROWS = (HT - 1) * SH + KH;
     static constexpr int XW = (HW - 1) * SH + KH;
     static constexpr int KTP = KT + 8;                      // padded row (elements)
-    static constexpr int A_SIZE = HROWS * kPairs * KTP;
-    static constexpr int B_SIZE = KH * NT * KTP;
+    static constexpr int A_SIZE = HROWS * kPairs * (DMA ? KT : KTP);
+    static constexpr int B_SIZE = KH * NT * (DMA ? KT : KTP);
     static constexpr int STAGE = A_SIZE + B_SIZE;
+    // DMA: 16-byte granules per thread and chunk (one instruction each)
+    static constexpr int ADMA = DMA ? A_SIZE / 8 / THREADS : 0;
+    static constexpr int BDMA = DMA ? B_SIZE / 8 / THREADS : 0;
     static constexpr int RG = KT / 8;
     static constexpr int A_ITEMS = HROWS * kPairs * RG;     // (x, pair, 8-r group)
     static constexpr int AJ = (A_ITEMS + THREADS - 1) / THREADS;
     static constexpr int B_ITEMS = KH * RG * (NT / 8);      // (a, 8-r group, 8-channel group)
     static constexpr int BJ = (B_ITEMS + THREADS - 1) / THREADS;
     static constexpr int EPI_HALVES = WAVES * 32 * 40 * 2;  // epilogue: one 32x40 fp32 block per wave
-    static constexpr int LDS_HALVES = 2 * STAGE > EPI_HALVES ? 2 * STAGE : EPI_HALVES;
+    static constexpr int MAIN_HALVES = DMA ? 3 * A_SIZE + 2 * B_SIZE : 2 * STAGE;
+    static constexpr int LDS_HALVES = MAIN_HALVES > EPI_HALVES ? MAIN_HALVES : EPI_HALVES;
     static constexpr size_t LDS_BYTES = LDS_HALVES * sizeof(E);
     static_assert(WAVES % WAVES_H == 0 && HT % WAVES_H == 0 && NB % WAVES_N == 0, "wave split");
     static_assert(KT % 16 == 0, "chunk");
+    static_assert(!DMA || (KT == 32 && VECA && NB % 4 == 0 && ADMA * 8 * THREADS == A_SIZE &&
+                           BDMA * 8 * THREADS == B_SIZE && ADMA + BDMA < 16), "DMA stage");
     static_assert(LDS_BYTES + 1024 <= 160 * 1024, "LDS");
 };
 
@@ -705,6 +721,19 @@ __device__ inline void transpose8x8_b16(const uint4 (&in)[8], uint4 (&out)[8]) {
         }
         out[c] = make_uint4(d[0], d[1], d[2], d[3]);
     }
+}
+
+// One 16-byte load per lane from base + voff straight into LDS at byte address
+// lds + 16 * lane (M0 holds the wave's LDS address; its previous value is put
+// back, since M0 cannot be declared clobbered). The compiler does not see the
+// load: the caller waits on vmcnt before the data is read.
+__device__ inline void lds_dma16(const void* base, uint32_t voff, uint32_t lds) {
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %2, %3\n\ts_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "s"(lds), "v"(voff), "s"(base)
+        : "memory");
 }
 
 template <class C>
@@ -791,6 +820,47 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_bf16_kernel(FixedParams 
             if (n0 + cg * 8 < p.k_c) bg[j] = (uint32_t)(((int64_t)a * p.R + rg * 8) * p.k_c + n0 + cg * 8);
         }
     }
+    // DMA: this thread's granules, as byte offsets from the tile's A and from
+    // K; instruction j of a wave fills LDS slots (j * waves + wave) * 64 + lane
+    // of a stage. A pair past the end reads the tile's first pair, a row past
+    // the input its last row and a channel group past k_c the tile's first:
+    // all three only reach outputs that are never stored.
+    uint32_t adma[C::ADMA > 0 ? C::ADMA : 1], bdma[C::BDMA > 0 ? C::BDMA : 1];
+    if constexpr (C::kDMA) {
+#pragma unroll
+        for (int j = 0; j < C::ADMA; ++j) {
+            const int G = (j * C::kWaves + wave) * 64 + lane;
+            const int q = G >> 2, g = (G & 3) ^ ((q >> 2) & 3);
+            const int pp = q % kPairs, x = q / kPairs;
+            const int64_t ab = abase_s[pp] >= 0 ? abase_s[pp] : abase0;
+            const int64_t xr = x0 + x < p.i_h ? x0 + x : p.i_h - 1;
+            adma[j] = (uint32_t)(2 * (ab - abase0 + xr * p.a_xstride + g * 8));
+        }
+#pragma unroll
+        for (int j = 0; j < C::BDMA; ++j) {
+            const int G = (j * C::kWaves + wave) * 64 + lane;
+            const int q = G >> 4, r = q % KT, a = q / KT;
+            const int g = (G & 15) ^ (r & 8 ? 4 : 0);
+            const int nc = n0 + 8 * g < p.k_c ? n0 + 8 * g : n0;
+            bdma[j] = (uint32_t)(2 * (((int64_t)a * p.R + r) * p.k_c + nc));
+        }
+    }
+    const uint32_t lds0 = (uint32_t)(size_t)(__attribute__((address_space(3))) uint16_t*)lds;
+    const uint32_t wave_u = (uint32_t)__builtin_amdgcn_readfirstlane(wave);
+    auto a_stage = [&](int sa) { return lds + (C::kDMA ? sa * A_SIZE : sa * STAGE); };
+    auto b_stage = [&](int sb) { return lds + (C::kDMA ? 3 * A_SIZE + sb * C::B_SIZE : sb * STAGE + A_SIZE); };
+    auto dma_a = [&](int rc, int sa) {
+        const uint32_t dst = lds0 + 2u * (uint32_t)(sa * A_SIZE) + wave_u * 1024u;
+        const uint32_t r0 = (uint32_t)rc * (2u * KT);
+#pragma unroll
+        for (int j = 0; j < C::ADMA; ++j) lds_dma16(Atile, adma[j] + r0, dst + (uint32_t)(j * C::kWaves) * 1024u);
+    };
+    auto dma_b = [&](int rc, int sb) {
+        const uint32_t dst = lds0 + 2u * (uint32_t)(3 * A_SIZE + sb * C::B_SIZE) + wave_u * 1024u;
+        const uint32_t r0 = (uint32_t)rc * (2u * KT) * (uint32_t)p.k_c;
+#pragma unroll
+        for (int j = 0; j < C::BDMA; ++j) lds_dma16(Kg, bdma[j] + r0, dst + (uint32_t)(j * C::kWaves) * 1024u);
+    };
     const uint32_t kstep = (uint32_t)(KT * p.k_c);
     const uint32_t krow = (uint32_t)p.k_c;
 
@@ -800,7 +870,7 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_bf16_kernel(FixedParams 
         constexpr bool FULL = decltype(full_tag)::value;
         const uint32_t r0 = (uint32_t)(rc * KT);
 #pragma unroll
-        for (int j = 0; j < AJ; ++j) {
+        for (int j = 0; j < (C::kDMA ? 0 : AJ); ++j) {
             if (C::kVecA && FULL && (j + 1) * C::THREADS <= C::A_ITEMS) {
                 areg[j] = *reinterpret_cast<const uint4*>(Atile + (ag[j] + r0));
             } else {
@@ -835,9 +905,10 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_bf16_kernel(FixedParams 
         }
     };
     auto store_stage = [&](int buf) {
-        uint16_t* st = lds + buf * STAGE;
+        uint16_t* st = a_stage(buf);
+        uint16_t* sb = b_stage(buf);
 #pragma unroll
-        for (int j = 0; j < AJ; ++j)
+        for (int j = 0; j < (C::kDMA ? 0 : AJ); ++j)
             if ((j + 1) * C::THREADS <= C::A_ITEMS || al[j] >= 0)
                 *reinterpret_cast<uint4*>(st + al[j]) = areg[j];
 #pragma unroll
@@ -846,7 +917,7 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_bf16_kernel(FixedParams 
                 uint4 col[8];
                 transpose8x8_b16(breg[j], col);
 #pragma unroll
-                for (int c = 0; c < 8; ++c) *reinterpret_cast<uint4*>(st + A_SIZE + bl[j] + c * KTP) = col[c];
+                for (int c = 0; c < 8; ++c) *reinterpret_cast<uint4*>(sb + bl[j] + c * KTP) = col[c];
             }
         }
     };
@@ -862,25 +933,52 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_bf16_kernel(FixedParams 
     const int row = lane & 31;
     const int kofs = (lane >> 5) * 8;
     const int a_lane = ((wh * HW * SH) * kPairs + row) * KTP + kofs;
-    const int b_lane = A_SIZE + ((wn * NBW) * 32 + row) * KTP + kofs;
+    const int b_lane = ((wn * NBW) * 32 + row) * KTP + kofs;
+    // DMA: a lane's two k-steps read granules (lane >> 5) and 2 + (lane >> 5)
+    // of its row, at their swizzled positions
+    const int a_row = ((wh * HW * SH) * kPairs + row) * KT;
+    const int swz = (lane >> 2) & 3;
+    const int a_dma0 = a_row + 8 * ((lane >> 5) ^ swz);
+    const int a_dma1 = a_row + 8 * ((2 + (lane >> 5)) ^ swz);
+    // DMA: a lane's B element (r = kofs + t, channel ch) at (r * NT + granule * 8
+    // + ch % 8); r & 8 is (lane >> 5) * 8 for both k-steps
+    int b_dma[NBW];
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb) {
+        const int ch = (wn * NBW + nb) * 32 + row;
+        b_dma[nb] = kofs * NT + (((ch >> 3) ^ ((lane >> 5) * 4)) * 8) + (ch & 7);
+    }
 
-    auto compute = [&](int buf, auto mid) {
-        const uint16_t* As = lds + buf * STAGE + a_lane;
-        const uint16_t* Bs = lds + buf * STAGE + b_lane;
-        mid();  // the next chunk's global loads, in flight during both k-steps
+    auto compute = [&](int abuf, int bbuf, auto mid) {
+        const uint16_t* As = a_stage(abuf);
+        const uint16_t* Bs = b_stage(bbuf) + b_lane;
+        mid();  // the next chunks' global loads, in flight during both k-steps
 #pragma unroll
         for (int kk = 0; kk < KT; kk += 16) {
             bf16x8 af[XW];
             bf16x8 bf[KH][NBW];
 #pragma unroll
-            for (int i = 0; i < XW; ++i)
-                af[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(As + i * kPairs * KTP + kk));
+            for (int i = 0; i < XW; ++i) {
+                const uint16_t* src = C::kDMA ? As + (kk == 0 ? a_dma0 : a_dma1) + i * kPairs * KT
+                                              : As + a_lane + i * kPairs * KTP + kk;
+                af[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(src));
+            }
 #pragma unroll
             for (int a = 0; a < KH; ++a)
 #pragma unroll
-                for (int nb = 0; nb < NBW; ++nb)
-                    bf[a][nb] = __builtin_bit_cast(
-                        bf16x8, *reinterpret_cast<const uint4*>(Bs + (a * NT + nb * 32) * KTP + kk));
+                for (int nb = 0; nb < NBW; ++nb) {
+                    if constexpr (C::kDMA) {
+                        const uint16_t* src = b_stage(bbuf) + b_dma[nb] + (a * KT + kk) * NT;
+                        uint32_t w[4];
+#pragma unroll
+                        for (int k = 0; k < 4; ++k)
+                            w[k] = (uint32_t)src[(2 * k) * NT] | ((uint32_t)src[(2 * k + 1) * NT] << 16);
+                        bf[a][nb] = __builtin_bit_cast(bf16x8, make_uint4(w[0], w[1], w[2], w[3]));
+                    } else {
+                        bf[a][nb] = __builtin_bit_cast(
+                            bf16x8, *reinterpret_cast<const uint4*>(Bs + (a * NT + nb * 32) * KTP + kk));
+                    }
+                }
 #pragma unroll
             for (int a = 0; a < KH; ++a)
 #pragma unroll
@@ -899,17 +997,53 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_bf16_kernel(FixedParams 
         __syncthreads();
         for (int rc = c_begin; rc < c_end; ++rc) {
             const bool more = rc + 1 < c_end;
-            compute((rc - c_begin) & 1, [&] {
+            compute((rc - c_begin) & 1, (rc - c_begin) & 1, [&] {
                 if (more) load_stage(rc + 1, full_tag);
             });
             if (more) store_stage((rc + 1 - c_begin) & 1);
             __syncthreads();
         }
     };
-    if (full)
-        main_loop(std::true_type{});
-    else
-        main_loop(std::false_type{});
+    // DMA: in step i, B chunk i + 1 is issued before A chunk i + 2, so waiting
+    // until only this wave's ADMA newest operations are outstanding completes
+    // A and B chunk i + 1 and leaves A chunk i + 2 in flight; the barrier then
+    // publishes every wave's part. The loads are invisible to the compiler,
+    // so the wait and the barrier are one statement that no LDS access may
+    // cross.
+    auto sync_keep_a = [] {
+        asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(C::ADMA) : "memory");
+    };
+    auto sync_all = [] { asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
+    auto main_loop_dma = [&]() {
+        const int n = c_end - c_begin;
+        dma_b(c_begin, 0);
+        dma_a(c_begin, 0);
+        if (n > 1) {
+            dma_a(c_begin + 1, 1);
+            sync_keep_a();
+        } else {
+            sync_all();
+        }
+        for (int i = 0; i < n; ++i) {
+            const int rc = c_begin + i;
+            compute(i % 3, i & 1, [&] {
+                if (i + 1 < n) dma_b(rc + 1, (i + 1) & 1);
+                if (i + 2 < n) dma_a(rc + 2, (i + 2) % 3);
+            });
+            if (i + 2 < n)
+                sync_keep_a();
+            else
+                sync_all();
+        }
+    };
+    if constexpr (C::kDMA) {
+        main_loop_dma();
+    } else {
+        if (full)
+            main_loop(std::true_type{});
+        else
+            main_loop(std::false_type{});
+    }
 
     const int64_t ostride_h = p.o_w * p.k_c;
     const bool add = p.ksplit > 1;  // split tile: add into the zeroed O, as in the fp32 kernel
@@ -985,6 +1119,7 @@ template <class C>
 bool usable(const Shape& s, const void* A, const void* K) {
     if (s.k_h != C::kKH || s.s_h != C::kSH) return false;
     if (!offsets_fit(s, C::kFused)) return false;
+    if (C::kDMA && s.R % C::kKT) return false;
     if (C::kVA > 1) {
         if (A && !aligned16(A)) return false;
         if (s.R % C::kVA) return false;
@@ -999,9 +1134,9 @@ bool usable(const Shape& s, const void* A, const void* K) {
 
 template <class C>
 struct KernelOf;
-template <int HT, int NB, int WH, int KT, int KH, int SH, bool F, int W, bool V>
-struct KernelOf<BF16Cfg<HT, NB, WH, KT, KH, SH, F, W, V>> {
-    static constexpr auto fn = slab_gemm_bf16_kernel<BF16Cfg<HT, NB, WH, KT, KH, SH, F, W, V>>;
+template <int HT, int NB, int WH, int KT, int KH, int SH, bool F, int W, bool V, bool D>
+struct KernelOf<BF16Cfg<HT, NB, WH, KT, KH, SH, F, W, V, D>> {
+    static constexpr auto fn = slab_gemm_bf16_kernel<BF16Cfg<HT, NB, WH, KT, KH, SH, F, W, V, D>>;
     static constexpr int threads = 64 * W;
 };
 template <int HT, int NB, int WH, int KT, int KH, int SH, int VA, int VB, bool F, int W>
@@ -1152,8 +1287,11 @@ template <bool F> using F32K1S1Scalar = F32Cfg<8, 2, 2, 4, 1, 1, 1, 1, F>;
 template <bool F> using BF16K1S1 = BF16Cfg<7, 8, 1, 32, 1, 1, F, 8>;
 // bf16, 3x3 stride 1: 8 waves, 32 pairs x 14 rows x 128 channels, r-chunks of 32.
 template <bool F> using BF16K3S1 = BF16Cfg<14, 4, 2, 32, 3, 1, F, 8>;
+// The same tile staged by direct-to-LDS loads (rows of a multiple of 32).
+template <bool F> using BF16K3S1D = BF16Cfg<14, 4, 2, 32, 3, 1, F, 8, true, true>;
 template <bool F> using BF16K3S1R4 = BF16Cfg<4, 4, 2, 32, 3, 1, F, 8>;
 template <bool F> using BF16K3S1R2 = BF16Cfg<2, 4, 2, 32, 3, 1, F, 8>;
+template <bool F> using BF16K3S1R2D = BF16Cfg<2, 4, 2, 32, 3, 1, F, 8, true, true>;
 // bf16, 5x5 stride 1 (8 staged rows, r-chunks of 32) and 7x7 stride 2 (13
 // staged rows, r-chunks of 16): 32 pairs x 4 rows x 128 channels.
 template <bool F> using BF16K5S1 = BF16Cfg<4, 4, 2, 32, 5, 1, F, 8>;
@@ -1306,10 +1444,25 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
     } else {
         if (layout) return hipErrorNotSupported;  // dense O only
         {
-            const int ht = s.k_h == 3 && s.s_h == 1 ? pick_rows(s, 128, {14, 4, 2}) : 14;
-            const int ks = split_shortens(s, ht, 128, 32) ? 2 : 1;
+            // Whole r-chunks (R % 32 == 0): the direct-to-LDS tiles, 14 rows (one
+            // workgroup per compute unit) where they occupy at least three
+            // quarters of the 256 compute units, else 2 rows (two per compute
+            // unit); the faster of the two on every 3x3 layer of Table 2 and on a
+            // 14x14x512 layer at batch 256 (the rows-x-rounds model below picks 2
+            // rows there, 1.7x slower than 14 with these kernels).
+            const int64_t tiles14 = ((s.pairs + kPairs - 1) / kPairs) * ((s.o_h + 13) / 14) * ((s.k_c + 127) / 128);
+            const bool dma = s.R % 32 == 0;
+            const int ht = dma ? (tiles14 >= 192 ? 14 : 2)
+                               : s.k_h == 3 && s.s_h == 1 ? pick_rows(s, 128, {14, 4, 2}) : 14;
+            // With these tiles a split pays only on small outputs: adding the
+            // halves into O costs ~24 us per million outputs (cv10 at batch 32,
+            // 2.8M outputs: 20 -> 87 us split; cv12, 0.4M: 37 -> 33 us).
+            const int64_t n_out = s.i_n * s.o_h * s.o_w * s.k_c;
+            const int ks = split_shortens(s, ht, 128, 32) && (!dma || n_out <= (int64_t(1) << 20)) ? 2 : 1;
+            if (ht == 2) MEC_TRY_FIXED_SPLIT(BF16K3S1R2D<F>, ks);
             if (ht == 2) MEC_TRY_FIXED_SPLIT(BF16K3S1R2<F>, ks);
             if (ht == 4) MEC_TRY_FIXED_SPLIT(BF16K3S1R4<F>, ks);
+            MEC_TRY_FIXED_SPLIT(BF16K3S1D<F>, ks);
             MEC_TRY_FIXED_SPLIT(BF16K3S1<F>, ks);
         }
         MEC_TRY_FIXED(BF16K5S1<F>);

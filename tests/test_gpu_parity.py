@@ -311,6 +311,39 @@ def test_split_reduction(orc, dims, algo):
 
 
 # bf16 3x3 layers with few tiles split their reduction the same way.
+# bf16 3x3 tiles staged by direct-to-LDS loads (rows of a multiple of 32): the
+# 14-row form where its tiles fill at least 192 compute units, else 2 rows.
+DMA_CASES_BF16 = [
+    (95, 20, 19, 32, 3, 3, 136, 1, 1),   # 14 rows: 204 tiles; ragged pairs (1615), rows (18), channels
+    (3, 13, 11, 64, 3, 3, 72, 1, 1),     # 2 rows: ragged pairs, odd row count, one ragged channel tile
+    (2, 9, 10, 128, 3, 3, 264, 1, 1),    # 2 rows: three channel tiles, the last 8 wide
+]
+
+
+def tiles14(dims):
+    i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w = dims
+    o_h, o_w = mec.output_dims(i_h, i_w, k_h, k_w, s_h, s_w)
+    return -(-i_n * o_w // 32) * -(-o_h // 14) * -(-k_c // 128)
+
+
+@pytest.mark.parametrize("dims", DMA_CASES_BF16)
+@pytest.mark.parametrize("algo", ["lowered", "fused"])
+def test_bf16_direct_to_lds_tiles(orc, dims, algo):
+    say("bf16 dma", algo, dims)
+    assert (dims[5] * dims[3]) % 32 == 0
+    assert (tiles14(dims) >= 192) == (dims == DMA_CASES_BF16[0])
+    s_h, s_w = dims[7], dims[8]
+    Ii, Ki = case(53 + sum(dims), dims, dtype="bf16", dist="int")
+    refi = orc.conv2d_direct(host(Ii), host(Ki), s_h, s_w)
+    assert np.abs(refi).max() < 2 ** 24
+    assert np.array_equal(run_conv(Ii, Ki, s_h, s_w, algo), refi.astype(np.float32))
+    I32, K32 = case(59 + sum(dims), dims, dtype="f32")
+    I, K = I32.to(torch.bfloat16), K32.to(torch.bfloat16)
+    got = run_conv(I, K, s_h, s_w, algo)
+    assert rel_l2(got, orc.conv2d_direct(host(I), host(K), s_h, s_w)) <= TOL_F32
+    assert rel_l2(got, orc.conv2d_direct(host(I32), host(K32), s_h, s_w)) <= TOL_BF16_VS_F32
+
+
 SPLIT_CASES_BF16 = [
     (2, 7, 7, 512, 3, 3, 512, 1, 1),     # 12 tiles of 48 r-chunks
     (3, 9, 8, 256, 3, 3, 136, 1, 1),     # ragged channel tile
