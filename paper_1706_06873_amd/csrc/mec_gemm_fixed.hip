@@ -40,6 +40,19 @@ struct FixedParams {
     int64_t o_img, o_row, o_col, o_off;
 };
 
+// One 16-byte load per lane from base + voff straight into LDS at byte address
+// lds + 16 * lane (M0 holds the wave's LDS address; its previous value is put
+// back, since M0 cannot be declared clobbered). The compiler does not see the
+// load: the caller waits on vmcnt before the data is read.
+__device__ inline void lds_dma16(const void* base, uint32_t voff, uint32_t lds) {
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %2, %3\n\ts_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "s"(lds), "v"(voff), "s"(base)
+        : "memory");
+}
+
 // ---------------------------------------------------------------- fp32 kernel
 // The fp32 variant lays both stages out so that MFMA fragment reads are
 // consecutive across lanes (conflict-free) and stage writes are 16-byte:
@@ -49,14 +62,22 @@ struct FixedParams {
 // Each thread loads 4 pairs x VA consecutive r (global reads keep their runs
 // along r) and transposes them in registers into VA 16-byte LDS writes of 4
 // consecutive pairs.
+// DMA = true (KT = 16, 16-byte rows): both stages are filled by direct-to-LDS
+// loads, A two r-chunks ahead through three stages and B one chunk ahead
+// through two:
+//   A [x][pair][16 r]       granule g of row q at g ^ ((q >> 2) & 3)
+//   B [a][r][channel]       K's own layout
+// A lane reads 4 consecutive r of its pair with one 16-byte read, and the
+// four MFMAs of each 8-r block take r = j (lanes 0-31) and r = 4 + j (lanes
+// 32-63), j = 0..3, from A and B alike. Needs R % 16 == 0.
 template <int HT, int NB, int WAVES_H, int KT, int KH, int SH, int VA, int VB, bool FUSED,
-          int WAVES = 4>
+          int WAVES = 4, bool DMA = false>
 struct F32Cfg {
     using T = TraitsF32;
     using E = uint32_t;
     static constexpr int kHT = HT, kKT = KT, kKH = KH, kSH = SH, kVA = VA, kVB = VB;
     static constexpr bool kFused = FUSED;
-    static constexpr bool kDMA = false;
+    static constexpr bool kDMA = DMA;
     static constexpr int NT = 32 * NB;
     static constexpr int kWaves = WAVES;
     static constexpr int THREADS = 64 * WAVES;
@@ -68,6 +89,8 @@ struct F32Cfg {
     static constexpr int A_SIZE = HROWS * KT * kPairs;
     static constexpr int B_SIZE = KH * KT * NT;
     static constexpr int STAGE = A_SIZE + B_SIZE;
+    static constexpr int ADMA = DMA ? A_SIZE / 4 / THREADS : 0;  // DMA: granules per thread
+    static constexpr int BDMA = DMA ? B_SIZE / 4 / THREADS : 0;
     static constexpr int RG = KT / VA;                  // r-groups per staged row
     static constexpr int A_ITEMS = HROWS * RG * 8;      // (x, r-group, 4-pair group)
     static constexpr int AJ = (A_ITEMS + THREADS - 1) / THREADS;
@@ -81,10 +104,13 @@ struct F32Cfg {
     static constexpr bool WIDE_EPI = EPI_WIDE_WORDS <= 2 * STAGE || EPI_WIDE_WORDS <= 10240;
     static constexpr int EPI_LD = WIDE_EPI ? 32 * NBW + 8 : 40;
     static constexpr int EPI_WORDS = WAVES * 32 * EPI_LD;
-    static constexpr int LDS_WORDS = 2 * STAGE > EPI_WORDS ? 2 * STAGE : EPI_WORDS;
+    static constexpr int MAIN_WORDS = DMA ? 3 * A_SIZE + 2 * B_SIZE : 2 * STAGE;
+    static constexpr int LDS_WORDS = MAIN_WORDS > EPI_WORDS ? MAIN_WORDS : EPI_WORDS;
     static constexpr size_t LDS_BYTES = LDS_WORDS * sizeof(E);
     static_assert(WAVES % WAVES_H == 0 && HT % WAVES_H == 0 && NB % WAVES_N == 0, "wave split");
     static_assert(KT % 2 == 0 && KT % VA == 0 && (VB == 1 || VB == 4), "chunk");
+    static_assert(!DMA || (KT == 16 && VA == 4 && VB == 4 && ADMA * 4 * THREADS == A_SIZE &&
+                           BDMA * 4 * THREADS == B_SIZE && ADMA + BDMA < 16), "DMA stage");
     static_assert(LDS_BYTES + 1024 <= 160 * 1024, "LDS");
 };
 
@@ -187,6 +213,46 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_kernel(FixedParams p
     }
     const uint32_t kstep = (uint32_t)(KT * p.k_c);  // K elements per r-chunk
 
+    // DMA: this thread's granules, as byte offsets from the tile's A and from
+    // K; instruction j of a wave fills LDS slots (j * waves + wave) * 64 + lane
+    // of a stage. A pair past the end reads the tile's first pair, a row past
+    // the input its last row and a channel group past k_c the tile's first:
+    // all three only reach outputs that are never stored.
+    uint32_t adma[C::ADMA > 0 ? C::ADMA : 1], bdma[C::BDMA > 0 ? C::BDMA : 1];
+    if constexpr (C::kDMA) {
+#pragma unroll
+        for (int j = 0; j < C::ADMA; ++j) {
+            const int G = (j * C::kWaves + wave) * 64 + lane;
+            const int q = G >> 2, g = (G & 3) ^ ((q >> 2) & 3);
+            const int pp = q % kPairs, x = q / kPairs;
+            const int64_t ab = abase_s[pp] >= 0 ? abase_s[pp] : abase0;
+            const int64_t xr = x0 + x < p.i_h ? x0 + x : p.i_h - 1;
+            adma[j] = (uint32_t)(4 * (ab - abase0 + xr * p.a_xstride + g * 4));
+        }
+#pragma unroll
+        for (int j = 0; j < C::BDMA; ++j) {
+            const int G = (j * C::kWaves + wave) * 64 + lane;
+            const int q = G / (NT / 4), gc = G % (NT / 4);
+            const int r = q % KT, a = q / KT;
+            const int nc = n0 + 4 * gc < p.k_c ? n0 + 4 * gc : n0;
+            bdma[j] = (uint32_t)(4 * (((int64_t)a * p.R + r) * p.k_c + nc));
+        }
+    }
+    const uint32_t lds0 = (uint32_t)(size_t)(__attribute__((address_space(3))) uint32_t*)lds;
+    const uint32_t wave_u = (uint32_t)__builtin_amdgcn_readfirstlane(wave);
+    auto dma_a = [&](int rc, int sa) {
+        const uint32_t dst = lds0 + 4u * (uint32_t)(sa * A_SIZE) + wave_u * 1024u;
+        const uint32_t r0 = (uint32_t)rc * (4u * KT);
+#pragma unroll
+        for (int j = 0; j < C::ADMA; ++j) lds_dma16(Atile, adma[j] + r0, dst + (uint32_t)(j * C::kWaves) * 1024u);
+    };
+    auto dma_b = [&](int rc, int sb) {
+        const uint32_t dst = lds0 + 4u * (uint32_t)(3 * A_SIZE + sb * C::B_SIZE) + wave_u * 1024u;
+        const uint32_t r0 = (uint32_t)rc * (4u * KT) * (uint32_t)p.k_c;
+#pragma unroll
+        for (int j = 0; j < C::BDMA; ++j) lds_dma16(Kg, bdma[j] + r0, dst + (uint32_t)(j * C::kWaves) * 1024u);
+    };
+
     VecN<VA, uint32_t> areg[AJ][4];
     VecN<4, uint32_t> breg[BJ];
     // global -> registers for r-chunk rc, one load ("piece") at a time: pieces
@@ -272,6 +338,41 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_kernel(FixedParams p
     // the first one, to have as long as possible to land.
     constexpr int KS = KT / 2;                    // MFMA k-steps per chunk
     constexpr int KSL = (KH * HW * NBW >= 8 && KS > 1) ? KS / 2 : 1;  // k-steps that issue loads
+    // DMA: a lane's 16-byte A read of 8-r block kb is granule 2 * kb + kofs of
+    // its row, at its swizzled position; B row r = 8 * kb + 4 * kofs + j
+    const int a_drow = ((wh * HW * SH) * kPairs + row) * KT;
+    const int swz = (row >> 2) & 3;
+    const int b_dlane = 4 * kofs * NT + (wn * NBW) * 32 + row;
+    auto compute_dma = [&](int abuf, int bbuf) {
+        const uint32_t* As = lds + abuf * A_SIZE + a_drow;
+        const uint32_t* Bs = lds + 3 * A_SIZE + bbuf * C::B_SIZE + b_dlane;
+#pragma unroll
+        for (int kb = 0; kb < KT / 8; ++kb) {
+            uint4 af[XW];
+            const int ga = 4 * ((2 * kb + kofs) ^ swz);
+#pragma unroll
+            for (int i = 0; i < XW; ++i) af[i] = *reinterpret_cast<const uint4*>(As + i * kPairs * KT + ga);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                float bf[KH][NBW];
+#pragma unroll
+                for (int a = 0; a < KH; ++a)
+#pragma unroll
+                    for (int nb = 0; nb < NBW; ++nb)
+                        bf[a][nb] = __builtin_bit_cast(float, Bs[(a * KT + 8 * kb + j) * NT + nb * 32]);
+#pragma unroll
+                for (int a = 0; a < KH; ++a)
+#pragma unroll
+                    for (int hw = 0; hw < HW; ++hw) {
+                        const uint4& v = af[hw * SH + a];
+                        const float av = __builtin_bit_cast(float, j == 0 ? v.x : j == 1 ? v.y : j == 2 ? v.z : v.w);
+#pragma unroll
+                        for (int nb = 0; nb < NBW; ++nb)
+                            acc[hw][nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bf[a][nb], acc[hw][nb], 0, 0, 0);
+                    }
+            }
+        }
+    };
     auto compute = [&](int buf, auto issue) {
         const uint32_t* As = lds + buf * STAGE + a_lane;
         const uint32_t* Bs = lds + buf * STAGE + b_lane;
@@ -315,10 +416,43 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_kernel(FixedParams p
             __syncthreads();
         }
     };
-    if (full)
-        main_loop(std::true_type{});
-    else
-        main_loop(std::false_type{});
+    // DMA: as in the bf16 kernel, B chunk i + 1 goes out before A chunk i + 2,
+    // so waiting until only this wave's ADMA newest operations are outstanding
+    // completes chunk i + 1 and leaves A chunk i + 2 in flight; wait and
+    // barrier are one statement that no LDS access may cross.
+    auto sync_keep_a = [] {
+        asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(C::ADMA) : "memory");
+    };
+    auto sync_all = [] { asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
+    auto main_loop_dma = [&]() {
+        const int n = c_end - c_begin;
+        dma_b(c_begin, 0);
+        dma_a(c_begin, 0);
+        if (n > 1) {
+            dma_a(c_begin + 1, 1);
+            sync_keep_a();
+        } else {
+            sync_all();
+        }
+        for (int i = 0; i < n; ++i) {
+            const int rc = c_begin + i;
+            if (i + 1 < n) dma_b(rc + 1, (i + 1) & 1);
+            if (i + 2 < n) dma_a(rc + 2, (i + 2) % 3);
+            compute_dma(i % 3, i & 1);
+            if (i + 2 < n)
+                sync_keep_a();
+            else
+                sync_all();
+        }
+    };
+    if constexpr (C::kDMA) {
+        main_loop_dma();
+    } else {
+        if (full)
+            main_loop(std::true_type{});
+        else
+            main_loop(std::false_type{});
+    }
 
     const int64_t ostride_h = p.o_row;
     // split tiles: exactly two partial sums added to +0 in either order give
@@ -721,19 +855,6 @@ __device__ inline void transpose8x8_b16(const uint4 (&in)[8], uint4 (&out)[8]) {
         }
         out[c] = make_uint4(d[0], d[1], d[2], d[3]);
     }
-}
-
-// One 16-byte load per lane from base + voff straight into LDS at byte address
-// lds + 16 * lane (M0 holds the wave's LDS address; its previous value is put
-// back, since M0 cannot be declared clobbered). The compiler does not see the
-// load: the caller waits on vmcnt before the data is read.
-__device__ inline void lds_dma16(const void* base, uint32_t voff, uint32_t lds) {
-    uint32_t saved;
-    asm volatile(
-        "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %2, %3\n\ts_mov_b32 m0, %0"
-        : "=&s"(saved)
-        : "s"(lds), "v"(voff), "s"(base)
-        : "memory");
 }
 
 template <class C>
@@ -1139,9 +1260,9 @@ struct KernelOf<BF16Cfg<HT, NB, WH, KT, KH, SH, F, W, V, D>> {
     static constexpr auto fn = slab_gemm_bf16_kernel<BF16Cfg<HT, NB, WH, KT, KH, SH, F, W, V, D>>;
     static constexpr int threads = 64 * W;
 };
-template <int HT, int NB, int WH, int KT, int KH, int SH, int VA, int VB, bool F, int W>
-struct KernelOf<F32Cfg<HT, NB, WH, KT, KH, SH, VA, VB, F, W>> {
-    static constexpr auto fn = slab_gemm_f32_kernel<F32Cfg<HT, NB, WH, KT, KH, SH, VA, VB, F, W>>;
+template <int HT, int NB, int WH, int KT, int KH, int SH, int VA, int VB, bool F, int W, bool D>
+struct KernelOf<F32Cfg<HT, NB, WH, KT, KH, SH, VA, VB, F, W, D>> {
+    static constexpr auto fn = slab_gemm_f32_kernel<F32Cfg<HT, NB, WH, KT, KH, SH, VA, VB, F, W, D>>;
     static constexpr int threads = 64 * W;
 };
 
@@ -1245,6 +1366,8 @@ template <bool F> using F32K3S1StreamScalar = F32Cfg<8, 2, 4, 10, 3, 1, 1, 1, F>
 // fp32, 3x3 stride 1, long rows (R % 4 == 0): 32 pairs x 14 rows x 64 channels,
 // r-chunks of 16, 16-byte loads of L (or I) and K.
 template <bool F> using F32K3S1Wide = F32Cfg<14, 2, 2, 16, 3, 1, 4, 4, F>;
+// The same tile staged by direct-to-LDS loads (rows of a multiple of 16).
+template <bool F> using F32K3S1WideD = F32Cfg<14, 2, 2, 16, 3, 1, 4, 4, F, 4, true>;
 // the same with 4 and 2 output rows per tile, for layers whose few pair tiles
 // and small o_h would leave most compute units idle with 14-row tiles
 template <bool F> using F32K3S1Wide4 = F32Cfg<4, 2, 2, 16, 3, 1, 4, 4, F>;
@@ -1419,6 +1542,7 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
                 MEC_TRY_FIXED_SPLIT(F32K3S1Wide2<F>, tc.ksplit);
             }
             if (tc.ht == 4) MEC_TRY_FIXED_SPLIT(F32K3S1Wide4<F>, tc.ksplit);
+            MEC_TRY_FIXED_SPLIT(F32K3S1WideD<F>, tc.ksplit);
             MEC_TRY_FIXED_SPLIT(F32K3S1Wide<F>, tc.ksplit);
         }
         MEC_TRY_STREAM(F32K3S1Stream<F>);

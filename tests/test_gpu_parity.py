@@ -311,6 +311,28 @@ def test_split_reduction(orc, dims, algo):
 
 
 # bf16 3x3 layers with few tiles split their reduction the same way.
+# fp32 3x3 layers whose 14-row tiles are staged by direct-to-LDS loads (rows
+# of a multiple of 16): ragged pairs, rows and channel tiles.
+DMA_CASES_F32 = [
+    (33, 30, 29, 16, 3, 3, 72, 1, 1),    # 891 pairs, 28 rows, channels 64 + 8
+    (40, 60, 58, 32, 3, 3, 64, 1, 1),    # 2240 pairs, 58 rows (four 14-row tiles and one of 2)
+]
+
+
+@pytest.mark.parametrize("dims", DMA_CASES_F32)
+@pytest.mark.parametrize("algo", ["lowered", "fused"])
+def test_f32_direct_to_lds_tiles(orc, dims, algo):
+    say("f32 dma", algo, dims)
+    assert (dims[5] * dims[3]) % 16 == 0
+    s_h, s_w = dims[7], dims[8]
+    Ii, Ki = case(61 + sum(dims), dims, dist="int")
+    refi = orc.conv2d_direct(host(Ii), host(Ki), s_h, s_w)
+    assert np.abs(refi).max() < 2 ** 24
+    assert np.array_equal(run_conv(Ii, Ki, s_h, s_w, algo), refi.astype(np.float32))
+    I, K = case(67 + sum(dims), dims)
+    assert rel_l2(run_conv(I, K, s_h, s_w, algo), orc.conv2d_direct(host(I), host(K), s_h, s_w)) <= TOL_F32
+
+
 # bf16 3x3 tiles staged by direct-to-LDS loads (rows of a multiple of 32): the
 # 14-row form where its tiles fill at least 192 compute units, else 2 rows.
 DMA_CASES_BF16 = [
