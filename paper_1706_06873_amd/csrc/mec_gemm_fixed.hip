@@ -1372,6 +1372,8 @@ template <bool F> using F32K3S1WideD = F32Cfg<14, 2, 2, 16, 3, 1, 4, 4, F, 4, tr
 // and small o_h would leave most compute units idle with 14-row tiles
 template <bool F> using F32K3S1Wide4 = F32Cfg<4, 2, 2, 16, 3, 1, 4, 4, F>;
 template <bool F> using F32K3S1Wide2 = F32Cfg<2, 2, 2, 16, 3, 1, 4, 4, F>;
+template <bool F> using F32K3S1Wide4D = F32Cfg<4, 2, 2, 16, 3, 1, 4, 4, F, 4, true>;
+template <bool F> using F32K3S1Wide2D = F32Cfg<2, 2, 2, 16, 3, 1, 4, 4, F, 4, true>;
 // 2-row tiles with r-chunks of 32 where there is at most one workgroup per
 // compute unit: twice the MFMAs per global-load round trip (one wave per SIMD
 // by registers, so only where no second tile would share the compute unit;
@@ -1470,7 +1472,9 @@ bool split_shortens(const Shape& s, int ht, int nt, int kt) {
 // 14; resnet_mid 14). A split is only considered where it shortens the
 // busiest compute unit's chunk count, for 2-row tiles at most two per compute
 // unit unsplit: layers whose tiles leave compute units idle (cv11 12%, cv12
-// 38% faster; the batch-1 layers).
+// 38% faster; the batch-1 layers). The model was measured on the
+// register-staged tiles; their direct-to-LDS forms (R % 16 == 0) are faster
+// at each of its choices measured and take them over unchanged.
 struct TileChoice {
     int ht, ksplit;
 };
@@ -1535,13 +1539,19 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
             // no split into a strided layout: zeroing O would clear other pixels
             const TileChoice tc =
                 s.k_h == 3 && s.s_h == 1 ? pick_tiles_f32_3x3(s, layout == nullptr) : TileChoice{14, 1};
+            // the direct-to-LDS form of the chosen tile where R % 16 == 0 (faster
+            // at every row count measured: cv9-cv12 and their input gradients)
             if (tc.ht == 2) {
+                MEC_TRY_FIXED_SPLIT(F32K3S1Wide2D<F>, tc.ksplit);
                 const int64_t wgs = ((s.pairs + kPairs - 1) / kPairs) * ((s.o_h + 1) / 2) *
                                     ((s.k_c + 63) / 64) * tc.ksplit;
                 if (wgs <= 256) MEC_TRY_FIXED_SPLIT(F32K3S1Wide2L<F>, tc.ksplit);
                 MEC_TRY_FIXED_SPLIT(F32K3S1Wide2<F>, tc.ksplit);
             }
-            if (tc.ht == 4) MEC_TRY_FIXED_SPLIT(F32K3S1Wide4<F>, tc.ksplit);
+            if (tc.ht == 4) {
+                MEC_TRY_FIXED_SPLIT(F32K3S1Wide4D<F>, tc.ksplit);
+                MEC_TRY_FIXED_SPLIT(F32K3S1Wide4<F>, tc.ksplit);
+            }
             MEC_TRY_FIXED_SPLIT(F32K3S1WideD<F>, tc.ksplit);
             MEC_TRY_FIXED_SPLIT(F32K3S1Wide<F>, tc.ksplit);
         }
