@@ -7,8 +7,12 @@ L followed by the o_h slab products (mec_lower + mec_gemm, exactly the two
 kernels mec_conv2d(MEC_ALGO_LOWERED) enqueues), on inputs already resident in
 device memory. Buffers rotate over several sets so that the 256 MB
 memory-attached last-level cache cannot serve a step from the previous one.
-Timing: HIP events on the stream the kernels run on, around every kernel
-launch, plus events around the whole timed loop.
+Timing, with HIP events on the stream the kernels run on: the K timed steps
+run between two events with nothing else on the stream (ms_per_step, value);
+then the same K steps run again with an event around every kernel launch
+(the per-kernel durations of the rooflines). The events are created without
+the system-scope fence, so recording one between two launches adds no cache
+maintenance to the interval it measures.
 
 Prints ONE JSON line: effective TFLOP/s (2*MAC/time) of the whole step, the
 workspace bytes against im2col's, the roofline of the dominant kernel (the slab
@@ -16,6 +20,7 @@ products) and of the lowering, the fused variant's rate, and the CPU oracle's
 rate on the host cores (a baseline, not the target).
 """
 import argparse
+import ctypes
 import json
 import os
 import sys
@@ -28,6 +33,47 @@ METRIC = "effective conv TFLOP/s (2·MAC/time) + workspace bytes vs im2col, 1×M
 PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}   # dense MFMA peaks of the MI355X
 PEAK_HBM_GBS = 8000.0
 DEFAULT_LAYER = "resnet_mid"
+
+
+class HipEvent:
+    """A timing event of the process's HIP runtime, created with
+    hipEventDisableSystemFence (no system-scope acquire or release when it is
+    recorded; the timestamps are the same)."""
+
+    _rt = None
+    DISABLE_SYSTEM_FENCE = 0x20000000
+
+    def __init__(self, runtime_path):
+        if HipEvent._rt is None:
+            rt = ctypes.CDLL(runtime_path)
+            rt.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+            rt.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+            rt.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                               ctypes.c_void_p]
+            rt.hipEventDestroy.argtypes = [ctypes.c_void_p]
+            HipEvent._rt = rt
+        self.h = ctypes.c_void_p()
+        self._check(HipEvent._rt.hipEventCreateWithFlags(ctypes.byref(self.h), self.DISABLE_SYSTEM_FENCE),
+                    "hipEventCreateWithFlags")
+
+    @staticmethod
+    def _check(status, what):
+        if status != 0:
+            raise RuntimeError("%s failed with HIP status %d" % (what, status))
+
+    def record(self, stream):
+        self._check(HipEvent._rt.hipEventRecord(self.h, ctypes.c_void_p(stream.cuda_stream)),
+                    "hipEventRecord")
+
+    def elapsed_time(self, end):
+        ms = ctypes.c_float()
+        self._check(HipEvent._rt.hipEventElapsedTime(ctypes.byref(ms), self.h, end.h),
+                    "hipEventElapsedTime")
+        return ms.value
+
+    def __del__(self):
+        if HipEvent._rt is not None and self.h:
+            HipEvent._rt.hipEventDestroy(self.h)
 
 
 def parse():
@@ -175,22 +221,30 @@ def main():
         if ev:
             ev[2].record(stream)
 
+    runtimes = mec._hip_runtimes()
+    if len(runtimes) != 1:
+        raise RuntimeError("expected one HIP runtime in the process, found %r" % runtimes)
     with torch.cuda.stream(stream):
         for w in range(args.warmup):
             step(sets[w % len(sets)])
         torch.cuda.synchronize()
-        n_ev = 2 if args.algo == "fused" else 3
-        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n_ev)]
-               for _ in range(args.steps)]
-        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        # the timed steps: nothing on the stream but the steps themselves
+        start, end = HipEvent(runtimes[0]), HipEvent(runtimes[0])
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         start.record(stream)
         for k in range(args.steps):
-            step(sets[k % len(sets)], evs[k])
+            step(sets[k % len(sets)])
         end.record(stream)
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
+        # the same steps again, an event around every launch: per-kernel durations
+        n_ev = 2 if args.algo == "fused" else 3
+        evs = [[HipEvent(runtimes[0]) for _ in range(n_ev)] for _ in range(args.steps)]
+        torch.cuda.synchronize()
+        for k in range(args.steps):
+            step(sets[k % len(sets)], evs[k])
+        torch.cuda.synchronize()
 
     total_ms = start.elapsed_time(end)
     ms_per_step = total_ms / args.steps
