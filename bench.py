@@ -20,7 +20,6 @@ products) and of the lowering, the fused variant's rate, and the CPU oracle's
 rate on the host cores (a baseline, not the target).
 """
 import argparse
-import ctypes
 import json
 import os
 import sys
@@ -33,47 +32,6 @@ METRIC = "effective conv TFLOP/s (2·MAC/time) + workspace bytes vs im2col, 1×M
 PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}   # dense MFMA peaks of the MI355X
 PEAK_HBM_GBS = 8000.0
 DEFAULT_LAYER = "resnet_mid"
-
-
-class HipEvent:
-    """A timing event of the process's HIP runtime, created with
-    hipEventDisableSystemFence (no system-scope acquire or release when it is
-    recorded; the timestamps are the same)."""
-
-    _rt = None
-    DISABLE_SYSTEM_FENCE = 0x20000000
-
-    def __init__(self, runtime_path):
-        if HipEvent._rt is None:
-            rt = ctypes.CDLL(runtime_path)
-            rt.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
-            rt.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
-            rt.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
-                                               ctypes.c_void_p]
-            rt.hipEventDestroy.argtypes = [ctypes.c_void_p]
-            HipEvent._rt = rt
-        self.h = ctypes.c_void_p()
-        self._check(HipEvent._rt.hipEventCreateWithFlags(ctypes.byref(self.h), self.DISABLE_SYSTEM_FENCE),
-                    "hipEventCreateWithFlags")
-
-    @staticmethod
-    def _check(status, what):
-        if status != 0:
-            raise RuntimeError("%s failed with HIP status %d" % (what, status))
-
-    def record(self, stream):
-        self._check(HipEvent._rt.hipEventRecord(self.h, ctypes.c_void_p(stream.cuda_stream)),
-                    "hipEventRecord")
-
-    def elapsed_time(self, end):
-        ms = ctypes.c_float()
-        self._check(HipEvent._rt.hipEventElapsedTime(ctypes.byref(ms), self.h, end.h),
-                    "hipEventElapsedTime")
-        return ms.value
-
-    def __del__(self):
-        if HipEvent._rt is not None and self.h:
-            HipEvent._rt.hipEventDestroy(self.h)
 
 
 def parse():
@@ -221,15 +179,13 @@ def main():
         if ev:
             ev[2].record(stream)
 
-    runtimes = mec._hip_runtimes()
-    if len(runtimes) != 1:
-        raise RuntimeError("expected one HIP runtime in the process, found %r" % runtimes)
+    from paper_1706_06873_amd.timing import HipEvent
     with torch.cuda.stream(stream):
         for w in range(args.warmup):
             step(sets[w % len(sets)])
         torch.cuda.synchronize()
         # the timed steps: nothing on the stream but the steps themselves
-        start, end = HipEvent(runtimes[0]), HipEvent(runtimes[0])
+        start, end = HipEvent(), HipEvent()
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         start.record(stream)
@@ -240,7 +196,7 @@ def main():
         wall = time.perf_counter() - t0
         # the same steps again, an event around every launch: per-kernel durations
         n_ev = 2 if args.algo == "fused" else 3
-        evs = [[HipEvent(runtimes[0]) for _ in range(n_ev)] for _ in range(args.steps)]
+        evs = [[HipEvent() for _ in range(n_ev)] for _ in range(args.steps)]
         torch.cuda.synchronize()
         for k in range(args.steps):
             step(sets[k % len(sets)], evs[k])

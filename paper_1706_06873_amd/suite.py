@@ -36,6 +36,7 @@ import torch
 
 import paper_1706_06873_amd as mec
 from paper_1706_06873_amd import workloads as wl
+from paper_1706_06873_amd.timing import HipEvent
 
 
 def _time_layer(layer, reps, warmup, sets, yardstick=False):
@@ -83,7 +84,7 @@ def _time_layer(layer, reps, warmup, sets, yardstick=False):
             for w in range(warmup):
                 run(bufs[w % sets])
             torch.cuda.synchronize()
-            evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(reps)]
+            evs = [[HipEvent() for _ in range(3)] for _ in range(reps)]
             for r in range(reps):
                 run(bufs[r % sets], evs[r])
             torch.cuda.synchronize()
@@ -103,7 +104,7 @@ def _time_layer(layer, reps, warmup, sets, yardstick=False):
                 for _ in range(warmup):
                     torch.matmul(Mv, Kv)
                 torch.cuda.synchronize()
-                gev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(reps)]
+                gev = [[HipEvent() for _ in range(2)] for _ in range(reps)]
                 for r in range(reps):
                     gev[r][0].record(stream)
                     torch.matmul(Mv, Kv)
@@ -167,7 +168,7 @@ def _time_train(layer, reps, warmup, yardstick):
             for _ in range(warmup):
                 fn()
             torch.cuda.synchronize()
-            ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            ev = [(HipEvent(), HipEvent())
                   for _ in range(reps)]
             for a, b in ev:
                 a.record(stream)
