@@ -1399,6 +1399,8 @@ template <bool F> using F32K2S1Wide = F32Cfg<8, 2, 2, 16, 2, 1, 4, 4, F>;
 template <bool F> using F32K4S1Wide = F32Cfg<8, 2, 2, 16, 4, 1, 4, 4, F>;
 // fp32, 5x5 stride 1: 32 pairs x 4 rows (8 staged rows) x 64 channels.
 template <bool F> using F32K5S1Wide = F32Cfg<4, 2, 2, 16, 5, 1, 4, 4, F>;
+// direct-to-LDS staging: 2.4% faster from I on cv5, 1% slower from L
+template <bool F> using F32K5S1WideD = F32Cfg<4, 2, 2, 16, 5, 1, 4, 4, F, 4, true>;
 template <bool F> using F32K5S1Narrow = F32Cfg<4, 2, 2, 4, 5, 1, 1, 4, F>;
 template <bool F> using F32K5S1Scalar = F32Cfg<4, 2, 2, 4, 5, 1, 1, 1, F>;
 // k_h = 1, stride 1: plain products with no slab overlap (1x1 convolutions,
@@ -1420,6 +1422,7 @@ template <bool F> using BF16K3S1R2D = BF16Cfg<2, 4, 2, 32, 3, 1, F, 8, true, tru
 // bf16, 5x5 stride 1 (8 staged rows, r-chunks of 32) and 7x7 stride 2 (13
 // staged rows, r-chunks of 16): 32 pairs x 4 rows x 128 channels.
 template <bool F> using BF16K5S1 = BF16Cfg<4, 4, 2, 32, 5, 1, F, 8>;
+template <bool F> using BF16K5S1D = BF16Cfg<4, 4, 2, 32, 5, 1, F, 8, true, true>;
 template <bool F> using BF16K7S2 = BF16Cfg<4, 4, 2, 16, 7, 2, F, 8>;
 // bf16, 11x11 stride 4 over few channels (rows of 33 elements, gathered element
 // by element): 32 pairs x 2 rows (15 staged rows) x 96 channels, r-chunks of 16.
@@ -1562,6 +1565,7 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
         MEC_TRY_FIXED(F32K7S2Wide<F>);
         MEC_TRY_FIXED(F32K7S2Narrow<F>);
         MEC_TRY_FIXED(F32K7S2Scalar<F>);
+        if (F) MEC_TRY_FIXED(F32K5S1WideD<F>);
         MEC_TRY_FIXED(F32K5S1Wide<F>);
         MEC_TRY_FIXED(F32K2S1Wide<F>);
         MEC_TRY_FIXED(F32K4S1Wide<F>);
@@ -1599,6 +1603,7 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
             MEC_TRY_FIXED_SPLIT(BF16K3S1D<F>, ks);
             MEC_TRY_FIXED_SPLIT(BF16K3S1<F>, ks);
         }
+        MEC_TRY_FIXED(BF16K5S1D<F>);
         MEC_TRY_FIXED(BF16K5S1<F>);
         MEC_TRY_FIXED(BF16K7S2<F>);
         MEC_TRY_FIXED(BF16K11S4<F>);

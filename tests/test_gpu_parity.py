@@ -311,11 +311,13 @@ def test_split_reduction(orc, dims, algo):
 
 
 # bf16 3x3 layers with few tiles split their reduction the same way.
-# fp32 3x3 layers whose 14-row tiles are staged by direct-to-LDS loads (rows
-# of a multiple of 16): ragged pairs, rows and channel tiles.
+# fp32 layers whose tiles are staged by direct-to-LDS loads (rows of a
+# multiple of 16): 3x3 14-row tiles, and 5x5 tiles from I; ragged pairs, rows
+# and channel tiles.
 DMA_CASES_F32 = [
     (33, 30, 29, 16, 3, 3, 72, 1, 1),    # 891 pairs, 28 rows, channels 64 + 8
     (40, 60, 58, 32, 3, 3, 64, 1, 1),    # 2240 pairs, 58 rows (four 14-row tiles and one of 2)
+    (3, 17, 21, 32, 5, 5, 72, 1, 1),     # 5x5 (from I only): ragged pairs, rows, channels
 ]
 
 
@@ -333,12 +335,14 @@ def test_f32_direct_to_lds_tiles(orc, dims, algo):
     assert rel_l2(run_conv(I, K, s_h, s_w, algo), orc.conv2d_direct(host(I), host(K), s_h, s_w)) <= TOL_F32
 
 
-# bf16 3x3 tiles staged by direct-to-LDS loads (rows of a multiple of 32): the
-# 14-row form where its tiles fill at least 192 compute units, else 2 rows.
+# bf16 tiles staged by direct-to-LDS loads (rows of a multiple of 32): 3x3 in
+# the 14-row form where its tiles fill at least 192 compute units, else 2
+# rows; 5x5.
 DMA_CASES_BF16 = [
     (95, 20, 19, 32, 3, 3, 136, 1, 1),   # 14 rows: 204 tiles; ragged pairs (1615), rows (18), channels
     (3, 13, 11, 64, 3, 3, 72, 1, 1),     # 2 rows: ragged pairs, odd row count, one ragged channel tile
     (2, 9, 10, 128, 3, 3, 264, 1, 1),    # 2 rows: three channel tiles, the last 8 wide
+    (3, 17, 21, 32, 5, 5, 72, 1, 1),     # 5x5: ragged pairs, rows, channels
 ]
 
 
