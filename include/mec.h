@@ -116,9 +116,12 @@ int mec_lower(const void* I, void* L,
  * final transposition nor the |O| <= |L| condition applies. L must hold the
  * output of mec_lower for the same arguments. O must not overlap L or K.
  * Results are reproducible run to run: each output's summation order is fixed
- * by the shape. (For fp32 3x3 layers whose tiles leave compute units idle, each
- * tile's reduction is split in two halves that are added into O after O is
- * zeroed; two partial sums added to zero commute exactly.)
+ * by the shape and by whether L, K and O are 16-byte aligned (alignment selects
+ * the staging path, and fp32 tiles staged straight into LDS sum their products
+ * in another order, within rounding of the others). (For 3x3 layers whose
+ * tiles leave compute units idle, each tile's reduction is split in two halves
+ * that are added into O after O is zeroed; two partial sums added to zero
+ * commute exactly.)
  * Returns MEC_OK or a negative status. */
 int mec_gemm(const void* L, const void* K, float* O,
              int i_n, int i_h, int i_w, int i_c,
