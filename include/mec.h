@@ -254,7 +254,12 @@ int mec_wgrad_gemm(const void* L, const float* G, float* dK,
 
 /* dK = dloss/dK from I: mec_lower into the start of `workspace`, then
  * mec_wgrad_gemm with the rest of it (mec_grad_workspace_bytes(...,
- * MEC_GRAD_KERNEL) in all). Returns MEC_OK or a negative status. */
+ * MEC_GRAD_KERNEL) in all). Where the short-row products apply (k_h = 1, 3 or
+ * 5, R = k_w*i_c a multiple of 4 and at least 48, R <= 256 or k_h = 5, and
+ * 3*s_h + k_h <= 8) they read the rows of L straight from I instead, as
+ * L[n*o_w + w, x, r] = I[n, x, s_w*w*i_c + r], and the L part of the workspace
+ * is left unused; dK is the same either way. Returns MEC_OK or a negative
+ * status. */
 int mec_conv2d_wgrad(const void* I, const float* G, float* dK,
                      void* workspace, size_t workspace_bytes,
                      int i_n, int i_h, int i_w, int i_c,

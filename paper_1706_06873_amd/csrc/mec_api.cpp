@@ -315,6 +315,11 @@ int mec_conv2d_wgrad(const void* I, const float* G, float* dK, void* workspace,
     float* Lw = static_cast<float*>(workspace);
     float* part = reinterpret_cast<float*>(static_cast<char*>(workspace) + lreg);
     clear_stale_error();
+    // the slab kernel reads L's rows straight from I: no lowering pass (the L
+    // part of the workspace then goes unused)
+    if (mec::wgrad_fused_ok(s))
+        return hip_status(mec::launch_wgrad(s, static_cast<const float*>(I), G, part, dK, st, true),
+                          "wgrad products from I");
     rc = hip_status(mec::launch_lower(s, I, Lw, 4, st), "lowering");
     if (rc != MEC_OK) return rc;
     return hip_status(mec::launch_wgrad(s, Lw, G, part, dK, st), "wgrad products");

@@ -270,7 +270,7 @@ constexpr int kWgA4 = kWgC * kWgJT / 4 / kGradThreads;  // float4 of the A stage
 constexpr int kWgB4 = kWgC * kWgMT / 4 / kGradThreads;  // float4 of the B stage per thread
 
 struct WgradParams {
-    const float* L;
+    const float* L;   // L, or I when fused (the slab kernel only)
     const float* G;
     float* part;      // splits x KD x k_c partial sums
     int32_t i_h, o_h, o_w, k_c, s_h, R, KD, pairs;
@@ -281,6 +281,8 @@ struct WgradParams {
     uint32_t ntiles;
     int32_t lvec;      // L loads as 16-byte vectors (R % 4 == 0, L aligned)
     int32_t gvec;      // G loads as 16-byte vectors (k_c % 4 == 0, G aligned)
+    int32_t fused;     // slab kernel: row (n*o_w + w, x) of L read from I
+    int32_t i_w, i_c, s_w;
     FastDiv div_ow;
 };
 
@@ -445,7 +447,15 @@ __global__ __launch_bounds__(kGradThreads) void wgrad_slab_kernel(WgradParams p)
                 const int x = rem / (kWs / 4), r = r0 + (rem - x * (kWs / 4)) * 4;
                 const int pair = pc * kWgPT + pp;
                 if (pair < p.pairs && x0 + x < p.i_h) {
-                    const float* src = p.L + ((int64_t)pair * p.i_h + x0 + x) * p.R + r;
+                    // L[n*o_w + w][x][r] = I[n][x][s_w*w*i_c + r] (the lowering's definition)
+                    int64_t base;
+                    if (p.fused) {
+                        const int n = (int)p.div_ow.div((uint32_t)pair), w = pair - n * p.o_w;
+                        base = (((int64_t)n * p.i_h + x0 + x) * p.i_w + (int64_t)p.s_w * w) * p.i_c;
+                    } else {
+                        base = ((int64_t)pair * p.i_h + x0 + x) * p.R;
+                    }
+                    const float* src = p.L + base + r;
                     if (VEC) {
                         if (r < p.R) v = *reinterpret_cast<const f32x4*>(src);
                     } else {
@@ -798,10 +808,17 @@ bool wgrad_supported(const Shape& s) {
            wgrad_tiles(s) * wgrad_splits(s) < (int64_t(1) << 31);
 }
 
+bool wgrad_fused_ok(const Shape& s) { return wgrad_slab_ok(s); }
+
 hipError_t launch_wgrad(const Shape& s, const float* L, const float* G, float* part, float* dK,
-                        hipStream_t stream) {
+                        hipStream_t stream, bool fused) {
+    if (fused && !wgrad_fused_ok(s)) return hipErrorNotSupported;
     WgradParams p{};
     p.L = L;
+    p.fused = fused;
+    p.i_w = (int32_t)s.i_w;
+    p.i_c = (int32_t)s.i_c;
+    p.s_w = (int32_t)s.s_w;
     p.G = G;
     p.part = part;
     p.i_h = (int32_t)s.i_h;
@@ -815,7 +832,7 @@ hipError_t launch_wgrad(const Shape& s, const float* L, const float* G, float* p
     p.h_chunks = (int32_t)((s.o_h + kWgHT - 1) / kWgHT);
     p.nstages = (int32_t)wgrad_stages(s);
     p.splits = (int32_t)wgrad_splits(s);
-    p.lvec = s.R % 4 == 0 && aligned16(L);
+    p.lvec = s.R % 4 == 0 && aligned16(L) && (!fused || s.i_c % 4 == 0);
     p.gvec = s.k_c % 4 == 0 && aligned16(G);
     p.div_ow = FastDiv((uint32_t)s.o_w);
     if (wgrad_slab_ok(s)) {
