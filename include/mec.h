@@ -185,8 +185,8 @@ int mec_conv2d(const void* I, const void* K, float* O,
  *   Ny = ceil((i_h - py)/s_h), Nx = ceil((i_w - px)/s_w) (stride 1: one phase,
  *   G' of (o_h + 2(k_h-1)) x (o_w + 2(k_w-1)) pixels); otherwise dL in fp32,
  *   |L| * 4 bytes exactly.
- * MEC_GRAD_KERNEL: mec_conv2d_wgrad -- L (|L| * 4 bytes, rounded up to 256)
- *   followed by the partial sums of dK.
+ * MEC_GRAD_KERNEL: mec_conv2d_wgrad -- the partial sums of dK only (its
+ *   products read the rows of L straight from I): as MEC_GRAD_KERNEL_FROM_L.
  * MEC_GRAD_KERNEL_FROM_L: mec_wgrad_gemm -- the partial sums of dK only:
  *   s * k_h*k_w*i_c*k_c * 4 bytes, s (1 <= s <= 1024) fixed by the shape. */
 enum mec_grad_pass { MEC_GRAD_INPUT = 0, MEC_GRAD_KERNEL = 1, MEC_GRAD_KERNEL_FROM_L = 2 };
@@ -252,14 +252,11 @@ int mec_wgrad_gemm(const void* L, const float* G, float* dK,
                    int k_h, int k_w, int k_c, int s_h, int s_w,
                    int dtype, void* stream);
 
-/* dK = dloss/dK from I: mec_lower into the start of `workspace`, then
- * mec_wgrad_gemm with the rest of it (mec_grad_workspace_bytes(...,
- * MEC_GRAD_KERNEL) in all). Where the short-row products apply (k_h = 1, 3 or
- * 5, R = k_w*i_c a multiple of 4 and at least 48, R <= 256 or k_h = 5, and
- * 3*s_h + k_h <= 8) they read the rows of L straight from I instead, as
- * L[n*o_w + w, x, r] = I[n, x, s_w*w*i_c + r], and the L part of the workspace
- * is left unused; dK is the same either way. Returns MEC_OK or a negative
- * status. */
+/* dK = dloss/dK from I: the products of mec_wgrad_gemm with the rows of L
+ * read straight from I, L[n*o_w + w, x, r] = I[n, x, s_w*w*i_c + r], so no
+ * lowered copy is made; `workspace` holds the partial sums
+ * (mec_grad_workspace_bytes(..., MEC_GRAD_KERNEL)). dK is bit-identical to
+ * mec_wgrad_gemm on mec_lower's L. Returns MEC_OK or a negative status. */
 int mec_conv2d_wgrad(const void* I, const float* G, float* dK,
                      void* workspace, size_t workspace_bytes,
                      int i_n, int i_h, int i_w, int i_c,

@@ -201,9 +201,6 @@ int mec_conv2d(const void* I, const void* K, float* O, void* workspace, size_t w
 
 namespace {
 
-// Start of the partial sums inside a MEC_GRAD_KERNEL workspace.
-int64_t wgrad_l_region(const mec::Shape& s) { return (lowered_elems(s) * 4 + 255) / 256 * 256; }
-
 // Common checks of the training entry points: shape, dtype (fp32 only),
 // and the 32-bit index ranges of the kernels.
 int grad_shape(mec::Shape& s, int i_n, int i_h, int i_w, int i_c, int k_h, int k_w, int k_c,
@@ -225,7 +222,7 @@ int64_t mec_grad_workspace_bytes(int i_n, int i_h, int i_w, int i_c, int k_h, in
     if (rc != MEC_OK) return rc;
     switch (pass) {
         case MEC_GRAD_INPUT: return mec::dgrad_workspace_bytes(s);
-        case MEC_GRAD_KERNEL: return wgrad_l_region(s) + mec::wgrad_partial_bytes(s);
+        case MEC_GRAD_KERNEL:  // the products read L's rows from I: partial sums only
         case MEC_GRAD_KERNEL_FROM_L: return mec::wgrad_partial_bytes(s);
         default: return MEC_ERR_INVALID_ARG;
     }
@@ -306,23 +303,15 @@ int mec_conv2d_wgrad(const void* I, const float* G, float* dK, void* workspace,
     if (!I || !G || !dK) return MEC_ERR_INVALID_ARG;
     if (!aligned(I, 4) || !aligned(G, 4) || !aligned(dK, 4)) return MEC_ERR_ALIGNMENT;
     if (!mec::wgrad_supported(s)) return MEC_ERR_UNSUPPORTED;
-    const int64_t lreg = wgrad_l_region(s);
-    if (!workspace ||
-        (uint64_t)workspace_bytes < (uint64_t)(lreg + mec::wgrad_partial_bytes(s)))
+    if (!workspace || (uint64_t)workspace_bytes < (uint64_t)mec::wgrad_partial_bytes(s))
         return MEC_ERR_WORKSPACE;
     if (!aligned(workspace, 4)) return MEC_ERR_ALIGNMENT;
     const hipStream_t st = (hipStream_t)stream;
-    float* Lw = static_cast<float*>(workspace);
-    float* part = reinterpret_cast<float*>(static_cast<char*>(workspace) + lreg);
+    float* part = static_cast<float*>(workspace);
     clear_stale_error();
-    // the slab kernel reads L's rows straight from I: no lowering pass (the L
-    // part of the workspace then goes unused)
-    if (mec::wgrad_fused_ok(s))
-        return hip_status(mec::launch_wgrad(s, static_cast<const float*>(I), G, part, dK, st, true),
-                          "wgrad products from I");
-    rc = hip_status(mec::launch_lower(s, I, Lw, 4, st), "lowering");
-    if (rc != MEC_OK) return rc;
-    return hip_status(mec::launch_wgrad(s, Lw, G, part, dK, st), "wgrad products");
+    // the products read L's rows straight from I: no lowering pass
+    return hip_status(mec::launch_wgrad(s, static_cast<const float*>(I), G, part, dK, st, true),
+                      "wgrad products from I");
 }
 
 const char* mec_strerror(int status) {

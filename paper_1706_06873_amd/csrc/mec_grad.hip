@@ -270,7 +270,7 @@ constexpr int kWgA4 = kWgC * kWgJT / 4 / kGradThreads;  // float4 of the A stage
 constexpr int kWgB4 = kWgC * kWgMT / 4 / kGradThreads;  // float4 of the B stage per thread
 
 struct WgradParams {
-    const float* L;   // L, or I when fused (the slab kernel only)
+    const float* L;   // L, or I when fused
     const float* G;
     float* part;      // splits x KD x k_c partial sums
     int32_t i_h, o_h, o_w, k_c, s_h, R, KD, pairs;
@@ -281,9 +281,10 @@ struct WgradParams {
     uint32_t ntiles;
     int32_t lvec;      // L loads as 16-byte vectors (R % 4 == 0, L aligned)
     int32_t gvec;      // G loads as 16-byte vectors (k_c % 4 == 0, G aligned)
-    int32_t fused;     // slab kernel: row (n*o_w + w, x) of L read from I
+    int32_t fused;     // the rows of L read from I: L[n*o_w + w, x, r] = I[n, x, s_w*w*i_c + r]
     int32_t i_w, i_c, s_w;
     FastDiv div_ow;
+    FastDiv div_R;     // fused wgrad_kernel: j -> (kernel row, r)
 };
 
 __global__ __launch_bounds__(kGradThreads) void wgrad_kernel(WgradParams p) {
@@ -311,7 +312,23 @@ __global__ __launch_bounds__(kGradThreads) void wgrad_kernel(WgradParams p) {
             const int pair = pc * kWgPT + (cidx >> 2), h = hc * kWgHT + (cidx & 3);
             const int j = j0 + jq;
             f32x4 v = {0.f, 0.f, 0.f, 0.f};
-            if (pair < p.pairs && h < p.o_h) {
+            if (pair < p.pairs && h < p.o_h && p.fused) {
+                // j = a*R + r of this (pair, h): I[n, h*s_h + a, s_w*w*i_c + r]; with
+                // R % 4 == 0 the four j of a vector stay in one kernel row
+                const int n = (int)p.div_ow.div((uint32_t)pair), w = pair - n * p.o_w;
+                const int64_t pix = ((int64_t)n * p.i_h + (int64_t)h * p.s_h) * p.i_w + (int64_t)p.s_w * w;
+                auto at = [&](int jj) {
+                    const int a = (int)p.div_R.div((uint32_t)jj);
+                    return p.L + (pix + (int64_t)a * p.i_w) * p.i_c + (jj - a * p.R);
+                };
+                if (p.lvec && j + 3 < p.KD) {
+                    v = *reinterpret_cast<const f32x4*>(at(j));
+                } else {
+#pragma unroll
+                    for (int k = 0; k < 4; ++k)
+                        if (j + k < p.KD) v[k] = *at(j + k);
+                }
+            } else if (pair < p.pairs && h < p.o_h) {
                 const float* src = p.L + ((int64_t)pair * p.i_h + (int64_t)h * p.s_h) * p.R + j;
                 if (p.lvec && j + 3 < p.KD) {
                     v = *reinterpret_cast<const f32x4*>(src);
@@ -808,11 +825,8 @@ bool wgrad_supported(const Shape& s) {
            wgrad_tiles(s) * wgrad_splits(s) < (int64_t(1) << 31);
 }
 
-bool wgrad_fused_ok(const Shape& s) { return wgrad_slab_ok(s); }
-
 hipError_t launch_wgrad(const Shape& s, const float* L, const float* G, float* part, float* dK,
                         hipStream_t stream, bool fused) {
-    if (fused && !wgrad_fused_ok(s)) return hipErrorNotSupported;
     WgradParams p{};
     p.L = L;
     p.fused = fused;
@@ -835,6 +849,7 @@ hipError_t launch_wgrad(const Shape& s, const float* L, const float* G, float* p
     p.lvec = s.R % 4 == 0 && aligned16(L) && (!fused || s.i_c % 4 == 0);
     p.gvec = s.k_c % 4 == 0 && aligned16(G);
     p.div_ow = FastDiv((uint32_t)s.o_w);
+    p.div_R = FastDiv((uint32_t)s.R);
     if (wgrad_slab_ok(s)) {
         p.j_tiles = (int32_t)((s.R + kWs - 1) / kWs);
         p.m_tiles = (int32_t)((s.k_c + kWs - 1) / kWs);

@@ -133,9 +133,7 @@ hipError_t launch_fold(const Shape& s, const float* dL, float* dI, hipStream_t s
 bool wgrad_supported(const Shape& s);
 int64_t wgrad_splits(const Shape& s);
 int64_t wgrad_partial_bytes(const Shape& s);
-// fused: the slab kernel reads the rows of L from I (L = I then), see
-// wgrad_fused_ok.
-bool wgrad_fused_ok(const Shape& s);
+// fused: the kernels read the rows of L from I (the L argument is I then).
 hipError_t launch_wgrad(const Shape& s, const float* L, const float* G, float* part, float* dK,
                         hipStream_t stream, bool fused = false);
 
