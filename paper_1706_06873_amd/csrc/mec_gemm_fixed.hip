@@ -1447,11 +1447,13 @@ int pick_rows(const Shape& s, int nt, std::initializer_list<int> rows) {
     return best;
 }
 
-// bf16 3x3 tiles (one workgroup per compute unit): split a tile's r-chunks
-// between two workgroups only where that shortens the busiest compute unit's
-// chunk count, the tiles are 2-row tiles at most two per compute unit
-// unsplit, and each half keeps at least 4 chunks (the small deep layers, e.g.
-// cv12: 60 tiles of 48 chunks on 256 compute units).
+// bf16 3x3 tiles: split a tile's r-chunks between two workgroups only where
+// that shortens the busiest compute unit's chunk count (counted at one
+// workgroup per compute unit), the tiles are 2-row tiles at most two per
+// compute unit unsplit, and each half keeps at least 4 chunks (the small deep
+// layers, e.g. cv12: 60 tiles of 48 chunks on 256 compute units). Measured
+// on the register-staged tiles; the direct-to-LDS ones add a bound on the
+// output size at the call.
 bool split_shortens(const Shape& s, int ht, int nt, int kt) {
     const int64_t nchunks = (s.R + kt - 1) / kt;
     if (nchunks < 8) return false;
