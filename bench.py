@@ -1,23 +1,34 @@
 """Benchmark of the MEC hot path on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--layer NAME] [--algo lowered|fused]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--layer NAME] [--algo lowered|fused|im2col]
+                    [--sweep all|none]
 
-One step is one MEC convolution of the layer: the compact lowering of I into
-L followed by the o_h slab products (mec_lower + mec_gemm, exactly the two
-kernels mec_conv2d(MEC_ALGO_LOWERED) enqueues), on inputs already resident in
-device memory. Buffers rotate over several sets so that the 256 MB
-memory-attached last-level cache cannot serve a step from the previous one.
-Timing, with HIP events on the stream the kernels run on: the K timed steps
-run between two events with nothing else on the stream (ms_per_step, value);
-then the same K steps run again with an event around every kernel launch
-(the per-kernel durations of the rooflines). The events are created without
-the system-scope fence, so recording one between two launches adds no cache
-maintenance to the interval it measures.
+One step is one MEC convolution of the layer on inputs already resident in
+device memory: the compact lowering of I into L followed by the o_h slab
+products (mec_lower + mec_gemm, exactly the two kernels
+mec_conv2d(MEC_ALGO_LOWERED) enqueues), or the fused kernel
+(mec_conv2d(MEC_ALGO_FUSED)). The default layer is the largest fp32 one,
+AlexNet conv1 (i_n=128, 227x227x3, 11x11x96 kernel, stride 4), from L.
+Buffers rotate over several sets so that the 256 MB memory-attached
+last-level cache cannot serve a step from the previous one.
+
+Timing, with HIP events on the stream the kernels run on (created without the
+system-scope fence, so recording one adds no cache maintenance to what it
+measures):
+  * untimed steps for --settle seconds (the GPU's clocks leave their idle
+    state), then the W warm-up steps;
+  * the K timed steps run between two events with nothing else on the stream
+    (ms_per_step, value);
+  * each kernel's duration is then timed on its own: K launches of that one
+    kernel back to back between two events (the per-kernel averages of the
+    rooflines), the lowering first so that the products read a lowered L.
 
 Prints ONE JSON line: effective TFLOP/s (2*MAC/time) of the whole step, the
 workspace bytes against im2col's, the roofline of the dominant kernel (the slab
-products) and of the lowering, the fused variant's rate, and the CPU oracle's
-rate on the host cores (a baseline, not the target).
+products) and of the lowering, the CPU oracle's rate on the host cores (a
+baseline, not the target) and, under "configs", the same step and per-kernel
+figures for every synthetic layer (tiny, resnet_mid, vgg_first, alexnet_conv1,
+deep_bf16), each from L and fused.
 """
 import argparse
 import json
@@ -31,7 +42,9 @@ sys.path.insert(0, REPO)
 METRIC = "effective conv TFLOP/s (2·MAC/time) + workspace bytes vs im2col, 1×MI355X"
 PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}   # dense MFMA peaks of the MI355X
 PEAK_HBM_GBS = 8000.0
-DEFAULT_LAYER = "resnet_mid"
+DEFAULT_LAYER = "alexnet_conv1"
+MIN_ROTATION_BYTES = 1 << 30   # bytes each kernel's rotating buffers span, at least
+SWEEP_ALGOS = ("lowered", "fused")
 
 
 def parse():
@@ -39,10 +52,15 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--settle", type=float, default=0.3,
+                    help="seconds of untimed steps before the warm-up steps (clocks leave idle)")
     ap.add_argument("--layer", default=DEFAULT_LAYER)
     ap.add_argument("--algo", default="lowered", choices=["lowered", "fused", "im2col"],
                     help="MEC from L (default), MEC fused, or the im2col + product baseline")
-    ap.add_argument("--sets", type=int, default=4, help="rotating buffer sets")
+    ap.add_argument("--sweep", default="all", choices=["all", "none"],
+                    help="also time every synthetic layer from L and fused (default), or not")
+    ap.add_argument("--sets", type=int, default=4,
+                    help="rotating buffer sets, at least (more where a kernel's buffers are small)")
     ap.add_argument("--batch", type=int, default=0,
                     help="override the layer's batch size i_n (0 keeps the layer's own)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
@@ -50,10 +68,6 @@ def parse():
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after timing, run one plain device-to-device copy of this many MiB "
                          "(a known-size reference for rocprofv3 byte counters)")
-    ap.add_argument("--traffic", default=None,
-                    help="profile summary holding the slab-product kernel's per-launch HBM "
-                         "bytes from rocprofv3 counters (default: profiles/slab_gemm_<dtype>_<layer>_"
-                         "<algo>_traffic.md when present)")
     return ap.parse_args()
 
 
@@ -80,25 +94,199 @@ def csrc_digest():
     return h.hexdigest()
 
 
-def load_traffic(path, kdt, layer_name, algo):
-    """Per-launch HBM bytes of the slab-product kernel from a profile summary:
-    the line starting with 'traffic-json:' holds FETCH_SIZE and WRITE_SIZE (KiB
-    per dispatch), the factors that make each counter read a plain copy of known
-    size correctly, and the digest of the sources the counters were taken on."""
-    if path is None:
-        path = os.path.join(REPO, "profiles", "slab_gemm_%s_%s_%s_traffic.md" % (kdt, layer_name, algo))
+def profile_path(dtype, layer_name, algo):
+    return os.path.join(REPO, "profiles", "slab_gemm_%s_%s_%s.md" % (dtype, layer_name, algo))
+
+
+def load_traffic(dtype, layer_name, algo, digest):
+    """Per-launch HBM bytes of the slab products and of the lowering from the
+    layer's profile summary: its lines 'traffic-json:' (products) and
+    'traffic-lower-json:' (lowering) hold FETCH_SIZE and WRITE_SIZE (KiB per
+    dispatch), the factors that make each counter read a plain copy of known
+    size correctly, and the digest of the sources the counters were taken on.
+    A figure taken on other sources is not reported (None)."""
+    path = profile_path(dtype, layer_name, algo)
+    out = {"products": None, "lower": None}
     if not os.path.exists(path):
-        return None
+        return out
     with open(path) as f:
         for line in f:
-            if line.startswith("traffic-json:"):
-                t = json.loads(line[len("traffic-json:"):])
-                break
+            for key, tag in (("products", "traffic-json:"), ("lower", "traffic-lower-json:")):
+                if line.startswith(tag):
+                    t = json.loads(line[len(tag):])
+                    if t.get("workload") == "%s %s" % (layer_name, algo) and t.get("csrc_sha256") == digest:
+                        out[key] = int(round((t["fetch_kib"] * t["fetch_scale"] +
+                                              t["write_kib"] * t["write_scale"]) * 1024))
+    return out
+
+
+class Config:
+    """One layer and algorithm: sizes, algorithmic work, buffers and launches."""
+
+    def __init__(self, mec, wl, torch, layer, algo, nsets, dev, stream):
+        self.mec, self.torch, self.layer, self.algo, self.stream = mec, torch, layer, algo, stream
+        self.dims = dims = layer.dims
+        i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w = dims
+        self.o_h, self.o_w = o_h, o_w = mec.output_dims(i_h, i_w, k_h, k_w, s_h, s_w)
+        self.dt_code = mec.BF16 if layer.dtype == "bf16" else mec.F32
+        self.es = es = 2 if layer.dtype == "bf16" else 4
+        self.macs = i_n * o_h * o_w * k_c * k_h * k_w * i_c
+        self.flops = 2.0 * self.macs
+        self.ws_lowered = mec.workspace_bytes(*dims, dtype=self.dt_code, algo=mec.LOWERED)
+        self.ws_im2col = mec.im2col_bytes(*dims, dtype=self.dt_code)
+        self.ws = {"lowered": self.ws_lowered, "fused": 0, "im2col": self.ws_im2col}[algo]
+        self.size_I = i_n * i_h * i_w * i_c
+        self.size_K = k_h * k_w * i_c * k_c
+        self.size_O = i_n * o_h * o_w * k_c
+        self.size_W = self.ws // es   # |L| or |M| elements (0 fused)
+        self.P = k_h * k_w * i_c      # im2col row length
+        self.I0, self.K0 = wl.make_inputs(layer)
+        # Enough sets that no kernel's rotating footprint fits the 256 MB
+        # memory-attached last-level cache: every launch reads its operands from
+        # HBM, as the rooflines assume.
+        if algo == "fused":
+            foot = es * (self.size_I + self.size_K) + 4 * self.size_O
         else:
-            return None
-    if t.get("workload") != "%s %s" % (layer_name, algo) or t.get("csrc_sha256") != csrc_digest():
-        return None
-    return int(round((t["fetch_kib"] * t["fetch_scale"] + t["write_kib"] * t["write_scale"]) * 1024))
+            foot = min(es * (self.size_I + self.size_W), es * (self.size_W + self.size_K) + 4 * self.size_O)
+        nsets = min(max(nsets, -(-MIN_ROTATION_BYTES // foot)), 256)
+        self.sets = []
+        for j in range(nsets):
+            I = self.I0.to(dev)
+            if j:
+                I = I.clone()
+            b = dict(I=I, K=self.K0.to(dev),
+                     O=torch.empty((i_n, o_h, o_w, k_c), dtype=torch.float32, device=dev))
+            if algo != "fused":
+                # the workspace the library asks for, in bytes
+                b["W"] = torch.empty(self.ws, dtype=torch.uint8, device=dev)
+            self.sets.append(b)
+
+    def lower(self, b):
+        m, (i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w) = self.mec, self.dims
+        if self.algo == "im2col":
+            M = b["W"].view(self.I0.dtype).view(i_n, self.o_w, self.o_h, k_h, k_w, i_c)
+            m.im2col(b["I"], k_h, k_w, k_c, s_h, s_w, M=M, stream=self.stream)
+        else:
+            L = b["W"].view(self.I0.dtype).view(i_n, self.o_w, i_h, k_w, i_c)
+            m.lower(b["I"], k_h, k_w, k_c, s_h, s_w, L=L, stream=self.stream)
+
+    def products(self, b):
+        m, (i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w) = self.mec, self.dims
+        if self.algo == "fused":
+            m.conv2d(b["I"], b["K"], s_h, s_w, algo="fused", O=b["O"], stream=self.stream)
+        elif self.algo == "im2col":
+            # the product of M and K: MEC's product phase of the 1x1 convolution
+            # whose pixels (n, y, x) carry the patches as channels
+            M = b["W"].view(self.I0.dtype).view(i_n, self.o_w, self.o_h, 1, self.P)
+            m.gemm(M, b["K"].view(1, 1, self.P, k_c), self.o_h, self.o_w, 1, 1, O=b["O"],
+                   stream=self.stream)
+        else:
+            L = b["W"].view(self.I0.dtype).view(i_n, self.o_w, i_h, k_w, i_c)
+            m.gemm(L, b["K"], i_h, i_w, s_h, s_w, O=b["O"], stream=self.stream)
+
+    def step(self, b):
+        if self.algo != "fused":
+            self.lower(b)
+        self.products(b)
+
+    def alg_bytes(self):
+        """Algorithmic HBM bytes of the products kernel per launch: each
+        element of L (or I when fused, or M) and K read once, O written once."""
+        src = self.size_I if self.algo == "fused" else self.size_W
+        return self.es * (src + self.size_K) + 4 * self.size_O
+
+    def lower_bytes(self):
+        return self.es * (self.size_I + self.size_W)
+
+
+def timed(HipEvent, stream, fn, sets, n):
+    """Average ms of n calls of fn over the rotating sets, between two events."""
+    import torch
+    start, end = HipEvent(), HipEvent()
+    torch.cuda.synchronize()
+    start.record(stream)
+    for k in range(n):
+        fn(sets[k % len(sets)])
+    end.record(stream)
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / n
+
+
+def settle(cfg, seconds):
+    """Untimed steps for about `seconds` of wall time, so that the GPU's clocks
+    have left their idle state before the warm-up steps; returns the count."""
+    import torch
+    n, t0 = 0, time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(8):
+            cfg.step(cfg.sets[n % len(cfg.sets)])
+            n += 1
+        torch.cuda.synchronize()
+    return n
+
+
+def measure(cfg, HipEvent, steps, warmup, digest, settle_s):
+    """Step time and per-kernel durations of one configuration, with rooflines."""
+    import torch
+    with torch.cuda.stream(cfg.stream):
+        settled = settle(cfg, settle_s)
+        for w in range(warmup):
+            cfg.step(cfg.sets[w % len(cfg.sets)])
+        t0 = time.perf_counter()
+        ms_step = timed(HipEvent, cfg.stream, cfg.step, cfg.sets, steps)
+        wall = time.perf_counter() - t0
+        lower_ms = None
+        if cfg.algo != "fused":
+            lower_ms = timed(HipEvent, cfg.stream, cfg.lower, cfg.sets, steps)
+        prod_ms = timed(HipEvent, cfg.stream, cfg.products, cfg.sets, steps)
+
+    layer = cfg.layer
+    peak = PEAK_TFLOPS[layer.dtype]
+    traffic = load_traffic(layer.dtype, layer.name, cfg.algo, digest)
+    kname = "slab_gemm_%s_kernel" % layer.dtype
+    kname += {"fused": " (from I)", "im2col": " (im2col product, k_h = 1)", "lowered": ""}[cfg.algo]
+    ab = cfg.alg_bytes()
+    ridge = peak * 1e12 / (PEAK_HBM_GBS * 1e9)
+    if layer.name == "tiny":
+        bound = "launch"   # 450 flops: the launch, not a roofline, is what it costs
+    else:
+        bound = "mfma" if cfg.flops / ab >= ridge else "hbm"
+    if bound == "hbm":
+        ach = ab / (prod_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "kernel": kname, "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4)}
+    else:
+        ach = cfg.flops / (prod_ms * 1e-3) / 1e12
+        roof = {"bound": bound, "kernel": kname, "achieved": round(ach, 3), "peak": peak,
+                "unit": "TFLOP/s", "frac": round(ach / peak, 4) if bound == "mfma" else None}
+    roof.update({"traffic": traffic["products"], "alg_flops": cfg.flops, "alg_bytes": ab,
+                 "avg_ms": round(prod_ms, 5)})
+    out = {"ms_per_step": round(ms_step, 5),
+           "tflops": round(cfg.flops / (ms_step * 1e-3) / 1e12, 3),
+           "settle_steps": settled,
+           "wall_s": round(wall, 4),
+           "gemm_ms": round(prod_ms, 5),
+           "roofline": roof}
+    if lower_ms is not None:
+        lb = cfg.lower_bytes()
+        gbs = lb / (lower_ms * 1e-3) / 1e9
+        out["lower_ms"] = round(lower_ms, 5)
+        out["roofline_lower"] = {
+            "bound": "hbm" if layer.name != "tiny" else "launch",
+            "kernel": "im2col_*_kernel" if cfg.algo == "im2col" else "lower_*_kernel",
+            "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": round(gbs / PEAK_HBM_GBS, 4) if layer.name != "tiny" else None,
+            "traffic": traffic["lower"], "alg_bytes": lb}
+    out["workspace_bytes"] = cfg.ws
+    out["im2col_bytes"] = cfg.ws_im2col
+    out["workspace_vs_mec_closed_form"] = round(cfg.ws / cfg.ws_lowered, 4) if cfg.algo == "lowered" else None
+    return out
+
+
+def workload_name(layer, o_h, o_w):
+    i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w = layer.dims
+    return ("%s: i_n=%d, I %dx%dx%d (%s), K %dx%dx%dx%d, s=%d/%d, o=%dx%d"
+            % (layer.name, i_n, i_h, i_w, i_c, layer.dtype, k_h, k_w, i_c, k_c, s_h, s_w, o_h, o_w))
 
 
 def main():
@@ -115,6 +303,7 @@ def main():
 
     import paper_1706_06873_amd as mec
     from paper_1706_06873_amd import workloads as wl
+    from paper_1706_06873_amd.timing import HipEvent
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -123,124 +312,19 @@ def main():
     if args.batch > 0:
         import dataclasses
         layer = dataclasses.replace(layer, i_n=args.batch)
-    dims = layer.dims
-    i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w = dims
-    o_h, o_w = mec.output_dims(i_h, i_w, k_h, k_w, s_h, s_w)
-    dt_code = mec.BF16 if layer.dtype == "bf16" else mec.F32
-    es = 2 if layer.dtype == "bf16" else 4
-    macs = i_n * o_h * o_w * k_c * k_h * k_w * i_c
-    flops = 2.0 * macs
-    ws_bytes = mec.workspace_bytes(*dims, dtype=dt_code, algo=mec.LOWERED)
-    im2col_bytes = mec.im2col_bytes(*dims, dtype=dt_code)
-    size_I = i_n * i_h * i_w * i_c
-    size_K = k_h * k_w * i_c * k_c
-    size_O = i_n * o_h * o_w * k_c
-    size_L = ws_bytes // es
-    size_M = im2col_bytes // es
-    P = k_h * k_w * i_c  # im2col row length
-
     dev = torch.device("cuda:0")
-    I0, K0 = wl.make_inputs(layer)
-    sets = []
-    for j in range(args.sets):
-        I = I0.to(dev)
-        if j:
-            I = I.clone()
-        lshape = (i_n, o_w, o_h, k_h, k_w, i_c) if args.algo == "im2col" else (i_n, o_w, i_h, k_w, i_c)
-        sets.append(dict(I=I, K=K0.to(dev),
-                         L=torch.empty(lshape, dtype=I0.dtype, device=dev),
-                         O=torch.empty((i_n, o_h, o_w, k_c), dtype=torch.float32, device=dev)))
     stream = torch.cuda.Stream(device=dev)  # default priority
+    digest = csrc_digest()
+
+    cfg = Config(mec, wl, torch, layer, args.algo, args.sets, dev, stream)
     torch.cuda.synchronize()
-
-    def step(bufs, ev=None):
-        if args.algo == "fused":
-            if ev:
-                ev[0].record(stream)
-            mec.conv2d(bufs["I"], bufs["K"], s_h, s_w, algo="fused", O=bufs["O"], stream=stream)
-            if ev:
-                ev[1].record(stream)
-            return
-        if ev:
-            ev[0].record(stream)
-        if args.algo == "im2col":
-            mec.im2col(bufs["I"], k_h, k_w, k_c, s_h, s_w, M=bufs["L"], stream=stream)
-        else:
-            mec.lower(bufs["I"], k_h, k_w, k_c, s_h, s_w, L=bufs["L"], stream=stream)
-        if ev:
-            ev[1].record(stream)
-        if args.algo == "im2col":
-            # the product of M and K: MEC's product phase of the 1x1 convolution
-            # whose pixels (n, y, x) carry the patches as channels
-            mec.gemm(bufs["L"].view(i_n, o_w, o_h, 1, P), bufs["K"].view(1, 1, P, k_c),
-                     o_h, o_w, 1, 1, O=bufs["O"], stream=stream)
-        else:
-            mec.gemm(bufs["L"], bufs["K"], i_h, i_w, s_h, s_w, O=bufs["O"], stream=stream)
-        if ev:
-            ev[2].record(stream)
-
-    from paper_1706_06873_amd.timing import HipEvent
-    with torch.cuda.stream(stream):
-        for w in range(args.warmup):
-            step(sets[w % len(sets)])
-        torch.cuda.synchronize()
-        # the timed steps: nothing on the stream but the steps themselves
-        start, end = HipEvent(), HipEvent()
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        start.record(stream)
-        for k in range(args.steps):
-            step(sets[k % len(sets)])
-        end.record(stream)
-        torch.cuda.synchronize()
-        wall = time.perf_counter() - t0
-        # the same steps again, an event around every launch: per-kernel durations
-        n_ev = 2 if args.algo == "fused" else 3
-        evs = [[HipEvent() for _ in range(n_ev)] for _ in range(args.steps)]
-        torch.cuda.synchronize()
-        for k in range(args.steps):
-            step(sets[k % len(sets)], evs[k])
-        torch.cuda.synchronize()
-
-    total_ms = start.elapsed_time(end)
-    ms_per_step = total_ms / args.steps
-    if args.algo == "fused":
-        kern_ms = [e[0].elapsed_time(e[1]) for e in evs]
-        lower_ms = None
-    else:
-        lower_ms = sorted(e[0].elapsed_time(e[1]) for e in evs)
-        kern_ms = [e[1].elapsed_time(e[2]) for e in evs]
-    kern_ms = sorted(kern_ms)
-    kern_avg = sum(kern_ms) / len(kern_ms)
-    value = flops / (ms_per_step * 1e-3) / 1e12
-
-    # roofline of the dominant kernel: algorithmic flops per launch / its average duration
-    peak = PEAK_TFLOPS[layer.dtype]
-    achieved = flops / (kern_avg * 1e-3) / 1e12
-    kname = "slab_gemm_%s_kernel" % ("bf16" if layer.dtype == "bf16" else "f32")
-    if args.algo == "fused":
-        alg_bytes = es * (size_I + size_K) + 4 * size_O
-        kname += " (from I)"
-    elif args.algo == "im2col":
-        alg_bytes = es * (size_M + size_K) + 4 * size_O
-        kname += " (im2col product, k_h = 1)"
-    else:
-        alg_bytes = es * (size_L + size_K) + 4 * size_O
-    # a kernel whose arithmetic intensity is below the ridge point is HBM-bound
-    ridge = peak * 1e12 / (PEAK_HBM_GBS * 1e9)
-    bound = "mfma" if flops / alg_bytes >= ridge else "hbm"
-    traffic = load_traffic(args.traffic, "bf16" if layer.dtype == "bf16" else "f32", layer.name, args.algo) if args.batch <= 0 else None
-    if bound == "mfma":
-        roof = {"bound": "mfma", "kernel": kname, "achieved": round(achieved, 2),
-                "peak": peak, "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
-                "traffic": traffic, "alg_flops": flops, "alg_bytes": alg_bytes,
-                "avg_ms": round(kern_avg, 5)}
-    else:
-        gbs = alg_bytes / (kern_avg * 1e-3) / 1e9
-        roof = {"bound": "hbm", "kernel": kname, "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": traffic,
-                "alg_flops": flops, "alg_bytes": alg_bytes, "avg_ms": round(kern_avg, 5)}
-
+    head = measure(cfg, HipEvent, args.steps, args.warmup, digest, args.settle)
+    if args.batch > 0:   # counters were taken at the layer's own batch
+        head["roofline"]["traffic"] = None
+        if "roofline_lower" in head:
+            head["roofline_lower"]["traffic"] = None
+    I0, K0, macs = cfg.I0, cfg.K0, cfg.macs
+    value = cfg.flops / (head["ms_per_step"] * 1e-3) / 1e12
     out = {
         "metric": METRIC,
         "value": round(value, 3),
@@ -248,35 +332,43 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 5),
+        "ms_per_step": head["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": layer.dtype,
         "data": "synthetic (seeded, %s)" % layer.note,
-        "config": {"workload": "%s: i_n=%d, I %dx%dx%d (%s), K %dx%dx%dx%d, s=%d/%d, o=%dx%d"
-                               % (layer.name, i_n, i_h, i_w, i_c, layer.dtype, k_h, k_w, i_c, k_c,
-                                  s_h, s_w, o_h, o_w),
-                   "algo": args.algo, "buffer_sets": args.sets},
-        "workspace_bytes": {"lowered": ws_bytes, "fused": 0, "im2col": im2col_bytes}[args.algo],
-        "im2col_bytes": im2col_bytes,
-        "workspace_vs_im2col": round(im2col_bytes / ws_bytes, 4),
-        "wall_s": round(wall, 4),
-        "gemm_ms": {"avg": round(kern_avg, 5), "median": round(kern_ms[len(kern_ms) // 2], 5),
-                    "min": round(kern_ms[0], 5)},
-        "roofline": roof,
+        "config": {"workload": workload_name(layer, cfg.o_h, cfg.o_w),
+                   "algo": args.algo, "buffer_sets": len(cfg.sets)},
+        "workspace_bytes": cfg.ws,
+        "im2col_bytes": cfg.ws_im2col,
+        "workspace_vs_im2col": round(cfg.ws_im2col / cfg.ws_lowered, 4),
+        "wall_s": head["wall_s"],
+        "gemm_ms": head["gemm_ms"],
+        "roofline": head["roofline"],
     }
-    if lower_ms is not None:
-        lavg = sum(lower_ms) / len(lower_ms)
-        lbytes = es * (size_I + (size_M if args.algo == "im2col" else size_L))
-        out["lower_ms"] = {"avg": round(lavg, 5), "median": round(lower_ms[len(lower_ms) // 2], 5),
-                           "min": round(lower_ms[0], 5)}
-        out["roofline_lower"] = {"bound": "hbm",
-                                 "kernel": "im2col_*_kernel" if args.algo == "im2col" else "lower_*_kernel",
-                                 "achieved": round(lbytes / (lavg * 1e-3) / 1e9, 1),
-                                 "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                                 "frac": round(lbytes / (lavg * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
-                                 "alg_bytes": lbytes}
+    if "lower_ms" in head:
+        out["lower_ms"] = head["lower_ms"]
+        out["roofline_lower"] = head["roofline_lower"]
+    del cfg
+    torch.cuda.empty_cache()
+
+    if args.sweep == "all":
+        sweep = {}
+        for name in wl.LAYER_ORDER:
+            for algo in SWEEP_ALGOS:
+                key = "%s/%s" % (name, algo)
+                if name == layer.name and algo == args.algo and args.batch <= 0:
+                    sweep[key] = dict(head, workload=out["config"]["workload"])
+                    continue
+                c = Config(mec, wl, torch, wl.LAYERS[name], algo, args.sets, dev, stream)
+                r = measure(c, HipEvent, args.steps, args.warmup, digest, args.settle)
+                r["workload"] = workload_name(c.layer, c.o_h, c.o_w)
+                sweep[key] = r
+                del c
+                torch.cuda.empty_cache()
+        out["configs"] = sweep
+
     if args.copy_mib > 0:
         # A plain copy of known size through the library's own row-copy
         # kernel: with i_w = k_w = 1 the lowering is L = I element for element.

@@ -1336,17 +1336,15 @@ hipError_t run_stream(const Shape& s, const void* A, const void* K, float* O, hi
     p.ntiles = (uint32_t)ntiles;
     set_layout(p, s, O, layout);
     p.div_ow = FastDiv((uint32_t)s.o_w);
-    // persistent grid: the workgroups every compute unit holds at once (LDS and
-    // registers), a multiple of 8 so each workgroup's tiles stay on its XCD
-    static const int per_cu = [] {
-        int b = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, slab_gemm_f32_stream_kernel<C>,
-                                                         C::THREADS, 0) != hipSuccess || b < 1)
-            b = 1;
-        return b;
-    }();
+    // persistent grid: the workgroups every compute unit of the stream's device
+    // holds at once (LDS and registers), a multiple of 8 so each workgroup's
+    // tiles stay on its XCD
+    int per_cu = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, slab_gemm_f32_stream_kernel<C>,
+                                                     C::THREADS, 0) != hipSuccess || per_cu < 1)
+        per_cu = 1;
     int dev = 0, cus = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
+    if (hipStreamGetDevice(stream, &dev) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
         cus = 1;
     int64_t grid = (int64_t)per_cu * cus / 8 * 8;

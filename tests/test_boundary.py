@@ -362,3 +362,88 @@ def test_grad_null_alignment_and_workspace():
     assert L.mec_conv2d_wgrad(FAKE, FAKE, FAKE, FAKE, need_k - 4, *GOOD, 0, NULL) == -2
     assert L.mec_wgrad_gemm(FAKE, FAKE, FAKE, FAKE, need_l - 4, *GOOD, 0, NULL) == -2
     assert L.mec_wgrad_gemm(FAKE, FAKE, FAKE, NULL, need_l, *GOOD, 0, NULL) == -2
+
+
+# ---------------------------------------------------------------- binding validation
+# Caller-supplied outputs and operands that do not match the shape must be
+# refused by the binding before any library entry point that launches work is
+# called. CPU tensors stand in for device ones: every check below runs before
+# the binding takes a device pointer.
+
+LAUNCHERS = ("mec_lower", "mec_im2col", "mec_gemm", "mec_conv2d", "mec_fold", "mec_dgrad_gemm",
+             "mec_conv2d_dgrad", "mec_wgrad_gemm", "mec_conv2d_wgrad")
+
+
+@pytest.fixture
+def no_launch(monkeypatch):
+    def refuse(*a, **k):
+        raise AssertionError("a launching entry point was called")
+    for name in LAUNCHERS:
+        monkeypatch.setattr(mec.lib, name, refuse)
+    return mec
+
+
+def _t(*shape, dtype=None):
+    import torch
+    return torch.zeros(shape, dtype=dtype or torch.float32)
+
+
+def test_binding_refuses_mismatched_operands(no_launch):
+    import torch
+    m = no_launch
+    d = (2, 9, 8, 4, 3, 3, 5, 1, 1)     # i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w
+    I, K = _t(2, 9, 8, 4), _t(3, 3, 4, 5)
+    L = _t(2, 6, 9, 3, 4)                 # o_w = 6
+    O = _t(2, 7, 6, 5)
+    # gemm: K must agree with L on k_w and i_c, and share its dtype
+    with pytest.raises(ValueError, match="do not agree"):
+        m.gemm(L, _t(3, 2, 4, 5), 9, 8, 1, 1, O=O)
+    with pytest.raises(ValueError, match="do not agree"):
+        m.gemm(L, _t(3, 3, 3, 5), 9, 8, 1, 1, O=O)
+    with pytest.raises(TypeError, match="same dtype"):
+        m.gemm(L, _t(3, 3, 4, 5, dtype=torch.bfloat16), 9, 8, 1, 1, O=O)
+    # a given O of the wrong shape or dtype
+    for bad in (_t(2, 7, 6, 4), _t(2, 7, 6, 5, dtype=torch.float64), _t(2 * 7 * 6 * 5)):
+        with pytest.raises(ValueError, match="O must be"):
+            m.gemm(L, K, 9, 8, 1, 1, O=bad)
+        with pytest.raises(ValueError, match="O must be"):
+            m.conv2d(I, K, 1, 1, algo="fused", O=bad)
+    # a workspace smaller than the library asks for
+    need = m.workspace_bytes(*d)
+    with pytest.raises(ValueError, match="workspace holds"):
+        m.conv2d(I, K, 1, 1, algo="lowered", O=O, workspace=_t(need - 1, dtype=torch.uint8))
+    # L and M of the wrong byte size or dtype
+    with pytest.raises(ValueError, match="L must hold"):
+        m.lower(I, 3, 3, 5, 1, 1, L=_t(L.numel() - 1))
+    with pytest.raises(ValueError, match="L must hold"):
+        m.lower(I, 3, 3, 5, 1, 1, L=_t(*L.shape, dtype=torch.bfloat16))
+    with pytest.raises(ValueError, match="M must hold"):
+        m.im2col(I, 3, 3, 5, 1, 1, M=_t(7))
+
+
+def test_binding_refuses_mismatched_gradients(no_launch):
+    import torch
+    m = no_launch
+    d = (2, 9, 8, 4, 3, 3, 5, 1, 1)
+    I, K, G = _t(2, 9, 8, 4), _t(3, 3, 4, 5), _t(2, 7, 6, 5)
+    L = _t(2, 6, 9, 3, 4)
+    with pytest.raises(ValueError, match="G must be"):
+        m.conv2d_dgrad(_t(2, 7, 5, 5), K, 9, 8)
+    for bad in (_t(2, 9, 8, 3), _t(2, 9, 8, 4, dtype=torch.float64)):
+        with pytest.raises(ValueError, match="dI must be"):
+            m.conv2d_dgrad(G, K, 9, 8, dI=bad)
+        with pytest.raises(ValueError, match="dI must be"):
+            m.fold(_t(2, 6, 9, 3, 4), 8, 1, dI=bad)
+    with pytest.raises(ValueError, match="dL must be"):
+        m.dgrad_gemm(G, K, 9, 8, dL=_t(2, 6, 9, 3, 3))
+    for bad in (_t(3, 3, 4, 4), _t(3, 3, 4, 5, dtype=torch.bfloat16)):
+        with pytest.raises(ValueError, match="dK must be"):
+            m.wgrad_gemm(L, G, 3, 8, dK=bad)
+        with pytest.raises(ValueError, match="dK must be"):
+            m.conv2d_wgrad(I, G, 3, 3, dK=bad)
+    need = m.grad_workspace_bytes(*d, grad_pass=m.GRAD_KERNEL)
+    with pytest.raises(ValueError, match="workspace holds"):
+        m.conv2d_wgrad(I, G, 3, 3, workspace=_t(max(need - 4, 0), dtype=torch.uint8))
+    need = m.grad_workspace_bytes(*d, grad_pass=m.GRAD_INPUT)
+    with pytest.raises(ValueError, match="workspace holds"):
+        m.conv2d_dgrad(G, K, 9, 8, workspace=_t(max(need - 4, 0), dtype=torch.uint8))
