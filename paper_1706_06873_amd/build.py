@@ -16,8 +16,12 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(REPO, "include")
 LIB = os.path.join(PKG, "libmec.so")
 SOURCES = ["mec_api.cpp", "mec_lower.hip", "mec_im2col.hip", "mec_gemm.hip", "mec_gemm_fixed.hip",
-           "mec_grad.hip"]
+           "mec_gemm_ring.hip", "mec_grad.hip"]
 ARCH = "gfx950"
+# Per-source flags. The flat-window kernel keeps its accumulators in
+# architectural VGPRs: with the default heuristic the compiler holds them in
+# AGPRs for the MFMAs but copies them through VGPRs at every loop back edge.
+EXTRA_FLAGS = {"mec_gemm_ring.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 HIPCC_FLAGS = [
     "--offload-arch=" + ARCH,
@@ -38,7 +42,8 @@ def build(verbose: bool = False) -> str:
     for src in SOURCES:
         obj = os.path.join(objdir, os.path.splitext(src)[0] + ".o")
         lang = ["-x", "hip"] if src.endswith(".hip") else []
-        cmd = ["hipcc"] + HIPCC_FLAGS + lang + ["-c", os.path.join(CSRC, src), "-o", obj]
+        cmd = (["hipcc"] + HIPCC_FLAGS + EXTRA_FLAGS.get(src, []) + lang +
+               ["-c", os.path.join(CSRC, src), "-o", obj])
         if verbose:
             print(" ".join(cmd), flush=True)
         subprocess.run(cmd, check=True)

@@ -1538,6 +1538,10 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
         return dry_run ? hipSuccess : run_stream<CFG>(s, A, K, O, stream, layout);  \
     }
     if (dtype == 0) {
+        // 11x11 stride 4 over few channels (rows of L of 33 elements): the flat
+        // windows through a ring of LDS (mec_gemm_ring.hip)
+        if (!layout && s.k_h == 11 && s.s_h == 4 && gemm_ring_usable(s, dtype))
+            return dry_run ? hipSuccess : launch_gemm_ring(s, A, K, O, F, stream);
         if (s.R >= 32) {
             // no split into a strided layout: zeroing O would clear other pixels
             const TileChoice tc =

@@ -1,0 +1,339 @@
+// MEC's slab products (Section 3.3, Algorithm 2, product phase) for tall,
+// strided kernels over few channels (fp32; the 11x11 stride-4 first layers of
+// Table 2, cv1 and cv2), where a row of L is short (R = k_w*i_c = 33) and the
+// slab of one output row, k_h*R = 363 elements, spans many of them.
+//
+// Section 3.2 views output row h of pair (n, w) as one dot product over a
+// contiguous window of that pair's row of L:
+//   O[n, h, w, :] = sum_{j < k_h*R} L[n, w][s_h*R*h + j] * K[j, :]
+// with K viewed as a (k_h*k_w*i_c) x k_c matrix. Consecutive output rows'
+// windows start s_h*R elements apart and overlap by (k_h - s_h)*R.
+//
+// This kernel takes that flat view literally. One wave is one workgroup. Its
+// 32x32 MFMA block has as rows 8 pairs x 4 consecutive output rows, so all 32
+// rows reduce over the same index j at every step and share one fragment of
+// K (read from global memory, where every wave finds it in the L2 cache). The
+// reduction runs over the window's k_h*R elements in steps of 2 (one
+// v_mfma_f32_32x32x2_f32), padded with zeros to whole blocks of 8 steps (363
+// -> 368, 1.4%): no per-row padding of R to a staging width. The wave streams its 8 pairs' rows of L (or, fused,
+// the same elements of I) through a ring in LDS, 512 elements per pair, filled
+// 64 elements at a time by direct-to-LDS loads one block of k-steps ahead of
+// use; every element of the rows it covers is loaded once per item, the
+// overlap between output rows is read from the ring. Waves share nothing, so
+// there is no barrier: several waves per SIMD hide each other's load latency.
+#include "mec_mfma.h"
+
+namespace mec {
+namespace {
+
+constexpr int kRPairs = 8;                 // pairs per wave tile
+constexpr int kRRows = 4;                  // output rows per wave tile: 8 x 4 = 32 MFMA rows
+constexpr int kChunk = 64;                 // elements per fill: one dword per lane
+constexpr int kRingChunks = 8;             // ring capacity in chunks
+constexpr int kRingLen = kChunk * kRingChunks;
+// floats between pairs' rings: 8 x 636 x 4 B = 19.9 KB per wave, so eight
+// waves fit a compute unit, two per SIMD (16.5 KB would fit nine, three on one
+// SIMD and two on the others: measured 1.5% slower); 636 = -4 mod 64 banks, so
+// a fragment read of 8 pairs x 4 rows spreads over the banks
+constexpr int kRingLD = kRingLen + 124;
+constexpr int kBlockSteps = 8;             // k-steps between fill points
+
+struct RingParams {
+    const float* A;   // L (lowered) or I (fused)
+    const float* K;   // (k_h*k_w*i_c) x k_c
+    float* O;
+    int64_t pairs, o_w, o_h, k_c;
+    int64_t rowlen;          // i_h * R: elements of one pair's row of L
+    int64_t img_stride;      // fused: i_h * i_w * i_c
+    int64_t x_stride;        // fused: i_w * i_c (next input row); lowered: R
+    int64_t w_stride;        // fused: s_w * i_c; lowered: i_h * R (next pair)
+    int32_t R, KR, nks, srow;  // KR = k_h*R; nks = ceil(KR / 2) rounded up to a whole block of
+                               // k-steps (the steps past KR multiply zeros); srow = s_h*R
+    int32_t ngroups;         // ceil(o_h / 4)
+    int32_t gpi;             // row groups per item
+    int32_t items_pg;        // items per pair group: ceil(ngroups / gpi)
+    int32_t n_tiles;         // channel tiles of 32*NB
+    uint32_t nitems;         // pair groups x items_pg x n_tiles
+    FastDiv divR;
+    FastDiv div_ow;          // pair -> (image, column); pairs < 2^31
+};
+
+// One dword per lane from base + voff (bytes) straight into LDS at lds + 4*lane.
+// M0 holds the LDS address; its previous value is put back (M0 cannot be
+// declared clobbered). s_waitcnt lgkmcnt(0) first: every LDS read issued
+// earlier has returned before the slot can be overwritten.
+__device__ inline void ring_dma(const float* base, uint32_t voff, uint32_t lds) {
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %2, %3\n\ts_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "s"(lds), "v"(voff), "s"(base)
+        : "memory");
+}
+
+template <int NB, bool FUSED>
+__global__ __launch_bounds__(64) void slab_gemm_f32_ring_kernel(RingParams p) {
+    __shared__ __align__(16) float ring[kRPairs * kRingLD];
+
+    const int lane = threadIdx.x;
+    const int m = lane & 31, kofs = lane >> 5;
+    const int pp = m & 7, ii = m >> 3;  // this lane's A row: pair pp, output row ii
+
+    const uint32_t t_item = xcd_remap(blockIdx.x, p.nitems);
+    const uint32_t nt = t_item % (uint32_t)p.n_tiles;
+    const uint32_t rest = t_item / (uint32_t)p.n_tiles;
+    const uint32_t ig = rest % (uint32_t)p.items_pg;
+    const int64_t pair0 = (int64_t)(rest / (uint32_t)p.items_pg) * kRPairs;
+    const int g_begin = (int)ig * p.gpi;
+    const int g_end = g_begin + p.gpi < p.ngroups ? g_begin + p.gpi : p.ngroups;
+    const int n0 = (int)nt * 32 * NB;
+
+    // Source of each pair's row of L: element o of pair q's row is at
+    // srcq[q] + (o / R) * x_stride + o % R (lowered: x_stride = R, so srcq[q] + o).
+    // Offsets are relative to the first pair's source, in elements.
+    int64_t src0;
+    {
+        const int64_t n = p.div_ow.div((uint32_t)pair0), w = pair0 - n * p.o_w;
+        src0 = FUSED ? n * p.img_stride + w * p.w_stride : pair0 * p.rowlen;
+    }
+    const float* __restrict__ Abase = p.A + src0;
+    uint32_t srcq[kRPairs];
+#pragma unroll
+    for (int q = 0; q < kRPairs; ++q) {
+        int64_t pr = pair0 + q;
+        if (pr >= p.pairs) pr = pair0;  // past the end: the first pair (never stored)
+        const int64_t n = p.div_ow.div((uint32_t)pr), w = pr - n * p.o_w;
+        const int64_t s = FUSED ? n * p.img_stride + w * p.w_stride : pr * p.rowlen;
+        srcq[q] = (uint32_t)(s - src0);
+    }
+    const uint32_t ring_lds =
+        (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(size_t)(__attribute__((address_space(3))) float*)ring);
+
+    // Fill chunk c (elements [64c, 64c + 64) of every pair's row) into its ring
+    // slot. Elements past the row's end repeat its last one: they only reach
+    // output rows past o_h, which are never stored.
+    auto fill = [&](int c) {
+        int64_t o = (int64_t)c * kChunk + lane;
+        if (o > p.rowlen - 1) o = p.rowlen - 1;
+        uint32_t rel;
+        if (FUSED) {
+            const uint32_t x = p.divR.div((uint32_t)o);
+            rel = x * (uint32_t)p.x_stride + ((uint32_t)o - x * (uint32_t)p.R);
+        } else {
+            rel = (uint32_t)o;
+        }
+        const uint32_t slot = (uint32_t)(c % kRingChunks) * kChunk;
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+        for (int q = 0; q < kRPairs; ++q)
+            ring_dma(Abase, 4u * (srcq[q] + rel), ring_lds + 4u * (uint32_t)(q * kRingLD) + 4u * slot);
+    };
+    int filled = -1;  // highest chunk issued (set at the item's start below)
+    auto fill_upto = [&](int target) {
+        for (int c = filled + 1; c <= target; ++c) fill(c);
+        if (target > filled) filled = target;
+    };
+    // chunks read by block b of group g: [lo, hi]
+    const int rspan = (kRRows - 1) * p.srow;
+    auto blk_lo = [&](int g, int b) { return (g * kRRows * p.srow + 2 * kBlockSteps * b) / kChunk; };
+    auto blk_hi = [&](int g, int b) {
+        return (g * kRRows * p.srow + rspan + 2 * kBlockSteps * b + 2 * kBlockSteps - 1) / kChunk;
+    };
+    const int nblk = (p.nks + kBlockSteps - 1) / kBlockSteps;
+
+    // K fragment of k-step t, channel block nb: K[2t + kofs][n0 + 32 nb + m],
+    // by buffer loads whose range check returns 0 past K's last element: the
+    // padding steps' rows j >= KR, and channels past k_c in the last row (the
+    // columns past k_c are never stored).
+    const __amdgpu_buffer_rsrc_t krsrc =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p.K), (short)0, p.KR * (int)p.k_c * 4, 0x00020000);
+    const uint32_t klane = (uint32_t)((kofs * (int)p.k_c + n0 + m) * 4);
+    const uint32_t kstep = (uint32_t)(2 * p.k_c * 4);  // bytes per k-step
+    // K fragments of a whole block are loaded one block ahead, into the other
+    // of two register sets; the stream of k-steps wraps at nks (every group
+    // reduces over the same rows of K).
+    float kb0[kBlockSteps][NB], kb1[kBlockSteps][NB];
+    int kt = 0;  // first k-step (mod nks) of the next block of K fragments
+    auto kload_block = [&](float (*dst)[NB]) {
+        const uint32_t base = klane + (uint32_t)kt * kstep;
+#pragma unroll
+        for (int u = 0; u < kBlockSteps; ++u)
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+                dst[u][nb] = __builtin_bit_cast(
+                    float, __builtin_amdgcn_raw_buffer_load_b32(krsrc, base + u * kstep + 128 * nb, 0, 0));
+        kt = kt + kBlockSteps == p.nks ? 0 : kt + kBlockSteps;
+        asm volatile("" ::: "memory");  // issued here, not sunk towards their use
+    };
+    kload_block(kb0);
+
+    // first group: everything its first two blocks read
+    filled = blk_lo(g_begin, 0) - 1;
+    fill_upto(blk_hi(g_begin, nblk > 1 ? 1 : 0) < blk_lo(g_begin, 0) + kRingChunks - 1
+                  ? blk_hi(g_begin, nblk > 1 ? 1 : 0)
+                  : blk_lo(g_begin, 0) + kRingChunks - 1);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+
+    floatx16 acc[NB];
+    uint32_t ridx = 0;
+    const uint32_t abase = (uint32_t)(pp * kRingLD);
+    // The item's blocks in one sequence: block beta is block b = beta % nblk of
+    // group g = g_begin + beta / nblk. Even blocks multiply kb0 and load kb1,
+    // odd ones the reverse (the loop is unrolled by two so that both register
+    // sets keep fixed roles).
+    auto do_block = [&](int g, int b, float (*kuse)[NB], float (*knext)[NB]) {
+        if (b == 0) {
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) acc[nb][v] = 0.f;
+            // this lane's ring position: element g*4*srow + ii*srow + kofs of its row
+            ridx = (uint32_t)(g * kRRows * p.srow + ii * p.srow + kofs) & (kRingLen - 1);
+        }
+        // The fills issued before this block have landed. After block 0 the
+        // last ones went out at the start of the previous block, followed by
+        // kBlockSteps * NB K loads (this block's fragments): all but those are
+        // complete. At block 0 the last ones went out before the previous
+        // group's O stores, whose count depends on the edges: wait for
+        // everything.
+        if (b > 0)
+            asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kBlockSteps * NB) : "memory");
+        else if (g > g_begin)
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        if (filled < blk_hi(g, b)) {  // not reached while the ring holds a block ahead
+            fill_upto(blk_hi(g, b));
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        }
+        // prefetch the next block's chunks as far as the ring allows
+        if (b + 1 < nblk) {
+            const int cap = blk_lo(g, b) + kRingChunks - 1;
+            const int want = blk_hi(g, b + 1);
+            fill_upto(want < cap ? want : cap);
+        }
+        // the next block's K fragments (this block's were loaded one block ago)
+        kload_block(knext);
+        // the block's A fragments, all read up front (one LDS round trip per block)
+        float a[kBlockSteps];
+#pragma unroll
+        for (int u = 0; u < kBlockSteps; ++u) a[u] = ring[abase + ((ridx + 2 * u) & (kRingLen - 1))];
+        const int t = b * kBlockSteps;
+        if (2 * (t + kBlockSteps) > p.KR) {  // the block reaches past KR: zeros there
+#pragma unroll
+            for (int u = 0; u < kBlockSteps; ++u)
+                if (2 * (t + u) + kofs >= p.KR) a[u] = 0.f;
+        }
+        ridx = (ridx + 2 * kBlockSteps) & (kRingLen - 1);
+#pragma unroll
+        for (int u = 0; u < kBlockSteps; ++u)
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+                acc[nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[u], kuse[u][nb], acc[nb], 0, 0, 0);
+        if (b + 1 < nblk) return;
+        // end of group g. The next group's first two blocks: its chunks as far
+        // as the ring allows once this group's reads are done (the fill waits
+        // for them).
+        if (g + 1 < g_end) {
+            const int cap = blk_lo(g + 1, 0) + kRingChunks - 1;
+            const int want = blk_hi(g + 1, nblk > 1 ? 1 : 0);
+            fill_upto(want < cap ? want : cap);
+        }
+        // O rows (pair, h) of this group, 32 channels per block: for register v
+        // of lane l the row is acc_row(v, l) = 8*(v/4) + 4*(l/32) + v%4, i.e.
+        // output row h = 4g + v/4 of pair 4*(l/32) + v%4
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+            const int64_t pr = pair0 + kofs * 4 + q4;
+            if (pr >= p.pairs) continue;
+            const int64_t n = p.div_ow.div((uint32_t)pr), w = pr - n * p.o_w;
+            float* orow = p.O + ((n * p.o_h) * p.o_w + w) * p.k_c + n0 + m;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int64_t h = (int64_t)g * kRRows + r;
+                if (h >= p.o_h) continue;
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb)
+                    if (n0 + 32 * nb + m < p.k_c)
+                        __builtin_nontemporal_store(acc[nb][r * 4 + q4], orow + h * p.o_w * p.k_c + 32 * nb);
+            }
+        }
+    };
+    const int nbeta = (g_end - g_begin) * nblk;
+    int g = g_begin, b = 0;
+    for (int beta = 0; beta < nbeta; beta += 2) {
+        do_block(g, b, kb0, kb1);
+        if (++b == nblk) { b = 0; ++g; }
+        if (beta + 1 < nbeta) {
+            do_block(g, b, kb1, kb0);
+            if (++b == nblk) { b = 0; ++g; }
+        }
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
+}  // namespace
+
+bool gemm_ring_usable(const Shape& s, int dtype) {
+    if (dtype != 0) return false;
+    const int64_t srow = s.s_h * s.R;
+    // the ring holds the chunks one block of the four rows reads plus the next
+    // block's: (3 srow + 4 kBlockSteps + 62) / 64 < 8 chunks
+    if ((kRRows - 1) * srow + 4 * kBlockSteps + 62 > (int64_t)kRingLen - 1) return false;
+    // the next group's first chunk is not older than this group's last block's:
+    // reads never move back past what the ring has already dropped
+    const int64_t nks = ((s.k_h * s.R + 1) / 2 + kBlockSteps - 1) / kBlockSteps * kBlockSteps;
+    if (2 * (nks - kBlockSteps) > kRRows * srow) return false;
+    if (s.R * s.k_h > (int64_t(1) << 20) || s.pairs >= (int64_t(1) << 31)) return false;
+    // byte offsets of one dword load within a pair group's source fit 32 bits:
+    // lowered, 8 rows of L; fused, three images
+    if (8 * s.i_h * s.R >= (int64_t(1) << 30)) return false;
+    if (3 * s.i_h * s.i_w * s.i_c >= (int64_t(1) << 30)) return false;
+    return true;
+}
+
+hipError_t launch_gemm_ring(const Shape& s, const void* A, const void* K, float* O, bool fused,
+                            hipStream_t stream) {
+    RingParams p{};
+    p.A = static_cast<const float*>(A);
+    p.K = static_cast<const float*>(K);
+    p.O = O;
+    p.pairs = s.pairs;
+    p.o_w = s.o_w;
+    p.o_h = s.o_h;
+    p.k_c = s.k_c;
+    p.rowlen = s.i_h * s.R;
+    p.img_stride = s.i_h * s.i_w * s.i_c;
+    p.x_stride = fused ? s.i_w * s.i_c : s.R;
+    p.w_stride = fused ? s.s_w * s.i_c : s.i_h * s.R;
+    p.R = (int32_t)s.R;
+    p.KR = (int32_t)(s.k_h * s.R);
+    p.nks = ((p.KR + 1) / 2 + kBlockSteps - 1) / kBlockSteps * kBlockSteps;
+    p.srow = (int32_t)(s.s_h * s.R);
+    p.ngroups = (int32_t)((s.o_h + kRRows - 1) / kRRows);
+    // one row group per workgroup: more, shorter items balance the compute units
+    // better at the end of the launch than two per item (alexnet_conv1: 7%)
+    p.gpi = 1;
+    p.items_pg = (p.ngroups + p.gpi - 1) / p.gpi;
+    p.divR = FastDiv((uint32_t)s.R);
+    p.div_ow = FastDiv((uint32_t)s.o_w);
+    const int nb = s.k_c > 64 ? 3 : s.k_c > 32 ? 2 : 1;
+    p.n_tiles = (int32_t)((s.k_c + 32 * nb - 1) / (32 * nb));
+    const int64_t pgroups = (s.pairs + kRPairs - 1) / kRPairs;
+    const int64_t nitems = pgroups * p.items_pg * p.n_tiles;
+    if (nitems > 0x7fffffff) return hipErrorInvalidValue;
+    p.nitems = (uint32_t)nitems;
+    const dim3 grid(p.nitems), block(64);
+#define MEC_RING(NB_)                                                                         \
+    if (nb == NB_) {                                                                          \
+        if (fused)                                                                            \
+            hipLaunchKernelGGL((slab_gemm_f32_ring_kernel<NB_, true>), grid, block, 0, stream, p); \
+        else                                                                                  \
+            hipLaunchKernelGGL((slab_gemm_f32_ring_kernel<NB_, false>), grid, block, 0, stream, p); \
+    }
+    MEC_RING(1)
+    MEC_RING(2)
+    MEC_RING(3)
+#undef MEC_RING
+    return hipGetLastError();
+}
+
+}  // namespace mec

@@ -112,6 +112,13 @@ hipError_t launch_gemm_fixed(const Shape& s, const void* A, const void* K, float
                              bool fused, hipStream_t stream, bool dry_run,
                              const OutLayout* layout = nullptr);
 
+// The flat-window kernel for tall strided fp32 kernels over few channels
+// (mec_gemm_ring.hip): whether its ring of LDS holds the shape's windows, and
+// the launch (dense n-h-w-c O).
+bool gemm_ring_usable(const Shape& s, int dtype);
+hipError_t launch_gemm_ring(const Shape& s, const void* A, const void* K, float* O, bool fused,
+                            hipStream_t stream);
+
 // ---------------------------------------------------------------- training passes
 // dL (fp32, L's layout) from G = dloss/dO and K, fp32.
 bool dgrad_supported(const Shape& s);

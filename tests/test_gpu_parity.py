@@ -335,6 +335,68 @@ def test_f32_direct_to_lds_tiles(orc, dims, algo):
     assert rel_l2(run_conv(I, K, s_h, s_w, algo), orc.conv2d_direct(host(I), host(K), s_h, s_w)) <= TOL_F32
 
 
+# fp32 11x11 stride-4 layers: the flat-window kernel (one wave per
+# workgroup, 8 pairs x 4 output rows per MFMA block, rows of L streamed
+# through a ring in LDS). Items of two row groups; the cases reach a ragged
+# last pair group, an item of one group, o_h not a multiple of 4, one, two and
+# three 32-channel blocks, several channel tiles, pair groups across images,
+# s_w = 1 and 3, i_c = 1 and 2, and o = 1 x 1.
+RING_CASES = [
+    (1, 35, 31, 3, 11, 11, 96, 4, 4),     # 3 row groups: items of 2 and 1 groups
+    (2, 39, 27, 3, 11, 11, 40, 4, 4),     # two channel blocks, the second 8 wide
+    (1, 47, 35, 3, 11, 11, 100, 4, 4),    # two channel tiles of 96, the second 4 wide
+    (3, 23, 19, 3, 11, 11, 20, 4, 4),     # one channel block; 9 pairs (ragged pair group)
+    (1, 11, 11, 3, 11, 11, 96, 4, 4),     # k = i: o = 1 x 1
+    (2, 30, 30, 2, 11, 11, 33, 4, 3),     # i_c = 2 (R = 22), s_w = 3
+    (3, 30, 25, 1, 11, 11, 1, 4, 4),      # i_c = 1, k_c = 1
+    (5, 15, 15, 3, 11, 11, 8, 4, 4),      # o = 2 x 2, pair groups across images
+    (1, 19, 40, 3, 11, 11, 96, 4, 1),     # s_w = 1
+    (1, 43, 20, 3, 11, 11, 130, 4, 4),    # two channel tiles, the second 34 wide
+]
+
+
+@pytest.mark.parametrize("dims", RING_CASES)
+@pytest.mark.parametrize("algo", ["lowered", "fused"])
+def test_ring_products(orc, dims, algo):
+    say("ring", algo, dims)
+    s_h, s_w = dims[7], dims[8]
+    Ii, Ki = case(71 + sum(dims), dims, dist="int")
+    refi = orc.conv2d_direct(host(Ii), host(Ki), s_h, s_w)
+    assert np.abs(refi).max() < 2 ** 24
+    assert np.array_equal(run_conv(Ii, Ki, s_h, s_w, algo), refi.astype(np.float32))
+    I, K = case(73 + sum(dims), dims)
+    assert rel_l2(run_conv(I, K, s_h, s_w, algo), orc.conv2d_direct(host(I), host(K), s_h, s_w)) <= TOL_F32
+
+
+@pytest.mark.parametrize("shift", [1, 3])
+def test_ring_unaligned_and_guarded(orc, shift):
+    """I, K, L and O one or three elements off their 16-byte boundaries, O
+    inside a guard band: element loads and stores only, nothing written
+    outside O."""
+    dims = RING_CASES[2]
+    say("ring unaligned", shift, dims)
+    I, K = case(79 + shift, dims, dist="int")
+    ref = orc.conv2d_direct(host(I), host(K), 4, 4).astype(np.float32)
+
+    def offset_copy(t):
+        buf = torch.zeros(t.numel() + 8, dtype=t.dtype, device=DEV)
+        v = buf[shift:shift + t.numel()].view(t.shape)
+        v.copy_(t.to(DEV))
+        return v
+
+    Id, Kd = offset_copy(I), offset_copy(K)
+    buf = torch.full((ref.size + 64,), 7.0, dtype=torch.float32, device=DEV)
+    Od = buf[32 + shift:32 + shift + ref.size].view(ref.shape)
+    ws = torch.zeros(mec.workspace_bytes(*dims) + 64, dtype=torch.uint8, device=DEV)[4 * shift:]
+    for algo in ("lowered", "fused"):
+        buf.fill_(7.0)
+        mec.conv2d(Id, Kd, 4, 4, algo=algo, O=Od, workspace=ws)
+        torch.cuda.synchronize()
+        b = buf.cpu().numpy()
+        assert np.all(b[:32 + shift] == 7.0) and np.all(b[32 + shift + ref.size:] == 7.0), algo
+        assert np.array_equal(Od.cpu().numpy(), ref), algo
+
+
 # bf16 tiles staged by direct-to-LDS loads (rows of a multiple of 32): 3x3 in
 # the 14-row form where its tiles fill at least 192 compute units, else 2
 # rows; 5x5.
