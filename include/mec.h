@@ -31,7 +31,8 @@
  *    synchronised.
  *  - Every argument is checked on the host before anything is enqueued; on
  *    any error nothing is launched and no memory is written.
- *  - No global state: calls are thread-safe. Calls on different streams that
+ *  - No global state (except the no-alloc entry point's per-device scratch
+ *    address, below): calls are thread-safe. Calls on different streams that
  *    write the same memory race, as with any asynchronous device work.
  *  - Status codes are returned; negative values are errors. No C++ exception
  *    crosses this interface.
@@ -67,8 +68,10 @@ enum mec_status {
     MEC_ERR_WORKSPACE = -2,   /* workspace NULL or smaller than required      */
     MEC_ERR_ALIGNMENT = -3,   /* a pointer not aligned to its element size    */
     MEC_ERR_HIP = -4,         /* the HIP runtime reported a launch error      */
-    MEC_ERR_UNSUPPORTED = -5  /* valid but beyond this build's kernel limits
+    MEC_ERR_UNSUPPORTED = -5, /* valid but beyond this build's kernel limits
                                  (k_h larger than the on-chip tile allows)    */
+    MEC_ERR_SCRATCH = -6      /* a no-alloc call needs more scratch than the
+                                 library's static array holds                 */
 };
 
 /* Output size, Eq. (1) with the floor reading: o_h = (i_h - k_h) / s_h + 1,
@@ -262,6 +265,33 @@ int mec_conv2d_wgrad(const void* I, const float* G, float* dK,
                      int i_n, int i_h, int i_w, int i_c,
                      int k_h, int k_w, int k_c, int s_h, int s_w,
                      int dtype, void* stream);
+
+/* ------------------------------------------------------------------------
+ * No-alloc entry point, for callers that cannot allocate device memory:
+ * code under HIP graph capture, tight serving or training loops, harnesses
+ * that forbid hipMalloc. It computes what mec_conv2d_wgrad computes, with the
+ * same kernels, but keeps the partial sums in a static device array of the
+ * library (mec_noalloc_scratch_bytes() bytes, 64 MiB) instead of a caller's
+ * workspace. It calls no hipMalloc, hipFree or other allocating routine.
+ *  - Each GPU the library runs on holds its own copy of the array from the
+ *    library's first use on it until the process ends. Its address on a
+ *    device is looked up once, at the first call on that device (the only
+ *    global state of the library: a per-device pointer set under a lock).
+ *  - Every call on one GPU shares that GPU's array and leaves the last
+ *    call's partial sums in it. Nothing in it must start at zero: every share
+ *    writes its partial sums whole before they are summed. Calls that overlap
+ *    on one GPU (other streams or threads) race on the array: serialise them.
+ *  - Shapes whose partial sums (mec_grad_workspace_bytes(..., MEC_GRAD_KERNEL))
+ *    exceed the array return MEC_ERR_SCRATCH before anything is enqueued.
+ *  - dK (fp32) is bit-identical to mec_conv2d_wgrad's for the same arguments.
+ * The caller passes I, G and dK as for mec_conv2d_wgrad. Returns MEC_OK or a
+ * negative status.
+ * ------------------------------------------------------------------------ */
+int64_t mec_noalloc_scratch_bytes(void);
+int mec_conv2d_wgrad_noalloc(const void* I, const float* G, float* dK,
+                             int i_n, int i_h, int i_w, int i_c,
+                             int k_h, int k_w, int k_c, int s_h, int s_w,
+                             int dtype, void* stream);
 
 /* Static, NUL-terminated description of a status code (never NULL). */
 const char* mec_strerror(int status);

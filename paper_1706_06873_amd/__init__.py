@@ -24,7 +24,8 @@ __all__ = [
     "MecError", "F32", "BF16", "LOWERED", "FUSED", "IM2COL", "lib", "output_dims",
     "workspace_bytes", "im2col_bytes", "lower", "im2col", "gemm", "conv2d", "strerror",
     "GRAD_INPUT", "GRAD_KERNEL", "GRAD_KERNEL_FROM_L", "grad_workspace_bytes", "fold",
-    "dgrad_gemm", "conv2d_dgrad", "wgrad_gemm", "conv2d_wgrad",
+    "dgrad_gemm", "conv2d_dgrad", "wgrad_gemm", "conv2d_wgrad", "noalloc_scratch_bytes",
+    "conv2d_wgrad_noalloc",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -69,6 +70,10 @@ def _load(path):
     for name in ("mec_conv2d_dgrad", "mec_wgrad_gemm", "mec_conv2d_wgrad"):
         getattr(L, name).argtypes = [_vp, _vp, _vp, _vp, ctypes.c_size_t] + _DIMS + [_i, _vp]
         getattr(L, name).restype = _i
+    L.mec_noalloc_scratch_bytes.argtypes = []
+    L.mec_noalloc_scratch_bytes.restype = ctypes.c_int64
+    L.mec_conv2d_wgrad_noalloc.argtypes = [_vp, _vp, _vp] + _DIMS + [_i, _vp]
+    L.mec_conv2d_wgrad_noalloc.restype = _i
     L.mec_strerror.argtypes = [_i]
     L.mec_strerror.restype = ctypes.c_char_p
     L.mec_last_error.argtypes = []
@@ -414,4 +419,34 @@ def conv2d_wgrad(I, G, k_h, k_w, s_h=1, s_w=1, dK=None, workspace=None, stream=N
     workspace, wp, wb = _given_workspace(need, workspace, G)
     _check(lib.mec_conv2d_wgrad(_f32(I, "I"), _f32(G, "G"), _f32(dK, "dK"), wp, wb, *d, F32,
                                 _stream_handle(stream)), "mec_conv2d_wgrad")
+    return dK
+
+
+def noalloc_scratch_bytes():
+    """Bytes of the library's static device scratch (per GPU) that
+    conv2d_wgrad_noalloc keeps its partial sums in."""
+    return int(lib.mec_noalloc_scratch_bytes())
+
+
+def conv2d_wgrad_noalloc(I, G, k_h, k_w, s_h=1, s_w=1, dK=None, stream=None):
+    """dK = dloss/dK from I, as conv2d_wgrad, with the partial sums in the
+    library's static device scratch instead of a workspace: the C call
+    allocates nothing (for graph capture and serving loops; the caller passes
+    dK). Calls that overlap on one GPU race on the scratch."""
+    import torch
+    if I.dim() != 4 or G.dim() != 4:
+        raise ValueError("I must be i_n x i_h x i_w x i_c and G i_n x o_h x o_w x k_c")
+    i_n, i_h, i_w, i_c = I.shape
+    k_c = G.shape[3]
+    o_h, o_w = output_dims(i_h, i_w, k_h, k_w, s_h, s_w)
+    if tuple(G.shape) != (i_n, o_h, o_w, k_c):
+        raise ValueError("G must be i_n x o_h x o_w x k_c = %s" % ((i_n, o_h, o_w, k_c),))
+    _same_device(G, I, "G")
+    shape = (k_h, k_w, i_c, k_c)
+    if dK is None:
+        dK = torch.empty(shape, dtype=torch.float32, device=G.device)
+    _check_out(dK, shape, torch.float32, G, "dK")
+    _check(lib.mec_conv2d_wgrad_noalloc(_f32(I, "I"), _f32(G, "G"), _f32(dK, "dK"), i_n, i_h, i_w,
+                                        i_c, k_h, k_w, k_c, s_h, s_w, F32, _stream_handle(stream)),
+           "mec_conv2d_wgrad_noalloc")
     return dK

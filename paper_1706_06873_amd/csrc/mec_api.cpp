@@ -314,6 +314,29 @@ int mec_conv2d_wgrad(const void* I, const float* G, float* dK, void* workspace,
                       "wgrad products from I");
 }
 
+int64_t mec_noalloc_scratch_bytes(void) { return mec::kNoAllocScratchBytes; }
+
+int mec_conv2d_wgrad_noalloc(const void* I, const float* G, float* dK, int i_n, int i_h, int i_w,
+                             int i_c, int k_h, int k_w, int k_c, int s_h, int s_w, int dtype,
+                             void* stream) {
+    mec::Shape s;
+    int rc = grad_shape(s, i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w, dtype);
+    if (rc != MEC_OK) return rc;
+    if (!I || !G || !dK) return MEC_ERR_INVALID_ARG;
+    if (!aligned(I, 4) || !aligned(G, 4) || !aligned(dK, 4)) return MEC_ERR_ALIGNMENT;
+    if (!mec::wgrad_supported(s)) return MEC_ERR_UNSUPPORTED;
+    // the same partial sums as mec_conv2d_wgrad, in the static array
+    if (mec::wgrad_partial_bytes(s) > mec::kNoAllocScratchBytes) return MEC_ERR_SCRATCH;
+    const hipStream_t st = (hipStream_t)stream;
+    clear_stale_error();
+    void* part = nullptr;
+    rc = hip_status(mec::noalloc_scratch(st, &part), "address of the static scratch");
+    if (rc != MEC_OK) return rc;
+    return hip_status(mec::launch_wgrad(s, static_cast<const float*>(I), G, static_cast<float*>(part), dK,
+                                        st, true),
+                      "wgrad products from I, partial sums in the static scratch");
+}
+
 const char* mec_strerror(int status) {
     switch (status) {
         case MEC_OK: return "success";
@@ -322,6 +345,7 @@ const char* mec_strerror(int status) {
         case MEC_ERR_ALIGNMENT: return "pointer not aligned to its element size";
         case MEC_ERR_HIP: return "HIP runtime error at kernel launch";
         case MEC_ERR_UNSUPPORTED: return "shape beyond this build's kernel limits";
+        case MEC_ERR_SCRATCH: return "the call needs more than the library's static scratch holds";
         default: return "unknown status";
     }
 }

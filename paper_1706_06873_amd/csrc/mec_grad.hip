@@ -41,6 +41,8 @@
 //            depend on scheduling.
 // Global loads of the next stage go to registers before the current stage's
 // MFMAs and to LDS after them.
+#include <mutex>
+
 #include "mec_mfma.h"
 
 namespace mec {
@@ -1067,6 +1069,47 @@ hipError_t launch_dgrad_phases(const Shape& s, const float* G, const float* K, f
             e = launch_gemm(t, Gp, Kp, dI, 0, true, stream, unit ? nullptr : &o);
             if (e != hipSuccess) return e;
         }
+    return hipSuccess;
+}
+
+// ---------------------------------------------------------------- no-alloc weight gradient
+// The partial sums of the weight gradient in a static device array instead of
+// a caller's workspace, for callers that cannot allocate device memory. Each
+// GPU the library runs on holds its own copy until the process ends. Host code
+// never passes `scratch` itself to a kernel (in host code the name is a
+// host-side stand-in, not a device address): it uses the address that
+// hipGetSymbolAddress returns for the stream's device, taken once per device
+// with that device current.
+static __device__ __align__(256) float scratch[kNoAllocScratchBytes / sizeof(float)];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];  // per device, set once under g_scratch_mu
+}  // namespace
+
+hipError_t noalloc_scratch(hipStream_t stream, void** ptr) {
+    int dev = 0;
+    hipError_t e = hipStreamGetDevice(stream, &dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        int cur = 0;
+        e = hipGetDevice(&cur);
+        if (e != hipSuccess) return e;
+        if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return e;
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (cur != dev) {
+            const hipError_t e2 = hipSetDevice(cur);
+            if (e == hipSuccess) e = e2;
+        }
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        g_scratch_ptr[dev] = p;
+    }
+    *ptr = g_scratch_ptr[dev];
     return hipSuccess;
 }
 

@@ -143,6 +143,11 @@ int64_t wgrad_partial_bytes(const Shape& s);
 // fused: the kernels read the rows of L from I (the L argument is I then).
 hipError_t launch_wgrad(const Shape& s, const float* L, const float* G, float* part, float* dK,
                         hipStream_t stream, bool fused = false);
+// The static device array that mec_conv2d_wgrad_noalloc uses for the partial
+// sums: its size, and its address on the stream's device (looked up once per
+// device; no allocation).
+constexpr int64_t kNoAllocScratchBytes = int64_t(64) << 20;
+hipError_t noalloc_scratch(hipStream_t stream, void** ptr);
 
 }  // namespace mec
 
