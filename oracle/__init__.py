@@ -42,9 +42,9 @@ def _load(path):
     L.oracle_mec_lower.restype = None
     L.oracle_im2col.argtypes = [vp, vp] + _DIMS + [ctypes.c_int]
     L.oracle_im2col.restype = None
-    L.oracle_mec_gemm.argtypes = [vp, vp, dp] + _DIMS + [ctypes.c_int, ctypes.c_int]
-    L.oracle_mec_gemm.restype = ctypes.c_int
-    L.oracle_mec_conv2d.argtypes = [vp, vp, dp] + _DIMS + [ctypes.c_int, _i64]
+    L.oracle_mec_gemm.argtypes = [vp, vp, dp] + _DIMS + [ctypes.c_int]
+    L.oracle_mec_gemm.restype = None
+    L.oracle_mec_conv2d.argtypes = [vp, vp, dp] + _DIMS + [ctypes.c_int]
     L.oracle_mec_conv2d.restype = ctypes.c_int
     L.oracle_vanilla_mec.argtypes = [vp, vp, dp, vp] + [_i64] * 6
     L.oracle_vanilla_mec.restype = None
@@ -159,34 +159,34 @@ def im2col(I, k_h, k_w, s_h, s_w):
     return M
 
 
-def mec_gemm(L, K, i_h, i_w, s_h, s_w, solution="A"):
-    """MEC product phase on a lowered L with Solution 'A' or 'B' (fp64 O)."""
+def mec_gemm(L, K, i_h, i_w, s_h, s_w):
+    """MEC product phase on a lowered L, from its definition (fp64 O, n-h-w-c):
+    O[n, h, w, m] = sum_j L[n, w][s_h*R*h + j] * K[j, m]."""
     i_n, o_w, i_h2, k_w, i_c = L.shape
     assert i_h2 == i_h
     k_h, k_w2, i_c2, k_c = K.shape
     assert (k_w2, i_c2) == (k_w, i_c)
     o_h = out_dim(i_h, k_h, s_h)
     O = np.empty((i_n, o_h, o_w, k_c), np.float64)
-    rc = lib().oracle_mec_gemm(_ptr(L), _ptr(K), _dptr(O), i_n, i_h, i_w, i_c, k_h, k_w, k_c,
-                               s_h, s_w, _dtype_code(L), ord(solution))
-    if rc != 0:
-        raise RuntimeError("oracle_mec_gemm failed (%d)" % rc)
+    lib().oracle_mec_gemm(_ptr(L), _ptr(K), _dptr(O), i_n, i_h, i_w, i_c, k_h, k_w, k_c,
+                          s_h, s_w, _dtype_code(L))
     return O
 
 
-def mec_conv2d(I, K, s_h, s_w, T=100):
-    """Algorithm 2 end to end (lowering, then Solution A or B by T)."""
+def mec_conv2d(I, K, s_h, s_w):
+    """MEC end to end: the compact lowering, then the product phase (fp64 O)."""
     d = _dims(I, K, s_h, s_w)
     o_h, o_w = out_dim(d[1], d[4], s_h), out_dim(d[2], d[5], s_w)
     O = np.empty((d[0], o_h, o_w, d[6]), np.float64)
-    rc = lib().oracle_mec_conv2d(_ptr(I), _ptr(K), _dptr(O), *d, _dtype_code(I), T)
+    rc = lib().oracle_mec_conv2d(_ptr(I), _ptr(K), _dptr(O), *d, _dtype_code(I))
     if rc != 0:
         raise RuntimeError("oracle_mec_conv2d failed (%d)" % rc)
     return O
 
 
 def vanilla_mec(I, K, s_h, s_w):
-    """Algorithm 1 (i_n = i_c = k_c = 1): returns (O fp64 o_h x o_w, L fp32)."""
+    """MEC for one image and one channel (Section 3.2, Algorithm 1's case
+    i_n = i_c = k_c = 1): returns (O fp64 o_h x o_w, L fp32)."""
     I = np.ascontiguousarray(I, np.float32)
     K = np.ascontiguousarray(K, np.float32)
     i_h, i_w = I.shape

@@ -178,10 +178,10 @@ void oracle_mec_lower(const void* I, void* L,
             }
 }
 
-/* Algorithm 1 (VanillaMEC), the single-image, single-channel case
- * i_n = i_c = k_c = 1. L is o_w x i_h x k_w; then output row h is
- * L[0:o_w, s_h*k_w*h : s_h*k_w*h + k_h*k_w] times K viewed as a
- * (k_h*k_w) x 1 matrix, the sub-matrix taken with leading dimension i_h*k_w.
+/* MEC for one image and one channel, i_n = i_c = k_c = 1 (Section 3.2,
+ * the case Algorithm 1 states): L is o_w x i_h x k_w, and output pixel (h, w)
+ * is the dot product of the k_h*k_w-element window of row w of L that starts
+ * at s_h*k_w*h with K read row by row.
  * I is i_h x i_w fp32, K is k_h x k_w fp32, O is o_h x o_w fp64;
  * Lout (o_w*i_h*k_w fp32) receives the lowered matrix. */
 void oracle_vanilla_mec(const float* I, const float* K, double* O, float* Lout,
@@ -206,91 +206,54 @@ void oracle_vanilla_mec(const float* I, const float* K, double* O, float* Lout,
         }
 }
 
-/* MEC's matrix-multiplication phase on an already lowered L (Algorithm 2,
- * from the point where K is viewed as a (k_h*k_w*i_c) x k_c matrix).
- * Let R = k_w*i_c, KD = k_h*R and LD = i_h*R (one row of L viewed as an
- * (i_n*o_w) x (i_h*k_w*i_c) matrix). The sub-matrix for output row h
- * starts at column s_h*R*h and is KD wide.
- *
- * solution 'A': o_h products over all i_n*o_w rows at once, giving O in
- *   h-n-w-c order; then the n-h-w-c order is recovered by copying the
- *   intermediate out and writing O[n,h,:] = tmp[h,n,:]. The paper reuses
- *   the storage of L for that intermediate; a separate fp64 buffer is used
- *   here, which changes no value.
- * solution 'B': i_n*o_h products, one per image and output row, each over
- *   o_w rows, giving n-h-w-c directly.
- * O receives fp64 n-h-w-c. Returns 0, or -1 if the scratch allocation fails
- * or solution is neither 'A' nor 'B'. */
-int oracle_mec_gemm(const void* L, const void* K, double* O,
-                    int64_t i_n, int64_t i_h, int64_t i_w, int64_t i_c,
-                    int64_t k_h, int64_t k_w, int64_t k_c,
-                    int64_t s_h, int64_t s_w, int dtype, int solution)
+/* MEC's product phase on an already lowered L, from its definition in
+ * Section 3.3 (and Section 3.2 for one channel). With R = k_w*i_c and
+ * LD = i_h*R, row (n, w) of L is an LD-element vector; output row h of that
+ * pair multiplies the contiguous window of k_h*R elements starting at
+ * s_h*R*h (the "slab") by K viewed as a (k_h*k_w*i_c) x k_c matrix:
+ *   O[n, h, w, m] = sum_{j < k_h*R} L[n, w][s_h*R*h + j] * K[j, m].
+ * The result is written straight in n-h-w-c order. How the products are
+ * grouped into matrix calls (Solutions A and B, the threshold T) and the
+ * transposition Solution A needs do not change any value, so none of that
+ * appears here. O receives fp64. */
+void oracle_mec_gemm(const void* L, const void* K, double* O,
+                     int64_t i_n, int64_t i_h, int64_t i_w, int64_t i_c,
+                     int64_t k_h, int64_t k_w, int64_t k_c,
+                     int64_t s_h, int64_t s_w, int dtype)
 {
     int64_t o_h = oracle_out_dim(i_h, k_h, s_h);
     int64_t o_w = oracle_out_dim(i_w, k_w, s_w);
-    int64_t R = k_w * i_c, KD = k_h * R, LD = i_h * R;
-
-    if (solution == 'A') {
-        int64_t rows = i_n * o_w; /* the (i_n*o_w) x KD sub-matrix */
-        double* tmp = (double*)malloc((size_t)(o_h * rows * k_c) * sizeof(double));
-        if (!tmp) return -1;
-        /* O viewed as o_h x (i_n*o_w*k_c): row h = L[0:rows, s_h*R*h : +KD] x K */
-#pragma omp parallel for schedule(static)
+    int64_t R = k_w * i_c, LD = i_h * R;
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t n = 0; n < i_n; ++n)
         for (int64_t h = 0; h < o_h; ++h)
-            for (int64_t r = 0; r < rows; ++r)
+            for (int64_t w = 0; w < o_w; ++w) {
+                int64_t row = (n * o_w + w) * LD;   /* row (n, w) of L */
+                int64_t start = s_h * R * h;        /* first element of output row h's slab */
                 for (int64_t m = 0; m < k_c; ++m) {
                     double acc = 0.0;
-                    for (int64_t j = 0; j < KD; ++j)
-                        acc += elem(L, r * LD + s_h * R * h + j, dtype) * elem(K, j * k_c + m, dtype);
-                    tmp[(h * rows + r) * k_c + m] = acc;
+                    for (int64_t j = 0; j < k_h * R; ++j)
+                        acc += elem(L, row + start + j, dtype) * elem(K, j * k_c + m, dtype);
+                    O[((n * o_h + h) * o_w + w) * k_c + m] = acc;
                 }
-        /* h-n-w-c to n-h-w-c: O[n, h, 0:o_w*k_c] = tmp[h, n, 0:o_w*k_c] */
-        int64_t chunk = o_w * k_c;
-#pragma omp parallel for collapse(2) schedule(static)
-        for (int64_t n = 0; n < i_n; ++n)
-            for (int64_t h = 0; h < o_h; ++h)
-                memcpy(O + (n * o_h + h) * chunk, tmp + (h * i_n + n) * chunk,
-                       (size_t)chunk * sizeof(double));
-        free(tmp);
-        return 0;
-    }
-    if (solution == 'B') {
-        /* L viewed as i_n matrices of o_w x LD; O as i_n matrices of o_h x (o_w*k_c) */
-#pragma omp parallel for collapse(2) schedule(static)
-        for (int64_t n = 0; n < i_n; ++n)
-            for (int64_t h = 0; h < o_h; ++h)
-                for (int64_t w = 0; w < o_w; ++w)
-                    for (int64_t m = 0; m < k_c; ++m) {
-                        double acc = 0.0;
-                        for (int64_t j = 0; j < KD; ++j)
-                            acc += elem(L, (n * o_w + w) * LD + s_h * R * h + j, dtype) *
-                                   elem(K, j * k_c + m, dtype);
-                        O[((n * o_h + h) * o_w + w) * k_c + m] = acc;
-                    }
-        return 0;
-    }
-    return -1;
+            }
 }
 
-/* The whole of Algorithm 2: allocate L, lower, then take Solution A when
- * o_w <= T and |O| <= |L|, else Solution B. O receives fp64 n-h-w-c.
- * Returns 0, or -1 on allocation failure. */
+/* MEC end to end (Section 3.3): the compact lowering of I into L, then the
+ * product phase above. O receives fp64 n-h-w-c. Returns 0, or -1 if L cannot
+ * be allocated. */
 int oracle_mec_conv2d(const void* I, const void* K, double* O,
                       int64_t i_n, int64_t i_h, int64_t i_w, int64_t i_c,
                       int64_t k_h, int64_t k_w, int64_t k_c,
-                      int64_t s_h, int64_t s_w, int dtype, int64_t T)
+                      int64_t s_h, int64_t s_w, int dtype)
 {
-    int64_t o_h = oracle_out_dim(i_h, k_h, s_h);
-    int64_t o_w = oracle_out_dim(i_w, k_w, s_w);
     int64_t nL = oracle_lowered_elems(i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w);
-    int64_t nO = i_n * o_h * o_w * k_c;
     void* L = malloc((size_t)(nL * elem_bytes(dtype)));
     if (!L) return -1;
     oracle_mec_lower(I, L, i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w, dtype);
-    int sol = (o_w <= T && nO <= nL) ? 'A' : 'B';
-    int rc = oracle_mec_gemm(L, K, O, i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w, dtype, sol);
+    oracle_mec_gemm(L, K, O, i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w, dtype);
     free(L);
-    return rc;
+    return 0;
 }
 
 /* im2col lowering of Section 3.1 / Fig. 1(b), the comparison point for

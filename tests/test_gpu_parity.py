@@ -597,7 +597,7 @@ def test_workspace_holds_L_and_gemm_alone(orc, dims):
     assert np.array_equal(ws.cpu().numpy().view(np.float32).reshape(ref_L.shape), ref_L)
     # the product phase alone, on the oracle's L
     O2 = mec.gemm(to_dev(torch.from_numpy(ref_L)), to_dev(K), dims[1], dims[2], s_h, s_w)
-    ref = orc.mec_gemm(ref_L, host(K), dims[1], dims[2], s_h, s_w, "B")
+    ref = orc.mec_gemm(ref_L, host(K), dims[1], dims[2], s_h, s_w)
     torch.cuda.synchronize()
     assert rel_l2(O2.cpu().numpy(), ref) <= TOL_F32
     assert np.array_equal(O2.cpu().numpy(), O.cpu().numpy())

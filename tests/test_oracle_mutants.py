@@ -2,7 +2,7 @@
 
 Each case copies the oracle's C source, makes one plausible mistake in it (a
 flipped or transposed kernel index, a swapped stride, a dropped term, a wrong
-lowering offset, a missing transpose, a narrower accumulator, a wrong bf16
+lowering offset, a wrong slab offset or row, a short slab, a narrower accumulator, a wrong bf16
 widening, and in the training passes a flipped kernel row, a swapped stride,
 a fold or slab offset without its stride), builds the copy with gcc and runs
 the pin battery of test_oracle_pins.py and test_oracle_training.py against it. At least one pin must fail. Every mutant keeps
@@ -34,10 +34,10 @@ MUTANTS = {
                                "int64_t src = ((n * i_h + h) * i_w + w) * i_c;"),
     "lower_rows_transposed": ("int64_t dst = (((n * o_w + w) * i_h + h) * k_w) * i_c;  /* L[n, w, h, 0, 0] */",
                               "int64_t dst = (((n * i_h + h) * o_w + w) * k_w) * i_c;"),
-    "slab_offset_without_channels": ("acc += elem(L, r * LD + s_h * R * h + j, dtype)",
-                                     "acc += elem(L, r * LD + s_h * k_w * h + j, dtype)"),
-    "solution_a_not_transposed": ("memcpy(O + (n * o_h + h) * chunk, tmp + (h * i_n + n) * chunk,",
-                                  "memcpy(O + (n * o_h + h) * chunk, tmp + (n * o_h + h) * chunk,"),
+    "slab_offset_without_channels": ("int64_t start = s_h * R * h;", "int64_t start = s_h * k_w * h;"),
+    "slab_rows_transposed": ("int64_t row = (n * o_w + w) * LD;", "int64_t row = (w * i_n + n) % (i_n * o_w) * LD;"),
+    "slab_one_row_short": ("for (int64_t j = 0; j < k_h * R; ++j)\n                        acc += elem(L, row + start + j",
+                           "for (int64_t j = 0; j < (k_h - 1) * R + (k_h == 1) * R; ++j)\n                        acc += elem(L, row + start + j"),
     "float_accumulator": ("double acc = 0.0;\n                    for (int64_t a = 0; a < k_h; ++a)",
                           "float acc = 0.0f;\n                    for (int64_t a = 0; a < k_h; ++a)"),
     "bf16_widen_wrong": ("uint32_t bits = (uint32_t)((const uint16_t*)base)[idx] << 16;",
