@@ -797,8 +797,9 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_f32_stream_kernel(FixedP
 // chunk ahead through two. Stages are unpadded and their 16-byte granules
 // permuted so that fragment reads spread over the banks:
 //   A [x][pair][32 r]      granule g of row q at g ^ ((q >> 2) & 3)
-//   B [a][32 r][channel]   K's own layout; granule g of row r at g ^ (r & 8 ? 4 : 0)
-// A B fragment (8 consecutive r of one channel) is gathered by 16-bit reads.
+//   B [a][32 r][channel]   K's own layout; granule g of row r at g ^ (2 (r % 4) | (r & 8))
+// A B fragment (8 consecutive r of one channel) is two transposing LDS reads
+// (ds_read_b64_tr_b16, 4 rows each).
 // Needs R % 32 == 0, so that no chunk holds a partial row.
 template <int HT, int NB, int WAVES_H, int KT, int KH, int SH, bool FUSED, int WAVES = 4,
           bool VECA = true, bool DMA = false>
@@ -835,7 +836,7 @@ struct BF16Cfg {
     static constexpr size_t LDS_BYTES = LDS_HALVES * sizeof(E);
     static_assert(WAVES % WAVES_H == 0 && HT % WAVES_H == 0 && NB % WAVES_N == 0, "wave split");
     static_assert(KT % 16 == 0, "chunk");
-    static_assert(!DMA || (KT == 32 && VECA && NB % 4 == 0 && ADMA * 8 * THREADS == A_SIZE &&
+    static_assert(!DMA || (KT == 32 && VECA && NB == 4 && ADMA * 8 * THREADS == A_SIZE &&
                            BDMA * 8 * THREADS == B_SIZE && ADMA + BDMA < 16), "DMA stage");
     static_assert(LDS_BYTES + 1024 <= 160 * 1024, "LDS");
 };
@@ -961,7 +962,7 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_bf16_kernel(FixedParams 
         for (int j = 0; j < C::BDMA; ++j) {
             const int G = (j * C::kWaves + wave) * 64 + lane;
             const int q = G >> 4, r = q % KT, a = q / KT;
-            const int g = (G & 15) ^ (r & 8 ? 4 : 0);
+            const int g = (G & 15) ^ (((r & 3) << 1) | (r & 8));
             const int nc = n0 + 8 * g < p.k_c ? n0 + 8 * g : n0;
             bdma[j] = (uint32_t)(2 * (((int64_t)a * p.R + r) * p.k_c + nc));
         }
@@ -1061,13 +1062,21 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_bf16_kernel(FixedParams 
     const int swz = (lane >> 2) & 3;
     const int a_dma0 = a_row + 8 * ((lane >> 5) ^ swz);
     const int a_dma1 = a_row + 8 * ((2 + (lane >> 5)) ^ swz);
-    // DMA: a lane's B element (r = kofs + t, channel ch) at (r * NT + granule * 8
-    // + ch % 8); r & 8 is (lane >> 5) * 8 for both k-steps
-    int b_dma[NBW];
+    // DMA: B fragments by transposing reads. ds_read_b64_tr_b16 gives lane j of
+    // each 16-lane group the elements 4k + (j / 4), j % 4 (k = 0..3) of the
+    // 8-byte pieces its 16 lanes address; lane i of a group addresses row
+    // r0 + i / 4 at channel c0 + 4 (i % 4), so lane j receives rows r0..r0+3 of
+    // channel c0 + j: half of its fragment (k = 8 (lane / 32) + 0..3; the
+    // second read takes rows r0 + 4..7). Row r's 16-byte granule g sits at
+    // g ^ (2 (r % 4) | (r & 8)): the four rows of one read and the two lane
+    // halves land on distinct banks.
+    int b_tr[NBW];
 #pragma unroll
     for (int nb = 0; nb < NBW; ++nb) {
-        const int ch = (wn * NBW + nb) * 32 + row;
-        b_dma[nb] = kofs * NT + (((ch >> 3) ^ ((lane >> 5) * 4)) * 8) + (ch & 7);
+        const int i = lane & 15;
+        const int ch = (wn * NBW + nb) * 32 + 16 * ((lane >> 4) & 1) + 4 * (i & 3);
+        const int swzb = ((i >> 2) << 1) | (8 * (lane >> 5));
+        b_tr[nb] = (kofs + (i >> 2)) * NT + (((ch >> 3) ^ swzb) << 3) + (ch & 7);
     }
 
     auto compute = [&](int abuf, int bbuf, auto mid) {
@@ -1089,12 +1098,14 @@ __global__ __launch_bounds__(C::THREADS) void slab_gemm_bf16_kernel(FixedParams 
 #pragma unroll
                 for (int nb = 0; nb < NBW; ++nb) {
                     if constexpr (C::kDMA) {
-                        const uint16_t* src = b_stage(bbuf) + b_dma[nb] + (a * KT + kk) * NT;
-                        uint32_t w[4];
-#pragma unroll
-                        for (int k = 0; k < 4; ++k)
-                            w[k] = (uint32_t)src[(2 * k) * NT] | ((uint32_t)src[(2 * k + 1) * NT] << 16);
-                        bf[a][nb] = __builtin_bit_cast(bf16x8, make_uint4(w[0], w[1], w[2], w[3]));
+                        typedef short short4v __attribute__((ext_vector_type(4)));
+                        typedef __attribute__((address_space(3))) short4v lds_short4v;
+                        const uint16_t* src = b_stage(bbuf) + b_tr[nb] + (a * KT + kk) * NT;
+                        const short4v lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4v*)src);
+                        const short4v hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4v*)(src + 4 * NT));
+                        typedef short short8v __attribute__((ext_vector_type(8)));
+                        const short8v v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+                        bf[a][nb] = __builtin_bit_cast(bf16x8, v);
                     } else {
                         bf[a][nb] = __builtin_bit_cast(
                             bf16x8, *reinterpret_cast<const uint4*>(Bs + (a * NT + nb * 32) * KTP + kk));
