@@ -48,5 +48,7 @@ class HipEvent:
         return ms.value
 
     def __del__(self):
-        if HipEvent._rt is not None and self.h:
-            HipEvent._rt.hipEventDestroy(self.h)
+        # at interpreter exit the class may already be torn down
+        rt = getattr(HipEvent, "_rt", None) if HipEvent is not None else None
+        if rt is not None and self.h:
+            rt.hipEventDestroy(self.h)
