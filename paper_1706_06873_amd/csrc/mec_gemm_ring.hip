@@ -37,6 +37,7 @@ constexpr int kRingLen = kChunk * kRingChunks;
 // a fragment read of 8 pairs x 4 rows spreads over the banks
 constexpr int kRingLD = kRingLen + 124;
 constexpr int kBlockSteps = 8;             // k-steps between fill points
+constexpr int kWavesPerCU = 8;             // resident waves per compute unit (LDS: 8 rings)
 
 struct RingParams {
     const float* A;   // L (lowered) or I (fused)
@@ -53,7 +54,7 @@ struct RingParams {
     int32_t gpi;             // row groups per item
     int32_t items_pg;        // items per pair group: ceil(ngroups / gpi)
     int32_t n_tiles;         // channel tiles of 32*NB
-    uint32_t nitems;         // pair groups x items_pg x n_tiles
+    uint32_t nfull;          // whole items: (pair group, items_pg) x n_tiles, or fewer (below)
     FastDiv divR;
     FastDiv div_ow;          // pair -> (image, column); pairs < 2^31
 };
@@ -71,22 +72,14 @@ __device__ inline void ring_dma(const float* base, uint32_t voff, uint32_t lds) 
         : "memory");
 }
 
+// One piece of work: row groups g_begin .. g_end-1 of the 8 pairs from pair0,
+// channels n0 .. n0 + 32*NB.
 template <int NB, bool FUSED>
-__global__ __launch_bounds__(64) void slab_gemm_f32_ring_kernel(RingParams p) {
-    __shared__ __align__(16) float ring[kRPairs * kRingLD];
-
+__device__ __forceinline__ void ring_item(const RingParams& p, float* ring, int64_t pair0, int g_begin,
+                                          int g_end, int n0) {
     const int lane = threadIdx.x;
     const int m = lane & 31, kofs = lane >> 5;
     const int pp = m & 7, ii = m >> 3;  // this lane's A row: pair pp, output row ii
-
-    const uint32_t t_item = xcd_remap(blockIdx.x, p.nitems);
-    const uint32_t nt = t_item % (uint32_t)p.n_tiles;
-    const uint32_t rest = t_item / (uint32_t)p.n_tiles;
-    const uint32_t ig = rest % (uint32_t)p.items_pg;
-    const int64_t pair0 = (int64_t)(rest / (uint32_t)p.items_pg) * kRPairs;
-    const int g_begin = (int)ig * p.gpi;
-    const int g_end = g_begin + p.gpi < p.ngroups ? g_begin + p.gpi : p.ngroups;
-    const int n0 = (int)nt * 32 * NB;
 
     // Source of each pair's row of L: element o of pair q's row is at
     // srcq[q] + (o / R) * x_stride + o % R (lowered: x_stride = R, so srcq[q] + o).
@@ -270,6 +263,68 @@ __global__ __launch_bounds__(64) void slab_gemm_f32_ring_kernel(RingParams p) {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
+// Items 0 .. nfull-1 whole (gpi row groups, all NB channel blocks of their
+// channel tile), in an XCD-contiguous order; then, dispatched last, the
+// remaining items split into one workgroup per row group and 32-channel
+// block: when the whole items leave a last, partial round on the wave slots,
+// its items would otherwise run alone at the end while the other slots idle
+// (alexnet_conv1: 12320 one-group items on 2048 slots leave 32).
+template <int NB, bool FUSED>
+__global__ __launch_bounds__(64) void slab_gemm_f32_ring_kernel(RingParams p) {
+    __shared__ __align__(16) float ring[kRPairs * kRingLD];
+    if (blockIdx.x < p.nfull) {
+        const uint32_t t = xcd_remap(blockIdx.x, p.nfull);
+        const uint32_t unit = t / (uint32_t)p.n_tiles;
+        const int g_begin = (int)(unit % (uint32_t)p.items_pg) * p.gpi;
+        const int g_end = g_begin + p.gpi < p.ngroups ? g_begin + p.gpi : p.ngroups;
+        ring_item<NB, FUSED>(p, ring, (int64_t)(unit / (uint32_t)p.items_pg) * kRPairs, g_begin, g_end,
+                             (int)(t % (uint32_t)p.n_tiles) * 32 * NB);
+    } else {
+        // one channel tile (n_tiles == 1): piece = (item, group of the item, channel block)
+        const uint32_t piece = blockIdx.x - p.nfull;
+        const uint32_t per = (uint32_t)(p.gpi * NB);
+        const uint32_t unit = p.nfull + piece / per, sub = piece % per;
+        const int g = (int)(unit % (uint32_t)p.items_pg) * p.gpi + (int)(sub / NB);
+        if (g < p.ngroups)
+            ring_item<1, FUSED>(p, ring, (int64_t)(unit / (uint32_t)p.items_pg) * kRPairs, g, g + 1,
+                                (int)(sub % NB) * 32);
+    }
+}
+
+struct RingPlan {
+    int gpi;                 // row groups per item
+    int64_t nfull, npieces;  // whole items, then single-group single-block pieces
+};
+
+// The launch's layout: gpi row groups per item, and the items of a last,
+// partial round on the wave slots split into one workgroup per row group and
+// 32-channel block when they are few (at most a quarter of the slots) and
+// there is something to split (one channel tile of several blocks, or items
+// of two groups). Two groups per item halve the items' start-ups (the first
+// chunks are loaded before the first product) and are taken when every slot
+// still gets an item and the estimated time, in rounds of the slots, is not
+// longer than with one (alexnet_conv1: 6160 two-group items, 16 of them
+// split, against 12320 one-group items, 32 of them split: 1% faster).
+RingPlan ring_plan(int64_t pgroups, int ngroups, int n_tiles, int nb, int64_t slots) {
+    RingPlan best{1, pgroups * ngroups * n_tiles, 0};
+    if (slots <= 0) return best;
+    int64_t best_cost = -1;
+    for (int gpi = 1; gpi <= 2; ++gpi) {
+        if (gpi > 1 && ngroups < 2) break;
+        const int64_t items = pgroups * ((ngroups + gpi - 1) / gpi) * n_tiles;
+        const int64_t rounds = items / slots, r = items % slots;
+        if (gpi > 1 && rounds == 0) break;  // would leave slots without an item
+        const bool split = n_tiles == 1 && nb * gpi > 1 && rounds > 0 && r > 0 && 4 * r <= slots;
+        // in units of one 32-channel block of one row group
+        const int64_t cost = rounds * gpi * nb + (r == 0 ? 0 : split ? 1 : gpi * nb);
+        if (best_cost < 0 || cost <= best_cost) {
+            best = {gpi, split ? items - r : items, split ? r * nb * gpi : 0};
+            best_cost = cost;
+        }
+    }
+    return best;
+}
+
 }  // namespace
 
 bool gemm_ring_usable(const Shape& s, int dtype) {
@@ -309,19 +364,25 @@ hipError_t launch_gemm_ring(const Shape& s, const void* A, const void* K, float*
     p.nks = ((p.KR + 1) / 2 + kBlockSteps - 1) / kBlockSteps * kBlockSteps;
     p.srow = (int32_t)(s.s_h * s.R);
     p.ngroups = (int32_t)((s.o_h + kRRows - 1) / kRRows);
-    // one row group per workgroup: more, shorter items balance the compute units
-    // better at the end of the launch than two per item (alexnet_conv1: 7%)
-    p.gpi = 1;
-    p.items_pg = (p.ngroups + p.gpi - 1) / p.gpi;
     p.divR = FastDiv((uint32_t)s.R);
     p.div_ow = FastDiv((uint32_t)s.o_w);
     const int nb = s.k_c > 64 ? 3 : s.k_c > 32 ? 2 : 1;
     p.n_tiles = (int32_t)((s.k_c + 32 * nb - 1) / (32 * nb));
     const int64_t pgroups = (s.pairs + kRPairs - 1) / kRPairs;
-    const int64_t nitems = pgroups * p.items_pg * p.n_tiles;
-    if (nitems > 0x7fffffff) return hipErrorInvalidValue;
-    p.nitems = (uint32_t)nitems;
-    const dim3 grid(p.nitems), block(64);
+    int64_t slots = 0;  // wave slots of the stream's device: eight per compute unit
+    {
+        int dev = 0, cus = 0;
+        if (hipStreamGetDevice(stream, &dev) == hipSuccess &&
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && cus > 0)
+            slots = (int64_t)kWavesPerCU * cus;
+    }
+    const RingPlan plan = ring_plan(pgroups, p.ngroups, p.n_tiles, nb, slots);
+    if (plan.nfull + plan.npieces > 0x7fffffff) return hipErrorInvalidValue;
+    p.gpi = plan.gpi;
+    p.items_pg = (p.ngroups + p.gpi - 1) / p.gpi;
+    p.nfull = (uint32_t)plan.nfull;
+    const int64_t nfull = plan.nfull, npieces = plan.npieces;
+    const dim3 grid((uint32_t)(nfull + npieces)), block(64);
 #define MEC_RING(NB_)                                                                         \
     if (nb == NB_) {                                                                          \
         if (fused)                                                                            \

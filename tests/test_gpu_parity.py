@@ -368,6 +368,60 @@ def test_ring_products(orc, dims, algo):
     assert rel_l2(run_conv(I, K, s_h, s_w, algo), orc.conv2d_direct(host(I), host(K), s_h, s_w)) <= TOL_F32
 
 
+def ring_plan(pgroups, ngroups, n_tiles, nb, slots):
+    """The ring launch's layout as the library chooses it: (row groups per
+    item, whole items, split pieces). Two groups per item when every slot
+    still gets an item and the estimated time in rounds of the slots is not
+    longer; the items of a last, partial round of at most a quarter of the
+    slots split into one workgroup per row group and 32-channel block."""
+    best, best_cost = (1, pgroups * ngroups * n_tiles, 0), None
+    for gpi in (1, 2):
+        if gpi > 1 and ngroups < 2:
+            break
+        items = pgroups * -(-ngroups // gpi) * n_tiles
+        rounds, r = divmod(items, slots)
+        if gpi > 1 and rounds == 0:
+            break
+        split = n_tiles == 1 and nb * gpi > 1 and rounds > 0 and r > 0 and 4 * r <= slots
+        cost = rounds * gpi * nb + (0 if r == 0 else 1 if split else gpi * nb)
+        if best_cost is None or cost <= best_cost:
+            best, best_cost = (gpi, items - r if split else items, r * nb * gpi if split else 0), cost
+    return best
+
+
+def ring_split_batch(slots, o_h, o_w, k_c, gpi):
+    """Smallest batch whose ring launch has `gpi` row groups per item and
+    splits at least 5 leftover items."""
+    nb = 3 if k_c > 64 else 2 if k_c > 32 else 1
+    for n in range(1, 8 * slots):
+        plan = ring_plan(-(-n * o_w // 8), -(-o_h // 4), -(-k_c // (32 * nb)), nb, slots)
+        if plan[0] == gpi and plan[2] >= 5 * nb * gpi:
+            return n, plan
+    raise AssertionError("no batch")
+
+
+@pytest.mark.parametrize("gpi", [1, 2])
+@pytest.mark.parametrize("k_c", [96, 40])
+@pytest.mark.parametrize("algo", ["lowered", "fused"])
+def test_ring_split_tail(orc, gpi, k_c, algo):
+    """The items past the last whole round of the wave slots (eight waves per
+    compute unit) run one row group and 32-channel block per workgroup: full
+    output compared bit for bit with integer inputs, at batches sized from the
+    device's compute units so that such a remainder exists, with items of one
+    row group (o_h = 10: three groups, the last one half full) and of two
+    (o_h = 7: two groups, the second one three rows). o_w = 7 puts pair
+    groups across images."""
+    slots = 8 * torch.cuda.get_device_properties(0).multi_processor_count
+    o_h = 10 if gpi == 1 else 7
+    n, plan = ring_split_batch(slots, o_h, 7, k_c, gpi)
+    dims = (n, 4 * o_h + 7, 35, 3, 11, 11, k_c, 4, 4)
+    say("ring split tail", algo, dims, "plan", plan)
+    I, K = case(83 + k_c + gpi, dims, dist="int")
+    ref = orc.conv2d_direct(host(I), host(K), 4, 4)
+    assert np.abs(ref).max() < 2 ** 24
+    assert np.array_equal(run_conv(I, K, 4, 4, algo), ref.astype(np.float32))
+
+
 @pytest.mark.parametrize("shift", [1, 3])
 def test_ring_unaligned_and_guarded(orc, shift):
     """I, K, L and O one or three elements off their 16-byte boundaries, O
