@@ -163,6 +163,19 @@ __device__ inline uint32_t xcd_remap(uint32_t b, uint32_t G) {
     return xcd * base + (xcd < rem ? xcd : rem) + slot;
 }
 
+// Block index remapped so that the 8 XCDs take turns over runs of g
+// consecutive logical blocks: XCD x processes runs x, x + 8, x + 16, ...
+// The blocks of one run share an XCD's L2 cache, while the blocks in flight
+// across the chip cover one compact range of the work (and of the memory it
+// writes) instead of eight ranges far apart. Blocks past the last whole round
+// of 8 runs keep their own index. A bijection on [0, G).
+__device__ inline uint32_t xcd_interleave(uint32_t b, uint32_t G, uint32_t g) {
+    const uint32_t full = G / (8 * g) * (8 * g);
+    if (b >= full) return b;
+    const uint32_t xcd = b & 7u, slot = b >> 3;
+    return (slot / g) * 8 * g + xcd * g + slot % g;
+}
+
 // 16-byte store of four output values that bypasses the caches' retention
 // policy: O is written once and not read back by the kernel, so streaming it
 // out keeps dirty O lines from being evicted later, on the time of whichever
