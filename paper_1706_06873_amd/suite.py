@@ -22,7 +22,9 @@ on the same im2col matrix, for context: im2col + vendor GEMM.
 For every layer it times MEC from L (compact lowering + slab products), MEC
 fused, and the im2col baseline (im2col lowering + one product through the
 same kernels), each kernel between HIP events on its stream, on seeded
-synthetic inputs already in device memory, and prints one JSON line with the
+synthetic inputs already in device memory (buffer sets rotating so that one
+rotation spans at least 1 GiB, after untimed launches that let the clocks
+settle, as the benchmark does), and prints one JSON line with the
 times, the effective TFLOP/s (2 x MAC / time) and the workspace of MEC
 against im2col. Parity of every one of these shapes with the CPU oracle is
 checked by the GPU tests, not here.
@@ -31,6 +33,7 @@ import argparse
 import dataclasses
 import json
 import sys
+import time
 
 import torch
 
@@ -39,7 +42,19 @@ from paper_1706_06873_amd import workloads as wl
 from paper_1706_06873_amd.timing import HipEvent
 
 
-def _time_layer(layer, reps, warmup, sets, yardstick=False):
+MIN_ROTATION_BYTES = 1 << 30  # per rotation: beyond the 256 MB last-level cache
+MAX_SETS = 64
+
+
+def _auto_sets(I0, K0, o_elems):
+    """Buffer sets so that one rotation through them spans at least 1 GiB
+    even for the fused form (I, K and O only): no launch finds its operands
+    in the last-level cache from an earlier one."""
+    foot = I0.numel() * I0.element_size() + K0.numel() * K0.element_size() + 4 * o_elems
+    return max(2, min(MAX_SETS, -(-MIN_ROTATION_BYTES // foot)))
+
+
+def _time_layer(layer, reps, warmup, sets, yardstick=False, settle=0.2):
     i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w = layer.dims
     o_h, o_w = mec.output_dims(i_h, i_w, k_h, k_w, s_h, s_w)
     dt = mec.BF16 if layer.dtype == "bf16" else mec.F32
@@ -47,6 +62,8 @@ def _time_layer(layer, reps, warmup, sets, yardstick=False):
     P = k_h * k_w * i_c
     dev = torch.device("cuda:0")
     I0, K0 = wl.make_inputs(layer)
+    if sets <= 0:
+        sets = _auto_sets(I0, K0, i_n * o_h * o_w * k_c)
     bufs = [dict(I=I0.to(dev) if j == 0 else I0.to(dev).clone(), K=K0.to(dev),
                  O=torch.empty((i_n, o_h, o_w, k_c), dtype=torch.float32, device=dev))
             for j in range(sets)]
@@ -81,6 +98,14 @@ def _time_layer(layer, reps, warmup, sets, yardstick=False):
             rec(2)
 
         with torch.cuda.stream(stream):
+            # untimed launches until the clocks have settled, then the warm-up
+            t0 = time.time()
+            k = 0
+            while time.time() - t0 < settle:
+                run(bufs[k % sets])
+                k += 1
+                if k % sets == 0:
+                    torch.cuda.synchronize()
             for w in range(warmup):
                 run(bufs[w % sets])
             torch.cuda.synchronize()
@@ -119,7 +144,7 @@ def _time_layer(layer, reps, warmup, sets, yardstick=False):
     ws_mec = mec.workspace_bytes(*layer.dims, dtype=dt, algo=mec.LOWERED)
     ws_im2col = mec.im2col_bytes(*layer.dims, dtype=dt)
     return {"layer": layer.name, "dims": list(layer.dims), "o": [o_h, o_w], "dtype": layer.dtype,
-            "gflop": round(2.0 * macs / 1e9, 3), "workspace_mec": ws_mec,
+            "gflop": round(2.0 * macs / 1e9, 3), "sets": sets, "workspace_mec": ws_mec,
             "workspace_im2col": ws_im2col, "im2col_over_mec": round(ws_im2col / ws_mec, 3),
             "timings": res,
             "mec_speedup_vs_im2col": round(res["im2col"]["us"] / min(res["lowered"]["us"],
@@ -206,7 +231,11 @@ def main(argv=None):
     ap.add_argument("--dtype", default="f32", choices=["f32", "bf16", "both"])
     ap.add_argument("--reps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--sets", type=int, default=2, help="rotating buffer sets")
+    ap.add_argument("--sets", type=int, default=0,
+                    help="rotating buffer sets (0: enough that a rotation spans 1 GiB, at most %d)"
+                         % MAX_SETS)
+    ap.add_argument("--settle", type=float, default=0.2,
+                    help="seconds of untimed launches per layer and algorithm before the warm-up")
     ap.add_argument("--layers", default="", help="comma-separated subset")
     args = ap.parse_args(argv)
     if not torch.cuda.is_available():
@@ -235,7 +264,7 @@ def main(argv=None):
         layers = [wl.table2_layer("cv1", batch, d, stride=s) for d in dtypes for s in strides]
     rows = []
     for layer in layers:
-        rows.append(_time_layer(layer, args.reps, args.warmup, args.sets, args.yardstick))
+        rows.append(_time_layer(layer, args.reps, args.warmup, args.sets, args.yardstick, args.settle))
         print(json.dumps(rows[-1]), flush=True)
     if args.which == "resnet101":
         for d in dtypes:

@@ -50,3 +50,21 @@ def test_weighted_times():
     assert s["im2col_us"] == pytest.approx(sum(wi * (10.0 + i) for i, wi in enumerate(w)))
     assert s["mec_fused_us"] == pytest.approx(sum(wi * (2.0 + i) for i, wi in enumerate(w)))
     assert s["time_ratio_lowered"] == pytest.approx(s["im2col_us"] / s["mec_lowered_us"], rel=1e-3)
+
+
+def test_auto_sets_span_the_last_level_cache():
+    """Buffer sets of the suite: a rotation through them spans at least 1 GiB
+    (I, K and O of the fused form), between 2 and the cap."""
+    import torch
+    for name in wl.TABLE2:
+        layer = wl.table2_layer(name, 32)
+        I0, K0 = wl.make_inputs(layer) if name in ("cv11", "cv12") else (
+            torch.empty(layer.i_n * layer.i_h * layer.i_w * layer.i_c),
+            torch.empty(layer.k_h * layer.k_w * layer.i_c * layer.k_c))
+        o_h, o_w = mec.output_dims(*layer.dims[1:3], *layer.dims[4:6], *layer.dims[7:9])
+        o_elems = layer.i_n * o_h * o_w * layer.k_c
+        sets = suite._auto_sets(I0, K0, o_elems)
+        foot = I0.numel() * I0.element_size() + K0.numel() * K0.element_size() + 4 * o_elems
+        assert 2 <= sets <= suite.MAX_SETS
+        assert sets * foot >= suite.MIN_ROTATION_BYTES or sets == suite.MAX_SETS
+        assert sets == 2 or (sets - 1) * foot < suite.MIN_ROTATION_BYTES
