@@ -106,7 +106,7 @@ def load_traffic(dtype, layer_name, algo, digest):
     size correctly, and the digest of the sources the counters were taken on.
     A figure taken on other sources is not reported (None)."""
     path = profile_path(dtype, layer_name, algo)
-    out = {"products": None, "lower": None}
+    out = {"products": None, "lower": None, "products_kernel": None, "lower_kernel": None}
     if not os.path.exists(path):
         return out
     with open(path) as f:
@@ -117,6 +117,7 @@ def load_traffic(dtype, layer_name, algo, digest):
                     if t.get("workload") == "%s %s" % (layer_name, algo) and t.get("csrc_sha256") == digest:
                         out[key] = int(round((t["fetch_kib"] * t["fetch_scale"] +
                                               t["write_kib"] * t["write_scale"]) * 1024))
+                        out[key + "_kernel"] = t.get("kernel")
     return out
 
 
@@ -243,7 +244,9 @@ def measure(cfg, HipEvent, steps, warmup, digest, settle_s):
     layer = cfg.layer
     peak = PEAK_TFLOPS[layer.dtype]
     traffic = load_traffic(layer.dtype, layer.name, cfg.algo, digest)
-    kname = "slab_gemm_%s_kernel" % layer.dtype
+    # the kernel's own name where the layer's profile (taken on these sources)
+    # recorded it, else its family
+    kname = traffic["products_kernel"] or "slab_gemm_%s_*kernel" % layer.dtype
     kname += {"fused": " (from I)", "im2col": " (im2col product, k_h = 1)", "lowered": ""}[cfg.algo]
     ab = cfg.alg_bytes()
     ridge = peak * 1e12 / (PEAK_HBM_GBS * 1e9)
@@ -273,7 +276,7 @@ def measure(cfg, HipEvent, steps, warmup, digest, settle_s):
         out["lower_ms"] = round(lower_ms, 5)
         out["roofline_lower"] = {
             "bound": "hbm" if layer.name != "tiny" else "launch",
-            "kernel": "im2col_*_kernel" if cfg.algo == "im2col" else "lower_*_kernel",
+            "kernel": "im2col_*_kernel" if cfg.algo == "im2col" else (traffic["lower_kernel"] or "lower_*_kernel"),
             "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
             "frac": round(gbs / PEAK_HBM_GBS, 4) if layer.name != "tiny" else None,
             "traffic": traffic["lower"], "alg_bytes": lb}
