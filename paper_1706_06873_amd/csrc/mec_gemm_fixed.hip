@@ -1561,9 +1561,13 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
         return dry_run ? hipSuccess : run_stream<CFG>(s, A, K, O, stream, layout);  \
     }
     if (dtype == 0) {
-        // 11x11 stride 4 over few channels (rows of L of 33 elements): the flat
-        // windows through a ring of LDS (mec_gemm_ring.hip)
-        if (!layout && s.k_h == 11 && s.s_h == 4 && gemm_ring_usable(s, dtype))
+        // tall kernels over short rows of L (11x11 over 3 channels: 33 elements):
+        // the flat windows through a ring of LDS (mec_gemm_ring.hip), where the
+        // ring holds four output rows' windows (strides up to 4 for 11x11).
+        // Measured on cv1 at batch 32: stride 4 325 -> 300 us at full size
+        // (alexnet_conv1), stride 3 207 -> 141 us; 7x7 stride 2 over 3
+        // channels (cv3) is even from L and 6% slower fused, so k_h >= 9.
+        if (!layout && s.k_h >= 9 && s.R <= 48 && gemm_ring_usable(s, dtype))
             return dry_run ? hipSuccess : launch_gemm_ring(s, A, K, O, F, stream);
         if (s.R >= 32) {
             // no split into a strided layout: zeroing O would clear other pixels
