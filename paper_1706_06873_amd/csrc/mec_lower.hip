@@ -43,7 +43,6 @@ namespace {
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kRowsThreads = 256;
 constexpr int kStripThreads = 512;
 constexpr int kLineBytes = 128;           // cache line
 constexpr int64_t kStripLineMinChunk = 512;  // bytes of L per chunk for line ownership
@@ -77,18 +76,18 @@ struct RowsParams {
     FastDiv div_ih, div_RV;
 };
 
-template <typename E>
-__global__ __launch_bounds__(kRowsThreads) void lower_rows_kernel(RowsParams p) {
+template <typename E, int THREADS>
+__global__ __launch_bounds__(THREADS) void lower_rows_kernel(RowsParams p) {
     extern __shared__ u32x4 row[];
     const uint32_t blk = blockIdx.x;  // input row n*i_h + h
     const uint32_t n = p.div_ih.div(blk), h = blk - n * p.i_h;
     const u32x4* __restrict__ I = reinterpret_cast<const u32x4*>(p.I) + (size_t)blk * p.rowv;
     // I is read once: streamed past the caches like the stores of L
-    for (uint32_t i = threadIdx.x; i < p.rowv; i += kRowsThreads) row[i] = __builtin_nontemporal_load(I + i);
+    for (uint32_t i = threadIdx.x; i < p.rowv; i += THREADS) row[i] = __builtin_nontemporal_load(I + i);
     __syncthreads();
     u32x4* __restrict__ L = reinterpret_cast<u32x4*>(p.L);
     const uint32_t total = p.o_w * p.RV;
-    for (uint32_t f = threadIdx.x; f < total; f += kRowsThreads) {
+    for (uint32_t f = threadIdx.x; f < total; f += THREADS) {
         const uint32_t w = p.div_RV.div(f);
         const uint32_t c = f - w * p.RV;
         __builtin_nontemporal_store(row[w * p.swv + c],
@@ -257,8 +256,22 @@ hipError_t launch_rows(const Shape& s, const void* I, void* L, hipStream_t strea
     p.swv = (uint32_t)(s.s_w * s.i_c / VEC);
     p.div_ih = FastDiv(p.i_h);
     p.div_RV = FastDiv(p.RV);
-    hipLaunchKernelGGL(lower_rows_kernel<E>, dim3(p.nrows_in), dim3(kRowsThreads),
-                       (size_t)p.rowv * 16, stream, p);
+    // Threads per workgroup (one input row each): 256 where the rows fill
+    // every compute unit with 4 to 12 workgroups, 512 where there are fewer
+    // (more bytes in flight per row) or more (measured: deep_bf16, 16 rows per
+    // compute unit, 43.8 -> 41.7 us; Table 2's cv4 350 -> 341 us, cv10-cv12 6-20%
+    // faster; resnet_mid and cv9, about 7 per compute unit, 2-3% slower at 512).
+    int dev = 0, cus = 0;
+    if (hipStreamGetDevice(stream, &dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+        cus = 256;
+    const int64_t per_cu = (int64_t)p.nrows_in / cus;
+    if (per_cu >= 4 && per_cu < 12)
+        hipLaunchKernelGGL((lower_rows_kernel<E, 256>), dim3(p.nrows_in), dim3(256), (size_t)p.rowv * 16,
+                           stream, p);
+    else
+        hipLaunchKernelGGL((lower_rows_kernel<E, 512>), dim3(p.nrows_in), dim3(512), (size_t)p.rowv * 16,
+                           stream, p);
     return hipGetLastError();
 }
 
