@@ -428,6 +428,35 @@ def test_ring_split_tail(orc, gpi, k_c, algo):
     assert np.array_equal(run_conv(I, K, 4, 4, algo), ref.astype(np.float32))
 
 
+# fp32 from L, kernels taller than one row with no tile of their own: the
+# windows of Section 3.2's flat view as the rows of one plain product through
+# the k_h = 1 tiles. Rows of a multiple of 4 (16-byte loads) and not, k_c
+# above and below 64 and not a multiple of 4, ragged pairs and output rows,
+# windows overlapping by several rows (stride 1, 2) or none (stride = k_h).
+FLAT_CASES = [
+    (3, 21, 19, 64, 3, 3, 72, 2, 2),      # 3x3 stride 2, rows of 192
+    (2, 25, 23, 32, 5, 5, 30, 2, 2),      # 5x5 stride 2, k_c not a multiple of 4
+    (3, 18, 20, 16, 2, 2, 128, 2, 2),     # 2x2 stride 2: windows side by side
+    (1, 31, 29, 3, 11, 11, 96, 1, 1),     # 11x11 stride 1 (rows of 33: element loads)
+    (2, 33, 35, 3, 11, 11, 40, 2, 3),     # 11x11 stride 2
+    (2, 45, 41, 3, 11, 11, 100, 5, 5),    # 11x11 stride 5: beyond the ring
+    (2, 30, 28, 16, 7, 7, 64, 1, 1),      # 7x7 stride 1
+    (3, 20, 22, 5, 3, 3, 9, 3, 3),        # 3x3 stride 3, rows of 15
+]
+
+
+@pytest.mark.parametrize("dims", FLAT_CASES)
+def test_flat_window_products(orc, dims):
+    say("flat windows", dims)
+    s_h, s_w = dims[7], dims[8]
+    Ii, Ki = case(91 + sum(dims), dims, dist="int")
+    refi = orc.conv2d_direct(host(Ii), host(Ki), s_h, s_w)
+    assert np.abs(refi).max() < 2 ** 24
+    assert np.array_equal(run_conv(Ii, Ki, s_h, s_w, "lowered"), refi.astype(np.float32))
+    I, K = case(93 + sum(dims), dims)
+    assert rel_l2(run_conv(I, K, s_h, s_w, "lowered"), orc.conv2d_direct(host(I), host(K), s_h, s_w)) <= TOL_F32
+
+
 @pytest.mark.parametrize("shift", [1, 3])
 def test_ring_unaligned_and_guarded(orc, shift):
     """I, K, L and O one or three elements off their 16-byte boundaries, O
