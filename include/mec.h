@@ -124,7 +124,9 @@ int mec_lower(const void* I, void* L,
  * in another order, within rounding of the others). (For 3x3 layers whose
  * tiles leave compute units idle, each tile's reduction is split in two halves
  * that are added into O after O is zeroed; two partial sums added to zero
- * commute exactly.)
+ * commute exactly.) Every kernel height runs: where no tile of its own fits,
+ * the windows L[n, w][s_h*R*h : s_h*R*h + k_h*R] are read as the rows of one
+ * plain product (Section 3.2's flat view).
  * Returns MEC_OK or a negative status. */
 int mec_gemm(const void* L, const void* K, float* O,
              int i_n, int i_h, int i_w, int i_c,
@@ -152,7 +154,9 @@ int mec_im2col(const void* I, void* M,
  *   workspace_bytes must be >= mec_workspace_bytes(..., MEC_ALGO_LOWERED) and
  *   the workspace must be aligned to the element size. On return (after the
  *   stream completes) the workspace holds L exactly as mec_lower writes it.
- * MEC_ALGO_FUSED: one kernel; workspace may be NULL and is not touched.
+ * MEC_ALGO_FUSED: one kernel; workspace may be NULL and is not touched. Its
+ *   tiles stage the slab rows from I on chip, so kernels taller than they hold
+ *   are refused with MEC_ERR_UNSUPPORTED (MEC_ALGO_LOWERED takes them).
  * MEC_ALGO_IM2COL: mec_im2col into `workspace` (at least mec_im2col_bytes),
  *   then the product of M and K; the workspace then holds M.
  * O must not overlap I, K or the workspace.

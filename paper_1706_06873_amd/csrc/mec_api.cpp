@@ -158,7 +158,7 @@ int mec_gemm(const void* L, const void* K, float* O, int i_n, int i_h, int i_w, 
     if (!valid_dtype(dtype) || !L || !K || !O) return MEC_ERR_INVALID_ARG;
     const int64_t es = elem_bytes(dtype);
     if (!aligned(L, es) || !aligned(K, es) || !aligned(O, 4)) return MEC_ERR_ALIGNMENT;
-    if (!mec::gemm_supported(s, dtype)) return MEC_ERR_UNSUPPORTED;
+    if (!mec::gemm_supported(s, dtype, false)) return MEC_ERR_UNSUPPORTED;
     clear_stale_error();
     return hip_status(mec::launch_gemm(s, L, K, O, dtype, false, (hipStream_t)stream),
                       "slab products");
@@ -182,7 +182,8 @@ int mec_conv2d(const void* I, const void* K, float* O, void* workspace, size_t w
         if (!aligned(workspace, es)) return MEC_ERR_ALIGNMENT;
     }
     const mec::Shape g = algo == MEC_ALGO_IM2COL ? im2col_product_shape(s) : s;
-    if (g.R > (int64_t(1) << 26) || !mec::gemm_supported(g, dtype)) return MEC_ERR_UNSUPPORTED;
+    if (g.R > (int64_t(1) << 26) || !mec::gemm_supported(g, dtype, algo == MEC_ALGO_FUSED))
+        return MEC_ERR_UNSUPPORTED;
     const hipStream_t st = (hipStream_t)stream;
     clear_stale_error();
     if (algo == MEC_ALGO_FUSED)

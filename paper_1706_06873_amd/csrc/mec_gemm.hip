@@ -440,9 +440,10 @@ hipError_t dispatch(const Shape& s, const void* A, const void* K, float* O, int 
 
 }  // namespace
 
-bool gemm_supported(const Shape& s, int dtype) {
-    if (launch_gemm_fixed(s, nullptr, nullptr, nullptr, dtype, false, nullptr, true) == hipSuccess)
+bool gemm_supported(const Shape& s, int dtype, bool fused) {
+    if (launch_gemm_fixed(s, nullptr, nullptr, nullptr, dtype, fused, nullptr, true) == hipSuccess)
         return true;
+    if (fused) return dispatch<true>(s, nullptr, nullptr, nullptr, dtype, nullptr, true) == hipSuccess;
     return dispatch<false>(s, nullptr, nullptr, nullptr, dtype, nullptr, true) == hipSuccess;
 }
 

@@ -974,7 +974,7 @@ bool dgrad_phases_ok(const Shape& s) {
             const Phase ph = dgrad_phase(s, py, px);
             if (ph.gp_elems >= (int64_t(1) << 31) || ph.t.R > (int64_t(1) << 26)) return false;
             if (unit) {
-                if (!gemm_supported(ph.t, 0)) return false;
+                if (!gemm_supported(ph.t, 0, true)) return false;
             } else {
                 const OutLayout o = phase_layout(s, ph);
                 if (launch_gemm_fixed(ph.t, nullptr, nullptr, nullptr, 0, true, nullptr, true, &o) !=

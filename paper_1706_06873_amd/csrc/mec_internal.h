@@ -93,8 +93,11 @@ struct OutLayout;
 hipError_t launch_gemm(const Shape& s, const void* A, const void* K, float* O, int dtype,
                        bool fused, hipStream_t stream, const OutLayout* layout = nullptr);
 
-// Whether the slab-product kernels can run this shape (LDS limits).
-bool gemm_supported(const Shape& s, int dtype);
+// Whether the slab-product kernels can run this shape (LDS limits), from L
+// (fused = false) or staged from I (fused = true): from L, every kernel height
+// runs (the flat windows of L through the one-row tiles); from I, the generic
+// kernel's tiles bound k_h.
+bool gemm_supported(const Shape& s, int dtype, bool fused);
 
 // Where the fp32 kernels of mec_gemm_fixed.hip write output element
 // (n, h, w, c): O + n*img + h*row + w*col + off + c. The default (nullptr)

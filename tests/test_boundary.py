@@ -185,9 +185,10 @@ def test_workspace_rejected():
 
 
 def test_unsupported_kernel_height():
-    # far taller than the on-chip tile holds: refused before any launch
+    # far taller than the fused form's on-chip tiles hold: refused before any
+    # launch (from L, the flat windows take every height, so this shape is not
+    # called there with these stand-in pointers)
     dims = (1, 300, 8, 1, 300, 3, 1, 1, 1)
-    assert mec.lib.mec_gemm(FAKE, FAKE, FAKE, *dims, 0, NULL) == -5
     assert mec.lib.mec_conv2d(FAKE, FAKE, FAKE, NULL, 0, *dims, 0, 1, NULL) == -5
     assert mec.workspace_bytes(*dims) == 1 * 6 * 300 * 3 * 4
 
