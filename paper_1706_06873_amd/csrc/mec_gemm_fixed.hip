@@ -1457,6 +1457,13 @@ template <bool F> using BF16K7S2 = BF16Cfg<4, 4, 2, 16, 7, 2, F, 8>;
 // bf16, 11x11 stride 4 over few channels (rows of 33 elements, gathered element
 // by element): 32 pairs x 2 rows (15 staged rows) x 96 channels, r-chunks of 16.
 template <bool F> using BF16K11S4 = BF16Cfg<2, 3, 2, 16, 11, 4, F, 6, false>;
+// bf16 flat windows (from L, one row per window; see dispatch_fixed): 32 pairs x
+// 8 windows x 96 or 128 channels, r-chunks of 32, windows gathered element by
+// element or, when their length and both strides are multiples of 8, in
+// 16-byte pieces.
+using BF16FlatG96 = BF16Cfg<8, 3, 2, 32, 1, 1, false, 6, false>;
+using BF16FlatG128 = BF16Cfg<8, 4, 2, 32, 1, 1, false, 8, false>;
+using BF16FlatV128 = BF16Cfg<8, 4, 2, 32, 1, 1, false, 8, true>;
 
 // Of tiles that differ only in their number of output rows, the one that
 // minimises (rounds of tiles over the 256 compute units) x (input rows each
@@ -1554,6 +1561,20 @@ TileChoice pick_tiles_f32_3x3(const Shape& s, bool allow_split) {
     return best;
 }
 
+// Section 3.2's flat view of L: the slab of output row h of pair (n, w) is the
+// window L[n, w][s_h*R*h : s_h*R*h + k_h*R]. flat_windows gives the one-row
+// product over those windows (row x of a pair = output row x, reduction over
+// k_h*R), flat_view where its rows lie in L.
+Shape flat_windows(const Shape& s) {
+    Shape f = s;
+    f.k_h = f.k_w = 1;
+    f.s_h = f.s_w = 1;
+    f.i_c = f.R = s.k_h * s.R;
+    f.i_h = s.o_h;  // one row x per output row
+    return f;
+}
+RowView flat_view(const Shape& s) { return RowView{s.s_h * s.R, s.i_h * s.R}; }
+
 template <bool F>
 hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O, int dtype,
                           hipStream_t stream, bool dry_run, const OutLayout* layout) {
@@ -1631,12 +1652,8 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
         // 3x3 stride 2 over 64 channels 183 -> 52 us; 5x5 stride 2 197 -> 70 us;
         // 7x7 stride 1 over 16 channels 153 -> 122 us.
         if (!F && !layout && s.k_h > 1 && offsets_fit(s, false)) {
-            Shape f = s;
-            f.k_h = f.k_w = 1;
-            f.s_h = f.s_w = 1;
-            f.i_c = f.R = s.k_h * s.R;
-            f.i_h = s.o_h;  // one row x per output row
-            const RowView view{s.s_h * s.R, s.i_h * s.R};
+            const Shape f = flat_windows(s);
+            const RowView view = flat_view(s);
 #define MEC_TRY_FLAT(CFG)                                                                  \
     if (usable<CFG>(f, A, K) && (CFG::kVA == 1 || view.xstride % CFG::kVA == 0) &&         \
         (CFG::kVA == 1 || view.pstride % CFG::kVA == 0)) {                                 \
@@ -1677,6 +1694,23 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
         MEC_TRY_FIXED(BF16K7S2<F>);
         MEC_TRY_FIXED(BF16K11S4<F>);
         MEC_TRY_FIXED(BF16K1S1<F>);
+        // From L, the flat windows (as for fp32 above) where consecutive windows
+        // overlap most (k_h >= 5 s_h) and no tile of its own fits: cv1 in bf16
+        // at stride 1 2473 -> 1213 us, stride 2 476 -> 325 us against the
+        // generic kernel; at stride 5 (118 against 113 us) and on 7x7 stride 2
+        // over 3 channels (170 against 110 us) the element-by-element gathering
+        // of bf16 windows loses.
+        if (!F && s.k_h > 1 && s.k_h >= 5 * s.s_h && offsets_fit(s, false)) {
+            const Shape f = flat_windows(s);
+            const RowView view = flat_view(s);
+            const bool vec = f.R % 8 == 0 && view.xstride % 8 == 0 && view.pstride % 8 == 0;
+            if (s.k_c <= 96 && usable<BF16FlatG96>(f, A, K))
+                return dry_run ? hipSuccess : run_fixed<BF16FlatG96>(f, A, K, O, stream, 1, nullptr, &view);
+            if (vec && usable<BF16FlatV128>(f, A, K))
+                return dry_run ? hipSuccess : run_fixed<BF16FlatV128>(f, A, K, O, stream, 1, nullptr, &view);
+            if (usable<BF16FlatG128>(f, A, K))
+                return dry_run ? hipSuccess : run_fixed<BF16FlatG128>(f, A, K, O, stream, 1, nullptr, &view);
+        }
     }
 #undef MEC_TRY_FIXED
 #undef MEC_TRY_STREAM

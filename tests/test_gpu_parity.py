@@ -457,6 +457,31 @@ def test_flat_window_products(orc, dims):
     assert rel_l2(run_conv(I, K, s_h, s_w, "lowered"), orc.conv2d_direct(host(I), host(K), s_h, s_w)) <= TOL_F32
 
 
+# bf16 from L, windows overlapping most (k_h >= 5 s_h) with no tile of their
+# own: the flat windows gathered element by element (96 channels or fewer, or
+# 128-channel tiles) or in 16-byte pieces (length and strides multiples of 8).
+FLAT_CASES_BF16 = [
+    (2, 25, 23, 3, 11, 11, 40, 1, 1),     # 11x11 stride 1, windows of 363
+    (1, 30, 20, 8, 11, 3, 136, 2, 2),     # windows of 264, 16-byte pieces, two channel tiles
+    (2, 24, 20, 5, 10, 3, 104, 2, 1),     # windows of 150, gathered, one ragged channel tile
+]
+
+
+@pytest.mark.parametrize("dims", FLAT_CASES_BF16)
+def test_flat_window_products_bf16(orc, dims):
+    say("flat windows bf16", dims)
+    s_h, s_w = dims[7], dims[8]
+    Ii, Ki = case(95 + sum(dims), dims, dtype="bf16", dist="int")
+    refi = orc.conv2d_direct(host(Ii), host(Ki), s_h, s_w)
+    assert np.abs(refi).max() < 2 ** 24
+    assert np.array_equal(run_conv(Ii, Ki, s_h, s_w, "lowered"), refi.astype(np.float32))
+    I32, K32 = case(97 + sum(dims), dims, dtype="f32")
+    I, K = I32.to(torch.bfloat16), K32.to(torch.bfloat16)
+    got = run_conv(I, K, s_h, s_w, "lowered")
+    assert rel_l2(got, orc.conv2d_direct(host(I), host(K), s_h, s_w)) <= TOL_F32
+    assert rel_l2(got, orc.conv2d_direct(host(I32), host(K32), s_h, s_w)) <= TOL_BF16_VS_F32
+
+
 @pytest.mark.parametrize("shift", [1, 3])
 def test_ring_unaligned_and_guarded(orc, shift):
     """I, K, L and O one or three elements off their 16-byte boundaries, O
