@@ -15,7 +15,9 @@
 // n-h-w-c with non-temporal stores. Layers whose whole reduction fits one stage
 // and whose time goes to writing O (3x3 over 1-3 channels) use a persistent
 // streaming variant that overlaps each tile's O stores with the next tile's
-// products.
+// products. From L, every other kernel height runs through the k_h = 1 tiles
+// over the flat windows of L (Section 3.2's view: the slab of output row h is
+// one contiguous window of its pair's row of L), read s_h*R elements apart.
 #include <initializer_list>
 #include <type_traits>
 
