@@ -428,6 +428,32 @@ def test_ring_split_tail(orc, gpi, k_c, algo):
     assert np.array_equal(run_conv(I, K, 4, 4, algo), ref.astype(np.float32))
 
 
+# fp32 3x3 stride 2 tiles (32 pairs x 2 output rows, 5 staged rows): rows of
+# a multiple of 4 (16-byte loads), short rows (element loads of I and L), k_c
+# not a multiple of 4 (element loads of K), ragged pairs, rows and channels,
+# s_w = 1.
+K3S2_CASES = [
+    (3, 21, 19, 64, 3, 3, 72, 2, 2),
+    (2, 17, 18, 3, 3, 3, 40, 2, 2),
+    (2, 15, 16, 5, 3, 3, 30, 2, 2),
+    (2, 19, 20, 8, 3, 3, 64, 2, 1),
+    (1, 9, 9, 128, 3, 3, 136, 2, 2),
+]
+
+
+@pytest.mark.parametrize("dims", K3S2_CASES)
+@pytest.mark.parametrize("algo", ["lowered", "fused"])
+def test_k3s2_tiles(orc, dims, algo):
+    say("3x3 stride 2", algo, dims)
+    s_h, s_w = dims[7], dims[8]
+    Ii, Ki = case(101 + sum(dims), dims, dist="int")
+    refi = orc.conv2d_direct(host(Ii), host(Ki), s_h, s_w)
+    assert np.abs(refi).max() < 2 ** 24
+    assert np.array_equal(run_conv(Ii, Ki, s_h, s_w, algo), refi.astype(np.float32))
+    I, K = case(103 + sum(dims), dims)
+    assert rel_l2(run_conv(I, K, s_h, s_w, algo), orc.conv2d_direct(host(I), host(K), s_h, s_w)) <= TOL_F32
+
+
 # fp32 from L, kernels taller than one row with no tile of their own: the
 # windows of Section 3.2's flat view as the rows of one plain product through
 # the k_h = 1 tiles. Rows of a multiple of 4 (16-byte loads) and not, k_c
