@@ -1653,8 +1653,8 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
         if (s.k_c > 64) MEC_TRY_FIXED(F32K1S1Narrow96<F>);
         MEC_TRY_FIXED(F32K1S1Narrow<F>);
         MEC_TRY_FIXED(F32K1S1Scalar<F>);
-        // From L, every other kernel taller than one row: Section 3.2's flat view
-        // again. The slab of output row h of pair (n, w) is the contiguous window
+        // From L, every other kernel taller than one row (or one row at a stride
+        // above 1): Section 3.2's flat view again. The slab of output row h of pair (n, w) is the contiguous window
         // L[n, w][s_h*R*h : s_h*R*h + k_h*R], so O is one plain product whose
         // rows (pair, h) are these windows, s_h*R elements apart, and whose
         // reduction runs over k_h*R elements with no per-kernel-row padding: the
@@ -1664,7 +1664,7 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
         // strides 1, 2, 5, 10 1284 -> 1063, 353 -> 281, 178 -> 96, 73 -> 57 us;
         // 3x3 stride 2 over 64 channels 183 -> 52 us; 5x5 stride 2 197 -> 70 us;
         // 7x7 stride 1 over 16 channels 153 -> 122 us.
-        if (!F && !layout && s.k_h > 1 && offsets_fit(s, false)) {
+        if (!F && !layout && (s.k_h > 1 || s.s_h > 1) && offsets_fit(s, false)) {
             const Shape f = flat_windows(s);
             const RowView view = flat_view(s);
 #define MEC_TRY_FLAT(CFG)                                                                  \

@@ -468,6 +468,7 @@ FLAT_CASES = [
     (2, 45, 41, 3, 11, 11, 100, 5, 5),    # 11x11 stride 5: beyond the ring
     (2, 30, 28, 16, 7, 7, 64, 1, 1),      # 7x7 stride 1
     (3, 20, 22, 5, 3, 3, 9, 3, 3),        # 3x3 stride 3, rows of 15
+    (2, 15, 14, 64, 1, 1, 40, 2, 2),      # 1x1 stride 2: every other row of L
 ]
 
 
