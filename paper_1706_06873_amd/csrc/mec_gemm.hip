@@ -408,6 +408,13 @@ template <bool F> using F32Wide = Cfg<TraitsF32, 8, 2, 4, 8, 16, 8, 4, true, F>;
 template <bool F> using F32Narrow = Cfg<TraitsF32, 8, 2, 4, 2, 16, 8, 1, true, F>;
 template <bool F> using F32Tall = Cfg<TraitsF32, 8, 3, 4, 2, 40, 12, 1, true, F>;
 template <bool F> using F32Gen4 = Cfg<TraitsF32, 4, 1, 4, 2, 64, 64, 1, false, F>;
+// 2 output rows per tile, tried first: the strided kernels that reach this
+// kernel (from I; from L they take the flat windows) lose little overlap at
+// 2 rows and gain four times the tiles. Measured from I at batch 32: 5x5
+// stride 2 197 -> 67 us, 2x2 stride 2 100 -> 59 us, 1x1 stride 2 349 -> 218 us,
+// 7x7 stride 1 150 us either way. (bf16 at 2 rows lost on every shape tried.)
+template <bool F> using F32Wide2 = Cfg<TraitsF32, 2, 2, 2, 8, 16, 8, 4, true, F>;
+template <bool F> using F32Narrow2 = Cfg<TraitsF32, 2, 2, 2, 2, 16, 8, 1, true, F>;
 template <bool F> using F32Gen1 = Cfg<TraitsF32, 1, 4, 1, 2, 64, 64, 1, false, F>;
 template <bool F> using BF16Vec4 = Cfg<TraitsBF16, 4, 2, 2, 16, 16, 8, 8, true, F>;
 template <bool F> using BF16Gen4 = Cfg<TraitsBF16, 4, 2, 2, 16, 16, 8, 1, false, F>;
@@ -422,6 +429,8 @@ hipError_t dispatch(const Shape& s, const void* A, const void* K, float* O, int 
         return dry_run ? hipSuccess : run<CFG>(s, A, K, O, stream); \
     }
     if (dtype == 0) {
+        if (s.R % 4 == 0 && s.R >= 16 && (dry_run || vec_ok<4>(s, F, A))) MEC_TRY(F32Wide2<F>);
+        MEC_TRY(F32Narrow2<F>);
         if (s.k_c > 64 && s.s_h > 1) MEC_TRY(F32Tall<F>);
         if (s.R % 4 == 0 && s.R >= 16 && (dry_run || vec_ok<4>(s, F, A))) MEC_TRY(F32Wide<F>);
         MEC_TRY(F32Narrow<F>);

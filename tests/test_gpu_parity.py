@@ -473,15 +473,18 @@ FLAT_CASES = [
 
 
 @pytest.mark.parametrize("dims", FLAT_CASES)
-def test_flat_window_products(orc, dims):
-    say("flat windows", dims)
+@pytest.mark.parametrize("algo", ["lowered", "fused"])
+def test_flat_window_products(orc, dims, algo):
+    """From L the flat windows; from I the same shapes take the generic kernel
+    (2-row tiles first where the kernel fits them) or the 3x3 stride-2 tiles."""
+    say("flat windows", algo, dims)
     s_h, s_w = dims[7], dims[8]
     Ii, Ki = case(91 + sum(dims), dims, dist="int")
     refi = orc.conv2d_direct(host(Ii), host(Ki), s_h, s_w)
     assert np.abs(refi).max() < 2 ** 24
-    assert np.array_equal(run_conv(Ii, Ki, s_h, s_w, "lowered"), refi.astype(np.float32))
+    assert np.array_equal(run_conv(Ii, Ki, s_h, s_w, algo), refi.astype(np.float32))
     I, K = case(93 + sum(dims), dims)
-    assert rel_l2(run_conv(I, K, s_h, s_w, "lowered"), orc.conv2d_direct(host(I), host(K), s_h, s_w)) <= TOL_F32
+    assert rel_l2(run_conv(I, K, s_h, s_w, algo), orc.conv2d_direct(host(I), host(K), s_h, s_w)) <= TOL_F32
 
 
 # bf16 from L, windows overlapping most (k_h >= 5 s_h) with no tile of their
