@@ -795,25 +795,47 @@ bool wgrad_slab_ok(const Shape& s) {
            (kWgHT - 1) * s.s_h + s.k_h <= kWsRows && (s.R <= 256 || s.k_h >= 5);
 }
 
+// Shares of the (pair, output row) reduction per dK tile. The time of the
+// products is set by the busiest compute unit: it holds ceil(tiles * splits /
+// 256) workgroups (the workspace size must not depend on the device, so the
+// 256 compute units of the MI355X are assumed), each running ceil(stages /
+// splits) stages one after another on shared SIMDs. Every share adds its
+// partial tile to write and to read back in the reduction. The count that
+// minimises the sum of the two, measured on this GPU: a stage costs the
+// products of one wave (32 k-steps x KH 64-cycle MFMAs in the slab kernel, 32
+// x 2 in the general one), a partial sum 8 bytes per element at 5 TB/s, with
+// the occupancy factors below. Choosing the
+// share count by workgroup count alone (about 512 or 1024) left 1 to 3
+// workgroups beyond whole rounds on some compute units: resnet_mid's 3 tiles
+// in 171 shares, 513 workgroups, ran 124.6 us against 91.0 us in 170 (cv8
+// 813 -> 547 us, cv4 2049 -> 1741 us, alexnet_conv1 645 -> 523 us).
 int64_t wgrad_splits(const Shape& s) {
     const int64_t stages = wgrad_stages(s);
     const int64_t E = s.k_h * s.R * s.k_c;
-    int64_t splits, cap;
-    if (wgrad_slab_ok(s)) {
-        // about two workgroups per compute unit, partial sums within 32 MiB
-        const int64_t tiles = ((s.R + kWs - 1) / kWs) * ((s.k_c + kWs - 1) / kWs);
-        splits = (512 + tiles - 1) / tiles;
-        cap = (int64_t(8) << 20) / E;
-    } else {
-        // enough workgroups to fill the chip about four times over, partial
-        // sums within 256 MiB
-        const int64_t tiles = wgrad_tiles(s);
-        splits = (1024 + tiles - 1) / tiles;
-        cap = (int64_t(64) << 20) / E;
+    const bool slab = wgrad_slab_ok(s);
+    const int64_t tiles = slab ? ((s.R + kWs - 1) / kWs) * ((s.k_c + kWs - 1) / kWs) : wgrad_tiles(s);
+    // partial sums within 32 MiB (slab) or 256 MiB
+    int64_t cap = slab ? (int64_t(8) << 20) / E : (int64_t(64) << 20) / E;
+    if (cap > stages) cap = stages;  // at most one share per stage
+    if (cap > 1024) cap = 1024;
+    if (cap < 1) return 1;
+    const double stage_us = (slab ? 32.0 * s.k_h : 64.0) * 64.0 / 2400.0;
+    const double share_us = 8.0 * (double)E / 5.0e6;
+    int64_t best = 1;
+    double best_t = 0.0;
+    for (int64_t sp = 1; sp <= cap; ++sp) {
+        const int64_t per_cu = (tiles * sp + 255) / 256;
+        double t = (double)per_cu * (double)((stages + sp - 1) / sp) * stage_us + (double)sp * share_us;
+        // one workgroup per compute unit leaves one wave per SIMD; the general
+        // kernel fits three per compute unit and runs best with three
+        if (per_cu == 1) t *= 1.25;
+        if (per_cu == 2 && !slab) t *= 1.07;
+        if (sp == 1 || t < best_t) {
+            best = sp;
+            best_t = t;
+        }
     }
-    if (splits > stages) splits = stages;  // at most one share per stage
-    if (splits > cap) splits = cap;
-    return splits < 1 ? 1 : splits;
+    return best;
 }
 
 int64_t wgrad_partial_bytes(const Shape& s) {
