@@ -38,6 +38,8 @@ constexpr int kRingLen = kChunk * kRingChunks;
 constexpr int kRingLD = kRingLen + 124;
 constexpr int kBlockSteps = 8;             // k-steps between fill points
 constexpr int kWavesPerCU = 8;             // resident waves per compute unit (LDS: 8 rings)
+constexpr uint32_t kStoreDrop = 0x80000000u;  // O byte offsets from here on are out of range
+constexpr int kStoreNT = 2;                // cache policy of the O stores: non-temporal
 
 struct RingParams {
     const float* A;   // L (lowered) or I (fused)
@@ -102,6 +104,27 @@ __device__ __forceinline__ void ring_item(const RingParams& p, float* ring, int6
     const uint32_t ring_lds =
         (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(size_t)(__attribute__((address_space(3))) float*)ring);
 
+    // O through a buffer resource based at the first pair's image. A lane's
+    // byte offset for each (pair, channel block) it stores is fixed for the
+    // item and the output row adds a scalar offset, so a group's stores are
+    // one instruction each. Channels past k_c and pairs past the end get an
+    // offset past the resource's range, whose check drops those stores.
+    const int64_t img0 = p.div_ow.div((uint32_t)pair0);
+    const int64_t obase = img0 * p.o_h * p.o_w * p.k_c;
+    const int64_t orange = (p.pairs * p.o_h * p.k_c - obase) * 4;
+    const __amdgpu_buffer_rsrc_t orsrc = __builtin_amdgcn_make_buffer_rsrc(
+        p.O + obase, (short)0, (int)(orange < kStoreDrop - 1 ? orange : kStoreDrop - 1), 0x00020000);
+    uint32_t ooff[4][NB];
+#pragma unroll
+    for (int q4 = 0; q4 < 4; ++q4) {
+        const int64_t pr = pair0 + kofs * 4 + q4;
+        const int64_t n = p.div_ow.div((uint32_t)pr), w = pr - n * p.o_w;
+        const int64_t rel = ((n - img0) * p.o_h * p.o_w + w) * p.k_c + n0 + m;
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+            ooff[q4][nb] = pr < p.pairs && n0 + 32 * nb + m < p.k_c ? (uint32_t)((rel + 32 * nb) * 4) : kStoreDrop;
+    }
+
     // Fill chunk c (elements [64c, 64c + 64) of every pair's row) into its ring
     // slot. Elements past the row's end repeat its last one: they only reach
     // output rows past o_h, which are never stored.
@@ -137,24 +160,33 @@ __device__ __forceinline__ void ring_item(const RingParams& p, float* ring, int6
     // K fragment of k-step t, channel block nb: K[2t + kofs][n0 + 32 nb + m],
     // by buffer loads whose range check returns 0 past K's last element: the
     // padding steps' rows j >= KR, and channels past k_c in the last row (the
-    // columns past k_c are never stored).
-    const __amdgpu_buffer_rsrc_t krsrc =
-        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p.K), (short)0, p.KR * (int)p.k_c * 4, 0x00020000);
+    // columns past k_c are never stored). Each block's loads go through a
+    // resource based at its first k-step, whose range ends at K's end, with a
+    // fixed vector offset per lane and step (the channel block's is the
+    // instruction's immediate): every offset stays in the vector operand that
+    // the range check covers, and the loads need no vector temporaries.
     const uint32_t klane = (uint32_t)((kofs * (int)p.k_c + n0 + m) * 4);
     const uint32_t kstep = (uint32_t)(2 * p.k_c * 4);  // bytes per k-step
+    const uint32_t kbytes = (uint32_t)(p.KR * p.k_c * 4);
+    uint32_t kvoff[kBlockSteps];
+#pragma unroll
+    for (int u = 0; u < kBlockSteps; ++u) kvoff[u] = klane + (uint32_t)u * kstep;
     // K fragments of a whole block are loaded one block ahead, into the other
     // of two register sets; the stream of k-steps wraps at nks (every group
     // reduces over the same rows of K).
     float kb0[kBlockSteps][NB], kb1[kBlockSteps][NB];
     int kt = 0;  // first k-step (mod nks) of the next block of K fragments
     auto kload_block = [&](float (*dst)[NB]) {
-        const uint32_t base = klane + (uint32_t)kt * kstep;
+        // kt <= nks - kBlockSteps, whose first row 2 kt lies inside K (the
+        // padding is less than one block), so the range is not empty
+        const uint32_t kfirst = (uint32_t)kt * kstep;
+        const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<float*>(p.K) + (int64_t)kt * 2 * p.k_c, (short)0, (int)(kbytes - kfirst), 0x00020000);
 #pragma unroll
         for (int u = 0; u < kBlockSteps; ++u)
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb)
-                dst[u][nb] = __builtin_bit_cast(
-                    float, __builtin_amdgcn_raw_buffer_load_b32(krsrc, base + u * kstep + 128 * nb, 0, 0));
+                dst[u][nb] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(kr, kvoff[u] + 128 * nb, 0, 0));
         kt = kt + kBlockSteps == p.nks ? 0 : kt + kBlockSteps;
         asm volatile("" ::: "memory");  // issued here, not sunk towards their use
     };
@@ -183,28 +215,25 @@ __device__ __forceinline__ void ring_item(const RingParams& p, float* ring, int6
             // this lane's ring position: element g*4*srow + ii*srow + kofs of its row
             ridx = (uint32_t)(g * kRRows * p.srow + ii * p.srow + kofs) & (kRingLen - 1);
         }
-        // The fills issued before this block have landed. After block 0 the
-        // last ones went out at the start of the previous block, followed by
-        // kBlockSteps * NB K loads (this block's fragments): all but those are
-        // complete. At block 0 the last ones went out before the previous
-        // group's O stores, whose count depends on the edges: wait for
-        // everything.
-        if (b > 0)
-            asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kBlockSteps * NB) : "memory");
-        else if (g > g_begin)
-            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        // Everything the previous block issued has landed: this block's K
+        // fragments and chunks (and, at the start of a later group, the
+        // previous group's O stores, issued last).
+        if (b > 0 || g > g_begin) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         if (filled < blk_hi(g, b)) {  // not reached while the ring holds a block ahead
             fill_upto(blk_hi(g, b));
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         }
+        // The next block's K fragments, issued before this block's fills: the
+        // registers they land in are then in flight when the fills' addresses
+        // are formed, so the compiler takes other registers for those (reusing
+        // a K register there would make it wait for every load in flight).
+        kload_block(knext);
         // prefetch the next block's chunks as far as the ring allows
         if (b + 1 < nblk) {
             const int cap = blk_lo(g, b) + kRingChunks - 1;
             const int want = blk_hi(g, b + 1);
             fill_upto(want < cap ? want : cap);
         }
-        // the next block's K fragments (this block's were loaded one block ago)
-        kload_block(knext);
         // the block's A fragments, all read up front (one LDS round trip per block)
         float a[kBlockSteps];
 #pragma unroll
@@ -232,22 +261,23 @@ __device__ __forceinline__ void ring_item(const RingParams& p, float* ring, int6
         }
         // O rows (pair, h) of this group, 32 channels per block: for register v
         // of lane l the row is acc_row(v, l) = 8*(v/4) + 4*(l/32) + v%4, i.e.
-        // output row h = 4g + v/4 of pair 4*(l/32) + v%4
+        // output row h = 4g + v/4 of pair 4*(l/32) + v%4. One buffer store per
+        // register, at the lane's fixed offset plus the row's scalar offset.
 #pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-            const int64_t pr = pair0 + kofs * 4 + q4;
-            if (pr >= p.pairs) continue;
-            const int64_t n = p.div_ow.div((uint32_t)pr), w = pr - n * p.o_w;
-            float* orow = p.O + ((n * p.o_h) * p.o_w + w) * p.k_c + n0 + m;
+        for (int r = 0; r < kRRows; ++r) {
+            const int64_t h = (int64_t)g * kRRows + r;
+            if (h >= p.o_h) break;
+            const int32_t soff = __builtin_amdgcn_readfirstlane((int32_t)(h * p.o_w * p.k_c * 4));
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int64_t h = (int64_t)g * kRRows + r;
-                if (h >= p.o_h) continue;
+            for (int q4 = 0; q4 < 4; ++q4)
 #pragma unroll
-                for (int nb = 0; nb < NB; ++nb)
-                    if (n0 + 32 * nb + m < p.k_c)
-                        __builtin_nontemporal_store(acc[nb][r * 4 + q4], orow + h * p.o_w * p.k_c + 32 * nb);
-            }
+                for (int nb = 0; nb < NB; ++nb) {
+                    // the element as a value first: a vector element has no
+                    // object representation of its own to reinterpret
+                    const float v = acc[nb][r * 4 + q4];
+                    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), orsrc,
+                                                          (int32_t)ooff[q4][nb], soff, kStoreNT);
+                }
         }
     };
     const int nbeta = (g_end - g_begin) * nblk;
@@ -342,6 +372,9 @@ bool gemm_ring_usable(const Shape& s, int dtype) {
     // lowered, 8 rows of L; fused, three images
     if (8 * s.i_h * s.R >= (int64_t(1) << 30)) return false;
     if (3 * s.i_h * s.i_w * s.i_c >= (int64_t(1) << 30)) return false;
+    // O byte offsets from the first image of an item's 8 pairs (at most 8
+    // images) plus an output row's stay below the dropped range
+    if (9 * s.o_h * s.o_w * s.k_c * 4 >= (int64_t)kStoreDrop) return false;
     return true;
 }
 
