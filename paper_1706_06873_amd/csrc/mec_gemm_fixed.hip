@@ -1604,10 +1604,13 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
         // tall kernels over short rows of L (11x11 over 3 channels: 33 elements):
         // the flat windows through a ring of LDS (mec_gemm_ring.hip), where the
         // ring holds four output rows' windows (strides up to 4 for 11x11).
-        // Measured on cv1 at batch 32: stride 4 325 -> 300 us at full size
-        // (alexnet_conv1), stride 3 207 -> 141 us; 7x7 stride 2 over 3
-        // channels (cv3) is even from L and 6% slower fused, so k_h >= 9.
-        if (!layout && s.k_h >= 9 && s.R <= 48 && gemm_ring_usable(s, dtype))
+        // Measured at batch 32 against the tiles, from L / fused: cv1 stride 3
+        // 207 -> 141 us; 7x7 stride 2 over 3 channels (cv3) 101 / 93 -> 86 us;
+        // 5x5 stride 2 over 3 channels 24 / 30 -> 18 us, over 6 channels 28 /
+        // 28 -> 21 us. At stride 1 below 9 rows it is even or slower (3x3 over
+        // 3 channels 51 / 50 -> 49 / 52 us, over 16 channels 92 / 81 -> 92 /
+        // 89 us; 5x5 over 8 channels even), so those keep the tiles.
+        if (!layout && (s.k_h >= 9 || (s.k_h >= 5 && s.s_h >= 2)) && s.R <= 48 && gemm_ring_usable(s, dtype))
             return dry_run ? hipSuccess : launch_gemm_ring(s, A, K, O, F, stream);
         if (s.R >= 32) {
             // no split into a strided layout: zeroing O would clear other pixels

@@ -1,7 +1,8 @@
 // MEC's slab products (Section 3.3, Algorithm 2, product phase) for tall,
 // strided kernels over few channels (fp32; the 11x11 first layers of Table 2,
-// cv1 and cv2, at strides 3 and 4), where a row of L is short (R = k_w*i_c =
-// 33) and the slab of one output row, k_h*R = 363 elements, spans many of them.
+// cv1 and cv2, at strides 3 and 4, and 5x5 or 7x7 kernels at stride 2 such as
+// cv3), where a row of L is short (R = k_w*i_c = 33 for 11x11 over 3 channels)
+// and the slab of one output row, k_h*R = 363 elements there, spans many of them.
 //
 // Section 3.2 views output row h of pair (n, w) as one dot product over a
 // contiguous window of that pair's row of L:

@@ -335,13 +335,13 @@ def test_f32_direct_to_lds_tiles(orc, dims, algo):
     assert rel_l2(run_conv(I, K, s_h, s_w, algo), orc.conv2d_direct(host(I), host(K), s_h, s_w)) <= TOL_F32
 
 
-# fp32 tall kernels over short rows (11x11 at strides 3 and 4, and other
-# k_h >= 9 with rows of L of at most 48 elements): the flat-window kernel (one
-# wave per workgroup, 8 pairs x 4 output rows per MFMA block, rows of L
-# streamed through a ring in LDS). The cases reach a ragged last pair group,
-# o_h not a multiple of 4, one, two and three 32-channel blocks, several
-# channel tiles, pair groups across images, s_w = 1, 2 and 3, i_c = 1 and 2,
-# strides of 3 to 16 down, and o = 1 x 1.
+# fp32 tall kernels over short rows (11x11 at strides 3 and 4, other k_h >= 9,
+# and k_h of 5 to 8 at strides of 2 and more down, with rows of L of at most 48
+# elements): the flat-window kernel (one wave per workgroup, 8 pairs x 4 output
+# rows per MFMA block, rows of L streamed through a ring in LDS). The cases
+# reach a ragged last pair group, o_h not a multiple of 4, one, two and three
+# 32-channel blocks, several channel tiles, pair groups across images, s_w = 1,
+# 2 and 3, i_c = 1, 2, 3 and 6, strides of 2 to 16 down, and o = 1 x 1.
 RING_CASES = [
     (1, 35, 31, 3, 11, 11, 96, 4, 4),     # 3 row groups: items of 2 and 1 groups
     (2, 39, 27, 3, 11, 11, 40, 4, 4),     # two channel blocks, the second 8 wide
@@ -358,6 +358,10 @@ RING_CASES = [
     (2, 33, 20, 2, 9, 5, 70, 3, 2),       # 9x5 over 2 channels (R = 10), stride 3 x 2
     (1, 40, 9, 1, 13, 3, 130, 9, 1),      # 13x3, stride 9 down (R = 3)
     (1, 60, 9, 1, 20, 3, 130, 16, 1),     # 20x3, stride 16 down
+    (2, 29, 25, 3, 7, 7, 64, 2, 2),       # 7x7 stride 2 over 3 channels (cv3-like)
+    (3, 21, 19, 3, 5, 5, 40, 2, 2),       # 5x5 stride 2, two channel blocks
+    (1, 23, 30, 6, 5, 5, 100, 2, 3),      # 5x5 over 6 channels, stride 2 x 3, two channel tiles
+    (2, 20, 17, 2, 6, 3, 33, 3, 2),       # 6x3 stride 3 down over 2 channels
 ]
 
 
