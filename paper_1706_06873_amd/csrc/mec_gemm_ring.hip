@@ -15,8 +15,9 @@
 // rows reduce over the same index j at every step and share one fragment of
 // K (read from global memory, where every wave finds it in the L2 cache). The
 // reduction runs over the window's k_h*R elements in steps of 2 (one
-// v_mfma_f32_32x32x2_f32), padded with zeros to whole blocks of 8 steps (363
-// -> 368, 1.4%): no per-row padding of R to a staging width. The wave streams its 8 pairs' rows of L (or, fused,
+// v_mfma_f32_32x32x2_f32), padded with zeros to whole blocks of 7 or 8 steps
+// (363 -> 364): no per-row padding of R to a staging width. The wave streams
+// its 8 pairs' rows of L (or, fused,
 // the same elements of I) through a ring in LDS, 512 elements per pair, filled
 // 64 elements at a time by direct-to-LDS loads one block of k-steps ahead of
 // use; every element of the rows it covers is loaded once per item, the
@@ -37,7 +38,8 @@ constexpr int kRingLen = kChunk * kRingChunks;
 // SIMD and two on the others: measured 1.5% slower); 636 = -4 mod 64 banks, so
 // a fragment read of 8 pairs x 4 rows spreads over the banks
 constexpr int kRingLD = kRingLen + 124;
-constexpr int kBlockSteps = 8;             // k-steps between fill points
+// k-steps between fill points (BS): 8, or 7 where that pads the reduction less
+// (the window's ceil(k_h*R / 2) steps are rounded up to whole blocks)
 constexpr int kWavesPerCU = 8;             // resident waves per compute unit (LDS: 8 rings)
 constexpr uint32_t kStoreDrop = 0x80000000u;  // O byte offsets from here on are out of range
 constexpr int kStoreNT = 2;                // cache policy of the O stores: non-temporal
@@ -77,7 +79,7 @@ __device__ inline void ring_dma(const float* base, uint32_t voff, uint32_t lds) 
 
 // One piece of work: row groups g_begin .. g_end-1 of the 8 pairs from pair0,
 // channels n0 .. n0 + 32*NB.
-template <int NB, bool FUSED>
+template <int NB, bool FUSED, int BS>
 __device__ __forceinline__ void ring_item(const RingParams& p, float* ring, int64_t pair0, int g_begin,
                                           int g_end, int n0) {
     const int lane = threadIdx.x;
@@ -152,11 +154,11 @@ __device__ __forceinline__ void ring_item(const RingParams& p, float* ring, int6
     };
     // chunks read by block b of group g: [lo, hi]
     const int rspan = (kRRows - 1) * p.srow;
-    auto blk_lo = [&](int g, int b) { return (g * kRRows * p.srow + 2 * kBlockSteps * b) / kChunk; };
+    auto blk_lo = [&](int g, int b) { return (g * kRRows * p.srow + 2 * BS * b) / kChunk; };
     auto blk_hi = [&](int g, int b) {
-        return (g * kRRows * p.srow + rspan + 2 * kBlockSteps * b + 2 * kBlockSteps - 1) / kChunk;
+        return (g * kRRows * p.srow + rspan + 2 * BS * b + 2 * BS - 1) / kChunk;
     };
-    const int nblk = (p.nks + kBlockSteps - 1) / kBlockSteps;
+    const int nblk = (p.nks + BS - 1) / BS;
 
     // K fragment of k-step t, channel block nb: K[2t + kofs][n0 + 32 nb + m],
     // by buffer loads whose range check returns 0 past K's last element: the
@@ -169,26 +171,26 @@ __device__ __forceinline__ void ring_item(const RingParams& p, float* ring, int6
     const uint32_t klane = (uint32_t)((kofs * (int)p.k_c + n0 + m) * 4);
     const uint32_t kstep = (uint32_t)(2 * p.k_c * 4);  // bytes per k-step
     const uint32_t kbytes = (uint32_t)(p.KR * p.k_c * 4);
-    uint32_t kvoff[kBlockSteps];
+    uint32_t kvoff[BS];
 #pragma unroll
-    for (int u = 0; u < kBlockSteps; ++u) kvoff[u] = klane + (uint32_t)u * kstep;
+    for (int u = 0; u < BS; ++u) kvoff[u] = klane + (uint32_t)u * kstep;
     // K fragments of a whole block are loaded one block ahead, into the other
     // of two register sets; the stream of k-steps wraps at nks (every group
     // reduces over the same rows of K).
-    float kb0[kBlockSteps][NB], kb1[kBlockSteps][NB];
+    float kb0[BS][NB], kb1[BS][NB];
     int kt = 0;  // first k-step (mod nks) of the next block of K fragments
     auto kload_block = [&](float (*dst)[NB]) {
-        // kt <= nks - kBlockSteps, whose first row 2 kt lies inside K (the
+        // kt <= nks - BS, whose first row 2 kt lies inside K (the
         // padding is less than one block), so the range is not empty
         const uint32_t kfirst = (uint32_t)kt * kstep;
         const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc(
             const_cast<float*>(p.K) + (int64_t)kt * 2 * p.k_c, (short)0, (int)(kbytes - kfirst), 0x00020000);
 #pragma unroll
-        for (int u = 0; u < kBlockSteps; ++u)
+        for (int u = 0; u < BS; ++u)
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb)
                 dst[u][nb] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(kr, kvoff[u] + 128 * nb, 0, 0));
-        kt = kt + kBlockSteps == p.nks ? 0 : kt + kBlockSteps;
+        kt = kt + BS == p.nks ? 0 : kt + BS;
         asm volatile("" ::: "memory");  // issued here, not sunk towards their use
     };
     kload_block(kb0);
@@ -236,18 +238,18 @@ __device__ __forceinline__ void ring_item(const RingParams& p, float* ring, int6
             fill_upto(want < cap ? want : cap);
         }
         // the block's A fragments, all read up front (one LDS round trip per block)
-        float a[kBlockSteps];
+        float a[BS];
 #pragma unroll
-        for (int u = 0; u < kBlockSteps; ++u) a[u] = ring[abase + ((ridx + 2 * u) & (kRingLen - 1))];
-        const int t = b * kBlockSteps;
-        if (2 * (t + kBlockSteps) > p.KR) {  // the block reaches past KR: zeros there
+        for (int u = 0; u < BS; ++u) a[u] = ring[abase + ((ridx + 2 * u) & (kRingLen - 1))];
+        const int t = b * BS;
+        if (2 * (t + BS) > p.KR) {  // the block reaches past KR: zeros there
 #pragma unroll
-            for (int u = 0; u < kBlockSteps; ++u)
+            for (int u = 0; u < BS; ++u)
                 if (2 * (t + u) + kofs >= p.KR) a[u] = 0.f;
         }
-        ridx = (ridx + 2 * kBlockSteps) & (kRingLen - 1);
+        ridx = (ridx + 2 * BS) & (kRingLen - 1);
 #pragma unroll
-        for (int u = 0; u < kBlockSteps; ++u)
+        for (int u = 0; u < BS; ++u)
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb)
                 acc[nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[u], kuse[u][nb], acc[nb], 0, 0, 0);
@@ -300,7 +302,7 @@ __device__ __forceinline__ void ring_item(const RingParams& p, float* ring, int6
 // block: when the whole items leave a last, partial round on the wave slots,
 // its items would otherwise run alone at the end while the other slots idle
 // (alexnet_conv1: 12320 one-group items on 2048 slots leave 32).
-template <int NB, bool FUSED>
+template <int NB, bool FUSED, int BS>
 __global__ __launch_bounds__(64) void slab_gemm_f32_ring_kernel(RingParams p) {
     __shared__ __align__(16) float ring[kRPairs * kRingLD];
     if (blockIdx.x < p.nfull) {
@@ -308,7 +310,7 @@ __global__ __launch_bounds__(64) void slab_gemm_f32_ring_kernel(RingParams p) {
         const uint32_t unit = t / (uint32_t)p.n_tiles;
         const int g_begin = (int)(unit % (uint32_t)p.items_pg) * p.gpi;
         const int g_end = g_begin + p.gpi < p.ngroups ? g_begin + p.gpi : p.ngroups;
-        ring_item<NB, FUSED>(p, ring, (int64_t)(unit / (uint32_t)p.items_pg) * kRPairs, g_begin, g_end,
+        ring_item<NB, FUSED, BS>(p, ring, (int64_t)(unit / (uint32_t)p.items_pg) * kRPairs, g_begin, g_end,
                              (int)(t % (uint32_t)p.n_tiles) * 32 * NB);
     } else {
         // one channel tile (n_tiles == 1): piece = (item, group of the item, channel block)
@@ -317,7 +319,7 @@ __global__ __launch_bounds__(64) void slab_gemm_f32_ring_kernel(RingParams p) {
         const uint32_t unit = p.nfull + piece / per, sub = piece % per;
         const int g = (int)(unit % (uint32_t)p.items_pg) * p.gpi + (int)(sub / NB);
         if (g < p.ngroups)
-            ring_item<1, FUSED>(p, ring, (int64_t)(unit / (uint32_t)p.items_pg) * kRPairs, g, g + 1,
+            ring_item<1, FUSED, BS>(p, ring, (int64_t)(unit / (uint32_t)p.items_pg) * kRPairs, g, g + 1,
                                 (int)(sub % NB) * 32);
     }
 }
@@ -327,29 +329,46 @@ struct RingPlan {
     int64_t nfull, npieces;  // whole items, then single-group single-block pieces
 };
 
+// k-steps per block for a window of KR elements: 7 where whole blocks of 7 pad
+// its ceil(KR / 2) steps less than blocks of 8 (alexnet_conv1: 182 steps, no
+// padding against 184; 3x3 over 3 channels: 14 against 16), else 8.
+int ring_block_steps(int64_t KR) {
+    const int64_t st = (KR + 1) / 2;
+    return (st + 6) / 7 * 7 < (st + 7) / 8 * 8 ? 7 : 8;
+}
+int64_t ring_nks(int64_t KR, int bs) { return ((KR + 1) / 2 + bs - 1) / bs * bs; }
+
+constexpr int kMaxGroupsPerItem = 8;
+// An item's start in k-steps of one channel block (one MFMA each): its first
+// chunks are loaded before any product, about 2 us with two waves per SIMD.
+constexpr int64_t kItemStart = 37;
+
 // The launch's layout: gpi row groups per item, and the items of a last,
 // partial round on the wave slots split into one workgroup per row group and
 // 32-channel block when they are few (at most a quarter of the slots) and
 // there is something to split (one channel tile of several blocks, or items
-// of two groups). Two groups per item halve the items' start-ups (the first
-// chunks are loaded before the first product) and are taken when every slot
-// still gets an item and the estimated time, in rounds of the slots, is not
-// longer than with one (alexnet_conv1: 6160 two-group items, 16 of them
-// split, against 12320 one-group items, 32 of them split: 1% faster).
-RingPlan ring_plan(int64_t pgroups, int ngroups, int n_tiles, int nb, int64_t slots) {
+// of several groups). gpi (1 to 8, every slot still given an item) minimises
+// the estimated time of the busiest slot, in k-steps of one channel block: a
+// whole item costs gpi * steps * nb plus its start, a split piece steps plus
+// its start, each round of the slots the most of what it runs. More groups
+// per item amortise the start over short reductions (3x3 over 3 channels:
+// 14 steps per group, 7 groups per item, vgg_first 50 -> 48 us); long ones
+// keep few (alexnet_conv1, 182 steps: 6160 two-group items, 16 of them split,
+// against 12320 one-group items, 32 of them split: 1% faster).
+RingPlan ring_plan(int64_t pgroups, int ngroups, int n_tiles, int nb, int64_t slots, int64_t steps) {
     RingPlan best{1, pgroups * ngroups * n_tiles, 0};
     if (slots <= 0) return best;
     int64_t best_cost = -1;
-    for (int gpi = 1; gpi <= 2; ++gpi) {
-        if (gpi > 1 && ngroups < 2) break;
+    for (int gpi = 1; gpi <= kMaxGroupsPerItem && gpi <= ngroups; ++gpi) {
         const int64_t items = pgroups * ((ngroups + gpi - 1) / gpi) * n_tiles;
         const int64_t rounds = items / slots, r = items % slots;
         if (gpi > 1 && rounds == 0) break;  // would leave slots without an item
         const bool split = n_tiles == 1 && nb * gpi > 1 && rounds > 0 && r > 0 && 4 * r <= slots;
-        // in units of one 32-channel block of one row group
-        const int64_t cost = rounds * gpi * nb + (r == 0 ? 0 : split ? 1 : gpi * nb);
-        if (best_cost < 0 || cost <= best_cost) {
-            best = {gpi, split ? items - r : items, split ? r * nb * gpi : 0};
+        const int64_t pieces = split ? r * nb * gpi : 0;
+        const int64_t item = gpi * steps * nb + kItemStart, piece = steps + kItemStart;
+        const int64_t cost = rounds * item + (r == 0 ? 0 : split ? (pieces + slots - 1) / slots * piece : item);
+        if (best_cost < 0 || cost < best_cost) {
+            best = {gpi, split ? items - r : items, pieces};
             best_cost = cost;
         }
     }
@@ -361,13 +380,13 @@ RingPlan ring_plan(int64_t pgroups, int ngroups, int n_tiles, int nb, int64_t sl
 bool gemm_ring_usable(const Shape& s, int dtype) {
     if (dtype != 0) return false;
     const int64_t srow = s.s_h * s.R;
+    const int bs = ring_block_steps(s.k_h * s.R);
     // the ring holds the chunks one block of the four rows reads plus the next
-    // block's: (3 srow + 4 kBlockSteps + 62) / 64 < 8 chunks
-    if ((kRRows - 1) * srow + 4 * kBlockSteps + 62 > (int64_t)kRingLen - 1) return false;
+    // block's: (3 srow + 4 bs + 62) / 64 < 8 chunks
+    if ((kRRows - 1) * srow + 4 * bs + 62 > (int64_t)kRingLen - 1) return false;
     // the next group's first chunk is not older than this group's last block's:
     // reads never move back past what the ring has already dropped
-    const int64_t nks = ((s.k_h * s.R + 1) / 2 + kBlockSteps - 1) / kBlockSteps * kBlockSteps;
-    if (2 * (nks - kBlockSteps) > kRRows * srow) return false;
+    if (2 * (ring_nks(s.k_h * s.R, bs) - bs) > kRRows * srow) return false;
     if (s.R * s.k_h > (int64_t(1) << 20) || s.pairs >= (int64_t(1) << 31)) return false;
     // byte offsets of one dword load within a pair group's source fit 32 bits:
     // lowered, 8 rows of L; fused, three images
@@ -395,7 +414,8 @@ hipError_t launch_gemm_ring(const Shape& s, const void* A, const void* K, float*
     p.w_stride = fused ? s.s_w * s.i_c : s.i_h * s.R;
     p.R = (int32_t)s.R;
     p.KR = (int32_t)(s.k_h * s.R);
-    p.nks = ((p.KR + 1) / 2 + kBlockSteps - 1) / kBlockSteps * kBlockSteps;
+    const int bs = ring_block_steps(p.KR);
+    p.nks = (int32_t)ring_nks(p.KR, bs);
     p.srow = (int32_t)(s.s_h * s.R);
     p.ngroups = (int32_t)((s.o_h + kRRows - 1) / kRRows);
     p.divR = FastDiv((uint32_t)s.R);
@@ -410,23 +430,26 @@ hipError_t launch_gemm_ring(const Shape& s, const void* A, const void* K, float*
             hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && cus > 0)
             slots = (int64_t)kWavesPerCU * cus;
     }
-    const RingPlan plan = ring_plan(pgroups, p.ngroups, p.n_tiles, nb, slots);
+    const RingPlan plan = ring_plan(pgroups, p.ngroups, p.n_tiles, nb, slots, p.nks);
     if (plan.nfull + plan.npieces > 0x7fffffff) return hipErrorInvalidValue;
     p.gpi = plan.gpi;
     p.items_pg = (p.ngroups + p.gpi - 1) / p.gpi;
     p.nfull = (uint32_t)plan.nfull;
     const int64_t nfull = plan.nfull, npieces = plan.npieces;
     const dim3 grid((uint32_t)(nfull + npieces)), block(64);
-#define MEC_RING(NB_)                                                                         \
-    if (nb == NB_) {                                                                          \
-        if (fused)                                                                            \
-            hipLaunchKernelGGL((slab_gemm_f32_ring_kernel<NB_, true>), grid, block, 0, stream, p); \
-        else                                                                                  \
-            hipLaunchKernelGGL((slab_gemm_f32_ring_kernel<NB_, false>), grid, block, 0, stream, p); \
+#define MEC_RING(NB_, BS_)                                                                        \
+    if (nb == NB_ && bs == BS_) {                                                                 \
+        if (fused)                                                                                \
+            hipLaunchKernelGGL((slab_gemm_f32_ring_kernel<NB_, true, BS_>), grid, block, 0, stream, p); \
+        else                                                                                      \
+            hipLaunchKernelGGL((slab_gemm_f32_ring_kernel<NB_, false, BS_>), grid, block, 0, stream, p); \
     }
-    MEC_RING(1)
-    MEC_RING(2)
-    MEC_RING(3)
+    MEC_RING(1, 7)
+    MEC_RING(2, 7)
+    MEC_RING(3, 7)
+    MEC_RING(1, 8)
+    MEC_RING(2, 8)
+    MEC_RING(3, 8)
 #undef MEC_RING
     return hipGetLastError();
 }
