@@ -144,19 +144,28 @@ class Config:
         self.I0, self.K0 = wl.make_inputs(layer)
         # Enough sets that no kernel's rotating footprint fits the 256 MB
         # memory-attached last-level cache: every launch reads its operands from
-        # HBM, as the rooflines assume.
+        # HBM, as the rooflines assume. Each kernel rotates over at least
+        # MIN_ROTATION_BYTES of its own operands, and not many times more: I
+        # and the workspace over the sets the lowering needs, O over the
+        # (fewer or as many) sets the products need, set j writing O number
+        # j % o_sets. (vgg_first's 39 MB lowering needs 28 sets; its 205 MB O
+        # over 28 sets would be 6.8 GB rotating, past what the address
+        # translation caches cover, where 5 sets span 1 GiB.)
+        prod_foot = es * (self.size_W + self.size_K) + 4 * self.size_O
         if algo == "fused":
-            foot = es * (self.size_I + self.size_K) + 4 * self.size_O
+            prod_foot = es * (self.size_I + self.size_K) + 4 * self.size_O
+            n_io = n_o = min(max(nsets, -(-MIN_ROTATION_BYTES // prod_foot)), 256)
         else:
-            foot = min(es * (self.size_I + self.size_W), es * (self.size_W + self.size_K) + 4 * self.size_O)
-        nsets = min(max(nsets, -(-MIN_ROTATION_BYTES // foot)), 256)
+            n_io = min(max(nsets, -(-MIN_ROTATION_BYTES // (es * (self.size_I + self.size_W)))), 256)
+            n_o = min(max(nsets, -(-MIN_ROTATION_BYTES // prod_foot)), n_io)
+        self.o_sets = n_o
+        outs = [torch.empty((i_n, o_h, o_w, k_c), dtype=torch.float32, device=dev) for _ in range(n_o)]
         self.sets = []
-        for j in range(nsets):
+        for j in range(n_io):
             I = self.I0.to(dev)
             if j:
                 I = I.clone()
-            b = dict(I=I, K=self.K0.to(dev),
-                     O=torch.empty((i_n, o_h, o_w, k_c), dtype=torch.float32, device=dev))
+            b = dict(I=I, K=self.K0.to(dev), O=outs[j % n_o])
             if algo != "fused":
                 # the workspace the library asks for, in bytes
                 b["W"] = torch.empty(self.ws, dtype=torch.uint8, device=dev)
@@ -280,6 +289,7 @@ def measure(cfg, HipEvent, steps, warmup, digest, settle_s):
             "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
             "frac": round(gbs / PEAK_HBM_GBS, 4) if layer.name != "tiny" else None,
             "traffic": traffic["lower"], "alg_bytes": lb}
+    out["buffer_sets"], out["o_sets"] = len(cfg.sets), cfg.o_sets
     out["workspace_bytes"] = cfg.ws
     out["im2col_bytes"] = cfg.ws_im2col
     out["workspace_vs_mec_closed_form"] = round(cfg.ws / cfg.ws_lowered, 4) if cfg.algo == "lowered" else None
@@ -342,7 +352,7 @@ def main():
         "dtype": layer.dtype,
         "data": "synthetic (seeded, %s)" % layer.note,
         "config": {"workload": workload_name(layer, cfg.o_h, cfg.o_w),
-                   "algo": args.algo, "buffer_sets": len(cfg.sets)},
+                   "algo": args.algo, "buffer_sets": len(cfg.sets), "o_sets": cfg.o_sets},
         "workspace_bytes": cfg.ws,
         "im2col_bytes": cfg.ws_im2col,
         "workspace_vs_im2col": round(cfg.ws_im2col / cfg.ws_lowered, 4),

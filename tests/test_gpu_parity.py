@@ -336,8 +336,8 @@ def test_f32_direct_to_lds_tiles(orc, dims, algo):
 
 
 # fp32 tall kernels over short rows (11x11 at strides 3 and 4, other k_h >= 9,
-# k_h of 5 to 8 at strides of 2 and more down, and k_h >= 3 over rows of at most
-# 10 elements, with rows of L of at most 48 elements): the flat-window kernel (one wave per workgroup, 8 pairs x 4 output
+# k_h of 5 to 8 at strides of 2 and more down, and, fused, k_h >= 3 over rows of
+# at most 10 elements, with rows of L of at most 48 elements): the flat-window kernel (one wave per workgroup, 8 pairs x 4 output
 # rows per MFMA block, rows of L streamed through a ring in LDS). The cases
 # reach a ragged last pair group, o_h not a multiple of 4, one, two and three
 # 32-channel blocks, several channel tiles, pair groups across images, s_w = 1,
@@ -828,7 +828,8 @@ def test_layer_reduced_batch_full_compare(orc, name):
 def test_layer_full_size_sampled(orc, name):
     """Full-size layers in the benchmark's launch configuration, checked on
     sampled outputs the oracle computes one by one (corners included), and
-    LOWERED == FUSED bit for bit (same staged values, same reduction order)."""
+    LOWERED == FUSED bit for bit (same staged values, same reduction order)
+    where both take the same kernel."""
     layer = wl.LAYERS[name]
     say("layer full sampled", name)
     I, K = wl.make_inputs(layer)
@@ -846,7 +847,13 @@ def test_layer_full_size_sampled(orc, name):
     ref = orc.conv2d_points(host(I), host(K), s_h, s_w, idx)
     g1 = O1.cpu().numpy()
     assert rel_l2(g1[tuple(idx.T)], ref) <= TOL_F32
-    assert torch.equal(O1, O2)
+    i_n, i_h, i_w, i_c, k_h, k_w, k_c, _, _ = layer.dims
+    if layer.dtype == "f32" and 3 <= k_h < 9 and s_h == 1 and k_w * i_c <= 10:
+        # rows of at most 10 elements: fused through the ring kernel, from L
+        # through the streaming kernel -- the same sums in another order
+        assert rel_l2(O2.cpu().numpy(), g1) <= TOL_F32
+    else:
+        assert torch.equal(O1, O2)
     assert np.isfinite(g1).all()
 
 
