@@ -1430,6 +1430,10 @@ template <bool F> using F32K3S2Wide = F32Cfg<2, 2, 2, 16, 3, 2, 4, 4, F>;
 template <bool F> using F32K3S2Narrow = F32Cfg<2, 2, 2, 4, 3, 2, 1, 4, F>;
 template <bool F> using F32K3S2Scalar = F32Cfg<2, 2, 2, 4, 3, 2, 1, 1, F>;
 template <bool F> using F32K7S2Wide = F32Cfg<8, 2, 2, 8, 7, 2, 4, 4, F>;
+// the same with 4 and 2 output rows, where 8-row tiles leave the chip idle
+// or rows 4 at a time run faster (chosen in dispatch_fixed)
+template <bool F> using F32K7S2Wide4 = F32Cfg<4, 2, 2, 8, 7, 2, 4, 4, F>;
+template <bool F> using F32K7S2Wide2 = F32Cfg<2, 2, 2, 8, 7, 2, 4, 4, F>;
 template <bool F> using F32K7S2Narrow = F32Cfg<8, 2, 4, 4, 7, 2, 1, 4, F>;
 template <bool F> using F32K7S2Scalar = F32Cfg<8, 2, 4, 4, 7, 2, 1, 1, F>;
 // fp32, 2x2 and 4x4 (any k_w) stride 1, 16-byte rows: 32 pairs x 8 rows x 64
@@ -1644,6 +1648,21 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
         MEC_TRY_FIXED(F32K3S2Wide<F>);
         MEC_TRY_FIXED(F32K3S2Narrow<F>);
         MEC_TRY_FIXED(F32K3S2Scalar<F>);
+        if (s.k_h == 7 && s.s_h == 2) {
+            // Rows per tile: 4 where that gives a tile per compute unit, else 2,
+            // split between two workgroups where 2-row tiles still leave compute
+            // units idle. Measured on 224x224x64 -> 64 (cv4's shape), 8 / 4 / 2
+            // rows / 2 rows split, from L: batch 1 267 / 129 / 84 / 78 us,
+            // batch 4 283 / 227 / 250 / 255 us, batch 32 1416 / 1338 / 1452 us.
+            const int64_t ptiles = (s.pairs + kPairs - 1) / kPairs, ctiles = (s.k_c + 63) / 64;
+            const int64_t t4 = ptiles * ((s.o_h + 3) / 4) * ctiles, t2 = ptiles * ((s.o_h + 1) / 2) * ctiles;
+            if (t4 >= 256) {
+                MEC_TRY_FIXED(F32K7S2Wide4<F>);
+            } else {
+                const bool split = t2 < 256 && !layout && s.pairs * s.o_h * s.k_c <= (int64_t(1) << 20);
+                MEC_TRY_FIXED_SPLIT(F32K7S2Wide2<F>, split ? 2 : 1);
+            }
+        }
         MEC_TRY_FIXED(F32K7S2Wide<F>);
         MEC_TRY_FIXED(F32K7S2Narrow<F>);
         MEC_TRY_FIXED(F32K7S2Scalar<F>);

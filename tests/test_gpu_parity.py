@@ -451,6 +451,33 @@ def test_ring_split_tail(orc, gpi, k_c, algo):
     assert np.array_equal(run_conv(I, K, 4, 4, algo), ref.astype(np.float32))
 
 
+# fp32 7x7 stride 2 tiles, rows per tile by the tile count: 2 rows split
+# between two workgroups (few tiles), 2 rows unsplit (4-row tiles short of one
+# per compute unit, 2-row tiles not), 4 rows (a tile per compute unit), with
+# one and two channel tiles and ragged pairs, rows and channels. Bit for bit on
+# integers (the split adds exactly two partial sums onto zero).
+K7S2_CASES = [
+    (2, 21, 19, 16, 7, 7, 40, 2, 2),      # 2 rows, split
+    (3, 30, 31, 8, 7, 7, 100, 2, 2),      # 2 rows, split, two channel tiles
+    (8, 100, 100, 8, 7, 7, 64, 2, 2),     # 2 rows: 144 4-row tiles, 288 2-row tiles
+    (16, 100, 99, 8, 7, 7, 60, 2, 2),     # 4 rows: 288 tiles
+    (8, 101, 100, 4, 7, 7, 100, 2, 2),    # 4 rows, two channel tiles
+]
+
+
+@pytest.mark.parametrize("dims", K7S2_CASES)
+@pytest.mark.parametrize("algo", ["lowered", "fused"])
+def test_k7s2_row_choice(orc, dims, algo):
+    say("7x7 stride 2", algo, dims)
+    s_h, s_w = dims[7], dims[8]
+    Ii, Ki = case(107 + sum(dims), dims, dist="int")
+    refi = orc.conv2d_direct(host(Ii), host(Ki), s_h, s_w)
+    assert np.abs(refi).max() < 2 ** 24
+    assert np.array_equal(run_conv(Ii, Ki, s_h, s_w, algo), refi.astype(np.float32))
+    I, K = case(109 + sum(dims), dims)
+    assert rel_l2(run_conv(I, K, s_h, s_w, algo), orc.conv2d_direct(host(I), host(K), s_h, s_w)) <= TOL_F32
+
+
 # fp32 3x3 stride 2 tiles (32 pairs x 2 output rows, 5 staged rows): rows of
 # a multiple of 4 (16-byte loads), short rows (element loads of I and L), k_c
 # not a multiple of 4 (element loads of K), ragged pairs, rows and channels,
