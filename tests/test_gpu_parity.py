@@ -89,7 +89,10 @@ SWEEP_BF16 = [
     (3, 18, 16, 40, 3, 3, 136, 1, 1),    # bf16 3x3: two channel tiles, the second ragged
     (2, 9, 40, 24, 3, 3, 8, 1, 2),       # bf16 3x3, R not a multiple of the r-chunk
     (2, 14, 13, 32, 5, 5, 136, 1, 1),    # bf16 5x5 s1: two channel tiles, the second ragged
-    (2, 21, 19, 16, 7, 7, 40, 2, 2),     # bf16 7x7 s2, ragged channels
+    (2, 21, 19, 16, 7, 7, 40, 2, 2),     # bf16 7x7 s2, ragged channels (the 64-channel tile)
+    (3, 29, 27, 16, 7, 7, 64, 2, 2),     # bf16 7x7 s2, 64 channels, ragged pairs and rows
+    (1, 21, 23, 8, 7, 7, 24, 2, 2),      # bf16 7x7 s2, fewer channels than one block
+    (2, 21, 19, 16, 7, 7, 96, 2, 2),     # bf16 7x7 s2, the 128-channel tile
     (2, 35, 33, 3, 11, 11, 104, 4, 3),   # bf16 11x11 s4, rows of 33 gathered by element, two channel tiles
     (1, 27, 29, 5, 11, 11, 40, 4, 4),    # the same, rows of 55
     (1, 23, 25, 3, 7, 7, 72, 2, 3),      # bf16 7x7 s2, rows of 21: the generic kernel
