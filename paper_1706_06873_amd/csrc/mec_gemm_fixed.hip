@@ -1445,6 +1445,9 @@ template <bool F> using F32K4S1Wide = F32Cfg<8, 2, 2, 16, 4, 1, 4, 4, F>;
 template <bool F> using F32K5S1Wide = F32Cfg<4, 2, 2, 16, 5, 1, 4, 4, F>;
 // direct-to-LDS staging: 2.4% faster from I on cv5, 1% slower from L
 template <bool F> using F32K5S1WideD = F32Cfg<4, 2, 2, 16, 5, 1, 4, 4, F, 4, true>;
+// 2 output rows, where 4-row tiles leave the chip idle (chosen in dispatch_fixed)
+template <bool F> using F32K5S1Wide2 = F32Cfg<2, 2, 2, 16, 5, 1, 4, 4, F>;
+template <bool F> using F32K5S1Wide2D = F32Cfg<2, 2, 2, 16, 5, 1, 4, 4, F, 4, true>;
 template <bool F> using F32K5S1Narrow = F32Cfg<4, 2, 2, 4, 5, 1, 1, 4, F>;
 template <bool F> using F32K5S1Scalar = F32Cfg<4, 2, 2, 4, 5, 1, 1, 1, F>;
 // k_h = 1, stride 1: plain products with no slab overlap (1x1 convolutions,
@@ -1670,6 +1673,22 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
         MEC_TRY_FIXED(F32K7S2Wide<F>);
         MEC_TRY_FIXED(F32K7S2Narrow<F>);
         MEC_TRY_FIXED(F32K7S2Scalar<F>);
+        if (s.k_h == 5 && s.s_h == 1) {
+            // 2 rows per tile where 4-row tiles number fewer than the compute
+            // units, split between two workgroups where even 2-row tiles fill
+            // at most half of them. Measured on 24x24x96 -> 256 (cv5's shape),
+            // from L / fused, 4 rows -> 2 rows -> 2 rows split: batch 1 94 / 79
+            // -> 57 / 47 -> 35 / 29 us; batch 8 86 / 80 -> 56 / 47 (split 62 /
+            // 56); batch 32 (400 4-row tiles) unchanged at 157 / 158 us.
+            const int64_t ptiles = (s.pairs + kPairs - 1) / kPairs, ctiles = (s.k_c + 63) / 64;
+            const int64_t t4 = ptiles * ((s.o_h + 3) / 4) * ctiles, t2 = ptiles * ((s.o_h + 1) / 2) * ctiles;
+            if (t4 < 256) {
+                const int ks =
+                    2 * t2 <= 256 && !layout && s.pairs * s.o_h * s.k_c <= (int64_t(1) << 20) ? 2 : 1;
+                if (F) MEC_TRY_FIXED_SPLIT(F32K5S1Wide2D<F>, ks);
+                MEC_TRY_FIXED_SPLIT(F32K5S1Wide2<F>, ks);
+            }
+        }
         if (F) MEC_TRY_FIXED(F32K5S1WideD<F>);
         MEC_TRY_FIXED(F32K5S1Wide<F>);
         MEC_TRY_FIXED(F32K2S1Wide<F>);

@@ -481,6 +481,31 @@ def test_k7s2_row_choice(orc, dims, algo):
     assert rel_l2(run_conv(I, K, s_h, s_w, algo), orc.conv2d_direct(host(I), host(K), s_h, s_w)) <= TOL_F32
 
 
+# fp32 5x5 stride 1, rows per tile by the tile count: 2 rows split between two
+# workgroups (few tiles), 2 rows unsplit, 4 rows; from L and from I (whose
+# direct-to-LDS form needs rows of a multiple of 16), ragged pairs, rows and
+# channels.
+K5S1_CASES = [
+    (1, 24, 24, 96, 5, 5, 256, 1, 1),     # 2 rows, split (40 tiles)
+    (2, 15, 17, 8, 5, 5, 40, 1, 1),       # 2 rows, split, rows of 40
+    (8, 24, 24, 96, 5, 5, 200, 1, 1),     # 2 rows (200 tiles), k_c ragged
+    (32, 40, 39, 16, 5, 5, 64, 1, 1),     # 4 rows (315 tiles)
+]
+
+
+@pytest.mark.parametrize("dims", K5S1_CASES)
+@pytest.mark.parametrize("algo", ["lowered", "fused"])
+def test_k5s1_row_choice(orc, dims, algo):
+    say("5x5 stride 1", algo, dims)
+    s_h, s_w = dims[7], dims[8]
+    Ii, Ki = case(113 + sum(dims), dims, dist="int")
+    refi = orc.conv2d_direct(host(Ii), host(Ki), s_h, s_w)
+    assert np.abs(refi).max() < 2 ** 24
+    assert np.array_equal(run_conv(Ii, Ki, s_h, s_w, algo), refi.astype(np.float32))
+    I, K = case(115 + sum(dims), dims)
+    assert rel_l2(run_conv(I, K, s_h, s_w, algo), orc.conv2d_direct(host(I), host(K), s_h, s_w)) <= TOL_F32
+
+
 # fp32 3x3 stride 2 tiles (32 pairs x 2 output rows, 5 staged rows): rows of
 # a multiple of 4 (16-byte loads), short rows (element loads of I and L), k_c
 # not a multiple of 4 (element loads of K), ragged pairs, rows and channels,
