@@ -1,8 +1,9 @@
-// MEC's slab products (Section 3.3, Algorithm 2, product phase) for tall,
-// strided kernels over few channels (fp32; the 11x11 first layers of Table 2,
-// cv1 and cv2, at strides 3 and 4, and 5x5 or 7x7 kernels at stride 2 such as
-// cv3), where a row of L is short (R = k_w*i_c = 33 for 11x11 over 3 channels)
-// and the slab of one output row, k_h*R = 363 elements there, spans many of them.
+// MEC's slab products (Section 3.3, Algorithm 2, product phase) for kernels
+// over few channels (fp32): the tall, strided 11x11 first layers of Table 2
+// (cv1 and cv2, at strides 3 and 4), 5x5 or 7x7 kernels at stride 2 such as
+// cv3, and, from I, 3x3 kernels over 3 channels (vgg_first, cv7). A row of L
+// is short there (R = k_w*i_c = 33 for 11x11 over 3 channels) and the slab of
+// one output row, k_h*R = 363 elements for that layer, spans many of them.
 //
 // Section 3.2 views output row h of pair (n, w) as one dot product over a
 // contiguous window of that pair's row of L:
@@ -17,8 +18,8 @@
 // reduction runs over the window's k_h*R elements in steps of 2 (one
 // v_mfma_f32_32x32x2_f32), padded with zeros to whole blocks of 7 or 8 steps
 // (363 -> 364): no per-row padding of R to a staging width. The wave streams
-// its 8 pairs' rows of L (or, fused,
-// the same elements of I) through a ring in LDS, 512 elements per pair, filled
+// its 8 pairs' rows of L (or, fused, the same elements of I) through a ring in
+// LDS, 512 elements per pair, filled
 // 64 elements at a time by direct-to-LDS loads one block of k-steps ahead of
 // use; every element of the rows it covers is loaded once per item, the
 // overlap between output rows is read from the ring. Waves share nothing, so
