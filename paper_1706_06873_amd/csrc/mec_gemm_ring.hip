@@ -339,23 +339,40 @@ int ring_block_steps(int64_t KR) {
 }
 int64_t ring_nks(int64_t KR, int bs) { return ((KR + 1) / 2 + bs - 1) / bs * bs; }
 
-constexpr int kMaxGroupsPerItem = 8;
+constexpr int kMaxGroupsPerItem = 16;
 // An item's start in k-steps of one channel block (one MFMA each): its first
 // chunks are loaded before any product, about 2 us with two waves per SIMD.
 constexpr int64_t kItemStart = 37;
+
+// Estimated time, in sixteenths of a k-step of one channel block, of n
+// workgroups of `work` k-steps plus a start each over `slots` wave slots (two
+// per SIMD). Whole rounds run two waves to a SIMD. A last round over at most
+// half the slots leaves most of its waves alone on a SIMD, where the products
+// take about 0.7 of the time (measured 0.62-0.71 with one item per SIMD on
+// vgg_first and cv3) and the start, mostly load latency, no less; a last
+// round over more than half of them takes about 1/16 longer than a whole
+// round (measured +4% to +8%).
+int64_t ring_rounds_cost(int64_t n, int64_t work, int64_t slots) {
+    const int64_t q = n / slots, r = n % slots, unit = work + kItemStart;
+    int64_t t = q * unit * 16;
+    if (r > 0) t += 2 * r <= slots ? work * 56 / 5 + kItemStart * 16 : unit * 17;
+    return t;
+}
 
 // The launch's layout: gpi row groups per item, and the items of a last,
 // partial round on the wave slots split into one workgroup per row group and
 // 32-channel block when they are few (at most a quarter of the slots) and
 // there is something to split (one channel tile of several blocks, or items
-// of several groups). gpi (1 to 8, every slot still given an item) minimises
-// the estimated time of the busiest slot, in k-steps of one channel block: a
-// whole item costs gpi * steps * nb plus its start, a split piece steps plus
-// its start, each round of the slots the most of what it runs. More groups
-// per item amortise the start over short reductions (3x3 over 3 channels:
-// 14 steps per group, 7 groups per item, vgg_first 50 -> 48 us); long ones
-// keep few (alexnet_conv1, 182 steps: 6160 two-group items, 16 of them split,
-// against 12320 one-group items, 32 of them split: 1% faster).
+// of several groups). gpi (1 to 16) minimises the estimated time of the
+// busiest slot (ring_rounds_cost), where a whole item's products take
+// gpi * steps * nb k-steps of one channel block and a split piece's steps.
+// More groups per item amortise the start over short reductions (3x3 over 3
+// channels, 14 steps per group: vgg_first fused takes 14 groups per item, one
+// round of 1792 items on 2048 slots, 44.0 us against 46.3 with 7 groups in
+// 3584 items); long ones keep few (alexnet_conv1, 182 steps: 6160 two-group
+// items, 16 of them split). The model still keeps cv3 at batch 32 on 2 groups
+// per item and a split tail (84.9 us, against 89.5 with 7 groups in one
+// round) and cv7 at batch 1 on one group per item (7.5 us, against 7.8 with 2).
 RingPlan ring_plan(int64_t pgroups, int ngroups, int n_tiles, int nb, int64_t slots, int64_t steps) {
     RingPlan best{1, pgroups * ngroups * n_tiles, 0};
     if (slots <= 0) return best;
@@ -363,13 +380,12 @@ RingPlan ring_plan(int64_t pgroups, int ngroups, int n_tiles, int nb, int64_t sl
     for (int gpi = 1; gpi <= kMaxGroupsPerItem && gpi <= ngroups; ++gpi) {
         const int64_t items = pgroups * ((ngroups + gpi - 1) / gpi) * n_tiles;
         const int64_t rounds = items / slots, r = items % slots;
-        if (gpi > 1 && rounds == 0) break;  // would leave slots without an item
         const bool split = n_tiles == 1 && nb * gpi > 1 && rounds > 0 && r > 0 && 4 * r <= slots;
-        const int64_t pieces = split ? r * nb * gpi : 0;
-        const int64_t item = gpi * steps * nb + kItemStart, piece = steps + kItemStart;
-        const int64_t cost = rounds * item + (r == 0 ? 0 : split ? (pieces + slots - 1) / slots * piece : item);
+        const int64_t work = gpi * steps * nb;
+        const int64_t cost = split ? rounds * (work + kItemStart) * 16 + ring_rounds_cost(r * nb * gpi, steps, slots)
+                                   : ring_rounds_cost(items, work, slots);
         if (best_cost < 0 || cost < best_cost) {
-            best = {gpi, split ? items - r : items, pieces};
+            best = {gpi, split ? items - r : items, split ? r * nb * gpi : 0};
             best_cost = cost;
         }
     }

@@ -391,26 +391,37 @@ def ring_block_steps(KR):
     return 7 if (st + 6) // 7 * 7 < (st + 7) // 8 * 8 else 8
 
 
+def _ring_rounds_cost(n, work, slots):
+    """n workgroups of `work` k-steps plus a start of 37 over `slots` wave
+    slots, in sixteenths of a k-step: whole rounds at two waves per SIMD; a
+    last round over at most half the slots with products at 0.7 of the time,
+    over more than half 17/16 of a whole round."""
+    q, r = divmod(n, slots)
+    t = q * (work + 37) * 16
+    if r:
+        t += work * 56 // 5 + 37 * 16 if 2 * r <= slots else (work + 37) * 17
+    return t
+
+
 def ring_plan(pgroups, ngroups, n_tiles, nb, slots, steps):
     """The ring launch's layout as the library chooses it: (row groups per
-    item, whole items, split pieces). 1 to 8 groups per item, every slot
-    still given an item, minimising the estimated time of the busiest slot in
-    k-steps of one channel block (an item: gpi * steps * nb plus a start of
-    37; a split piece: steps plus the start); the items of a last, partial
-    round of at most a quarter of the slots split into one workgroup per row
-    group and 32-channel block."""
+    item, whole items, split pieces). 1 to 16 groups per item, minimising the
+    estimated time of the busiest slot (an item's products: gpi * steps * nb
+    k-steps of one channel block; a split piece's: steps); the items of a
+    last, partial round of at most a quarter of the slots split into one
+    workgroup per row group and 32-channel block."""
     best, best_cost = (1, pgroups * ngroups * n_tiles, 0), None
-    for gpi in range(1, min(8, ngroups) + 1):
+    for gpi in range(1, min(16, ngroups) + 1):
         items = pgroups * -(-ngroups // gpi) * n_tiles
         rounds, r = divmod(items, slots)
-        if gpi > 1 and rounds == 0:
-            break
         split = n_tiles == 1 and nb * gpi > 1 and rounds > 0 and r > 0 and 4 * r <= slots
-        pieces = r * nb * gpi if split else 0
-        item, piece = gpi * steps * nb + 37, steps + 37
-        cost = rounds * item + (0 if r == 0 else -(-pieces // slots) * piece if split else item)
+        work = gpi * steps * nb
+        if split:
+            cost = rounds * (work + 37) * 16 + _ring_rounds_cost(r * nb * gpi, steps, slots)
+        else:
+            cost = _ring_rounds_cost(items, work, slots)
         if best_cost is None or cost < best_cost:
-            best, best_cost = (gpi, items - r if split else items, pieces), cost
+            best, best_cost = (gpi, items - r if split else items, r * nb * gpi if split else 0), cost
     return best
 
 
@@ -425,6 +436,36 @@ def ring_split_batch(slots, o_h, o_w, k_c, gpi):
         if plan[0] == gpi and plan[2] >= 5 * nb * gpi:
             return n, plan
     raise AssertionError("no batch")
+
+
+# Items of more than 8 row groups, in a single round of fewer items than
+# wave slots (3x3 over one and three channels, fused, 8 channels): 10 groups
+# per item, each pair group's whole height, the last group one row; 9 and 8
+# groups per item over 17 groups; 16 groups per item, the last one one row.
+LONG_ITEM_CASES = [
+    ((175, 39, 49, 1, 3, 3, 8, 1, 1), 10),
+    ((126, 68, 49, 3, 3, 3, 8, 1, 1), 9),
+    ((197, 63, 49, 1, 3, 3, 8, 1, 1), 16),
+]
+
+
+@pytest.mark.parametrize("dims,gpi", LONG_ITEM_CASES)
+def test_ring_long_items(orc, dims, gpi):
+    """Bit for bit with integer inputs, full output, at the plan the library
+    takes on a device of 256 compute units (checked against the plan model)."""
+    n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w = dims
+    o_h, o_w = i_h - k_h + 1, i_w - k_w + 1
+    KR = k_h * k_w * i_c
+    bs = ring_block_steps(KR)
+    slots = 8 * torch.cuda.get_device_properties(0).multi_processor_count
+    plan = ring_plan(-(-n * o_w // 8), -(-o_h // 4), 1, 1, slots, -(-((KR + 1) // 2) // bs) * bs)
+    say("ring long items", dims, "plan", plan)
+    if slots == 2048:
+        assert plan[0] == gpi and plan[1] < slots and plan[2] == 0
+    I, K = case(89 + sum(dims), dims, dist="int")
+    ref = orc.conv2d_direct(host(I), host(K), s_h, s_w)
+    assert np.abs(ref).max() < 2 ** 24
+    assert np.array_equal(run_conv(I, K, s_h, s_w, "fused"), ref.astype(np.float32))
 
 
 _SPLIT_TAIL = {}
