@@ -9,8 +9,9 @@ products (mec_lower + mec_gemm, exactly the two kernels
 mec_conv2d(MEC_ALGO_LOWERED) enqueues), or the fused kernel
 (mec_conv2d(MEC_ALGO_FUSED)). The default layer is the largest fp32 one,
 AlexNet conv1 (i_n=128, 227x227x3, 11x11x96 kernel, stride 4), from L.
-Buffers rotate over several sets so that the 256 MB memory-attached
-last-level cache cannot serve a step from the previous one.
+Every operand a kernel reads rotates over at least 512 MB of buffer sets
+(twice the 256 MB memory-attached last-level cache), so that no launch finds
+it in that cache from an earlier one.
 
 Timing, with HIP events on the stream the kernels run on (created without the
 system-scope fence, so recording one adds no cache maintenance to what it
@@ -44,6 +45,7 @@ PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}   # dense MFMA peaks of the MI355X
 PEAK_HBM_GBS = 8000.0
 DEFAULT_LAYER = "alexnet_conv1"
 MIN_ROTATION_BYTES = 1 << 30   # bytes each kernel's rotating buffers span, at least
+READ_ROTATION_BYTES = 1 << 29  # bytes each operand a kernel reads rotates over, at least
 SWEEP_ALGOS = ("lowered", "fused")
 
 
@@ -142,34 +144,38 @@ class Config:
         self.size_W = self.ws // es   # |L| or |M| elements (0 fused)
         self.P = k_h * k_w * i_c      # im2col row length
         self.I0, self.K0 = wl.make_inputs(layer)
-        # Enough sets that no kernel's rotating footprint fits the 256 MB
-        # memory-attached last-level cache: every launch reads its operands from
-        # HBM, as the rooflines assume. Each kernel rotates over at least
-        # MIN_ROTATION_BYTES of its own operands, and not many times more: I
-        # and the workspace over the sets the lowering needs, O over the
-        # (fewer or as many) sets the products need, set j writing O number
-        # j % o_sets. (vgg_first's 39 MB lowering needs 28 sets; its 205 MB O
-        # over 28 sets would be 6.8 GB rotating, past what the address
-        # translation caches cover, where 5 sets span 1 GiB.)
-        prod_foot = es * (self.size_W + self.size_K) + 4 * self.size_O
-        if algo == "fused":
-            prod_foot = es * (self.size_I + self.size_K) + 4 * self.size_O
-            n_io = n_o = min(max(nsets, -(-MIN_ROTATION_BYTES // prod_foot)), 256)
-        else:
-            n_io = min(max(nsets, -(-MIN_ROTATION_BYTES // (es * (self.size_I + self.size_W)))), 256)
-            n_o = min(max(nsets, -(-MIN_ROTATION_BYTES // prod_foot)), n_io)
-        self.o_sets = n_o
-        outs = [torch.empty((i_n, o_h, o_w, k_c), dtype=torch.float32, device=dev) for _ in range(n_o)]
-        self.sets = []
-        for j in range(n_io):
-            I = self.I0.to(dev)
-            if j:
-                I = I.clone()
-            b = dict(I=I, K=self.K0.to(dev), O=outs[j % n_o])
-            if algo != "fused":
-                # the workspace the library asks for, in bytes
-                b["W"] = torch.empty(self.ws, dtype=torch.uint8, device=dev)
-            self.sets.append(b)
+        # Buffer sets. Every operand a kernel reads (I and K; the workspace,
+        # which the products read) rotates over at least READ_ROTATION_BYTES
+        # on its own, twice the 256 MB memory-attached last-level cache, so no
+        # launch finds it there from an earlier one; O, only written, over the
+        # sets that make the products' operands span MIN_ROTATION_BYTES
+        # together. Launch k takes entry k of each list modulo its length.
+        # (Over 5 sets, vgg_first's 9.8 MB I stayed in that cache while 1 GiB
+        # of O went through it: its fused products took 44 us there against
+        # 62 us with I read from HBM.)
+        def read_sets(nbytes):
+            return min(max(nsets, -(-READ_ROTATION_BYTES // max(nbytes, 1))), 256)
+        src = self.size_I if algo == "fused" else self.size_W
+        prod_foot = es * (src + self.size_K) + 4 * self.size_O
+        n_o = min(max(nsets, -(-MIN_ROTATION_BYTES // prod_foot)), 256)
+        self.Is = [self.I0.to(dev) if j == 0 else self.I0.to(dev).clone()
+                   for j in range(read_sets(es * self.size_I))]
+        self.Ks = [self.K0.to(dev) for _ in range(read_sets(es * self.size_K))]
+        self.Os = [torch.empty((i_n, o_h, o_w, k_c), dtype=torch.float32, device=dev) for _ in range(n_o)]
+        # the workspace the library asks for, in bytes
+        self.Ws = [] if algo == "fused" else [torch.empty(self.ws, dtype=torch.uint8, device=dev)
+                                               for _ in range(read_sets(self.ws))]
+        self.nsets = {"I": len(self.Is), "K": len(self.Ks), "W": len(self.Ws), "O": n_o}
+        self.k = 0
+
+    def next(self):
+        """The buffers of the next launch."""
+        k = self.k
+        self.k += 1
+        b = dict(I=self.Is[k % len(self.Is)], K=self.Ks[k % len(self.Ks)], O=self.Os[k % len(self.Os)])
+        if self.Ws:
+            b["W"] = self.Ws[k % len(self.Ws)]
+        return b
 
     def lower(self, b):
         m, (i_n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w) = self.mec, self.dims
@@ -209,14 +215,15 @@ class Config:
         return self.es * (self.size_I + self.size_W)
 
 
-def timed(HipEvent, stream, fn, sets, n):
-    """Average ms of n calls of fn over the rotating sets, between two events."""
+def timed(HipEvent, stream, fn, cfg, n):
+    """Average ms of n calls of fn over the rotating buffers, between two events."""
     import torch
+    bufs = [cfg.next() for _ in range(n)]
     start, end = HipEvent(), HipEvent()
     torch.cuda.synchronize()
     start.record(stream)
-    for k in range(n):
-        fn(sets[k % len(sets)])
+    for b in bufs:
+        fn(b)
     end.record(stream)
     torch.cuda.synchronize()
     return start.elapsed_time(end) / n
@@ -229,7 +236,7 @@ def settle(cfg, seconds):
     n, t0 = 0, time.perf_counter()
     while time.perf_counter() - t0 < seconds:
         for _ in range(8):
-            cfg.step(cfg.sets[n % len(cfg.sets)])
+            cfg.step(cfg.next())
             n += 1
         torch.cuda.synchronize()
     return n
@@ -241,14 +248,14 @@ def measure(cfg, HipEvent, steps, warmup, digest, settle_s):
     with torch.cuda.stream(cfg.stream):
         settled = settle(cfg, settle_s)
         for w in range(warmup):
-            cfg.step(cfg.sets[w % len(cfg.sets)])
+            cfg.step(cfg.next())
         t0 = time.perf_counter()
-        ms_step = timed(HipEvent, cfg.stream, cfg.step, cfg.sets, steps)
+        ms_step = timed(HipEvent, cfg.stream, cfg.step, cfg, steps)
         wall = time.perf_counter() - t0
         lower_ms = None
         if cfg.algo != "fused":
-            lower_ms = timed(HipEvent, cfg.stream, cfg.lower, cfg.sets, steps)
-        prod_ms = timed(HipEvent, cfg.stream, cfg.products, cfg.sets, steps)
+            lower_ms = timed(HipEvent, cfg.stream, cfg.lower, cfg, steps)
+        prod_ms = timed(HipEvent, cfg.stream, cfg.products, cfg, steps)
 
     layer = cfg.layer
     peak = PEAK_TFLOPS[layer.dtype]
@@ -289,7 +296,7 @@ def measure(cfg, HipEvent, steps, warmup, digest, settle_s):
             "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
             "frac": round(gbs / PEAK_HBM_GBS, 4) if layer.name != "tiny" else None,
             "traffic": traffic["lower"], "alg_bytes": lb}
-    out["buffer_sets"], out["o_sets"] = len(cfg.sets), cfg.o_sets
+    out["buffer_sets"] = cfg.nsets
     out["workspace_bytes"] = cfg.ws
     out["im2col_bytes"] = cfg.ws_im2col
     out["workspace_vs_mec_closed_form"] = round(cfg.ws / cfg.ws_lowered, 4) if cfg.algo == "lowered" else None
@@ -352,7 +359,7 @@ def main():
         "dtype": layer.dtype,
         "data": "synthetic (seeded, %s)" % layer.note,
         "config": {"workload": workload_name(layer, cfg.o_h, cfg.o_w),
-                   "algo": args.algo, "buffer_sets": len(cfg.sets), "o_sets": cfg.o_sets},
+                   "algo": args.algo, "buffer_sets": cfg.nsets},
         "workspace_bytes": cfg.ws,
         "im2col_bytes": cfg.ws_im2col,
         "workspace_vs_im2col": round(cfg.ws_im2col / cfg.ws_lowered, 4),

@@ -1619,13 +1619,15 @@ hipError_t dispatch_fixed(const Shape& s, const void* A, const void* K, float* O
         // 207 -> 141 us; 7x7 stride 2 over 3 channels (cv3) 101 / 93 -> 86 us;
         // 5x5 stride 2 over 3 channels 24 / 30 -> 18 us, over 6 channels 28 /
         // 28 -> 21 us; fused, rows of at most 10 elements, 3x3 over 3 channels
-        // (vgg_first, cv7) 51 -> 46 us and 93 -> 83 us. From L those keep the
-        // streaming kernel: with the workspace rotating over 28 buffers (1.1
-        // GB of L and I) the ring read vgg_first's L in 67 us against 61, while
-        // over 4 buffers it was 46 against 51. At stride 1 with longer rows it
-        // is even or slower (3x3 over 16 channels 92 / 81 -> 92 / 89 us, 5x5
-        // over 8 channels even): those keep the tiles.
-        if (!layout && (s.k_h >= 9 || (s.k_h >= 5 && s.s_h >= 2) || (F && s.k_h >= 3 && s.R <= 10)) &&
+        // (vgg_first, cv7) 51 -> 46 us and 93 -> 83 us. From L the ring takes
+        // only windows of at most two blocks (K held in registers, fills five
+        // blocks ahead): with L read from HBM, vgg_first 59 -> 54 us and cv7
+        // 116 -> 99 us against the streaming kernel, which keeps the longer
+        // windows (the ring read those more slowly). At stride 1 with longer
+        // rows it is even or slower (3x3 over 16 channels 92 / 81 -> 92 / 89
+        // us, 5x5 over 8 channels even): those keep the tiles.
+        if (!layout &&
+            (s.k_h >= 9 || (s.k_h >= 5 && s.s_h >= 2) || (s.k_h >= 3 && s.R <= 10 && (F || gemm_ring_short(s)))) &&
             s.R <= 48 && gemm_ring_usable(s, dtype))
             return dry_run ? hipSuccess : launch_gemm_ring(s, A, K, O, F, stream);
         if (s.R >= 32) {

@@ -78,9 +78,35 @@ __device__ inline void ring_dma(const float* base, uint32_t voff, uint32_t lds) 
         : "memory");
 }
 
+// Waits until at most n vector memory operations of this wave are in flight
+// (n >= 0, wave-uniform), rounded down to a multiple of 8 and at most 56: a
+// stricter wait than asked, never a looser one. The counter retires loads,
+// direct-to-LDS loads and stores in the order they were issued.
+__device__ __forceinline__ void wait_vm_at_most(int n) {
+    switch (n >> 3) {
+    case 0: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+    case 1: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
+    case 2: asm volatile("s_waitcnt vmcnt(16)" ::: "memory"); break;
+    case 3: asm volatile("s_waitcnt vmcnt(24)" ::: "memory"); break;
+    case 4: asm volatile("s_waitcnt vmcnt(32)" ::: "memory"); break;
+    case 5: asm volatile("s_waitcnt vmcnt(40)" ::: "memory"); break;
+    case 6: asm volatile("s_waitcnt vmcnt(48)" ::: "memory"); break;
+    default: asm volatile("s_waitcnt vmcnt(56)" ::: "memory"); break;
+    }
+}
+
+// s_waitcnt vmcnt(0) as the instruction the compiler knows (expcnt and
+// lgkmcnt fields at their maxima): its own wait analysis then sees the loads
+// it issued before as complete.
+constexpr int kWaitVm0 = 0x0F70;
+
+// Short windows (at most two blocks of k-steps): blocks whose fills are
+// issued this many blocks ahead of their reads.
+constexpr int kShortLead = 5;
+
 // One piece of work: row groups g_begin .. g_end-1 of the 8 pairs from pair0,
 // channels n0 .. n0 + 32*NB.
-template <int NB, bool FUSED, int BS>
+template <int NB, bool FUSED, int BS, bool SHORT>
 __device__ __forceinline__ void ring_item(const RingParams& p, float* ring, int64_t pair0, int g_begin,
                                           int g_end, int n0) {
     const int lane = threadIdx.x;
@@ -196,6 +222,119 @@ __device__ __forceinline__ void ring_item(const RingParams& p, float* ring, int6
     };
     kload_block(kb0);
 
+    if constexpr (SHORT) {
+        // A window of at most two blocks (nks <= 2 BS): kb0 holds block 0 and
+        // kb1 block 1 (block 0 again when there is one) for the whole item, so
+        // the loop issues no loads into registers, only fills and stores, and
+        // its waits are counted: the fills of block beta's chunks go out
+        // kShortLead blocks ahead, and block beta waits only for what was
+        // issued up to the end of the oldest of the last kShortLead blocks
+        // (or the item's start) by which its chunks had been issued; what was
+        // issued after that may still be in flight. Where the ring could not
+        // hold the chunks that far ahead, the lead is shorter (not on 3x3 or
+        // 5x5 kernels over 1 to 3 channels at strides up to 2).
+        kload_block(kb1);
+        const int nbeta = (g_end - g_begin) * nblk;
+        auto g_of = [&](int beta) { return g_begin + (nblk == 2 ? beta >> 1 : beta); };
+        auto lo_b = [&](int beta) { return blk_lo(g_of(beta), nblk == 2 ? beta & 1 : 0); };
+        auto hi_b = [&](int beta) { return blk_hi(g_of(beta), nblk == 2 ? beta & 1 : 0); };
+        filled = lo_b(0) - 1;
+        {
+            const int want = hi_b(kShortLead - 1 < nbeta - 1 ? kShortLead - 1 : nbeta - 1);
+            const int cap = lo_b(0) + kRingChunks - 1;
+            fill_upto(want < cap ? want : cap);
+        }
+        __builtin_amdgcn_s_waitcnt(kWaitVm0);
+        // mark[i]: the highest chunk issued by the end of block beta - kShortLead + i;
+        // nops[i]: the operations that block issued (the item's start: before block 0)
+        int mark[kShortLead], nops[kShortLead];
+#pragma unroll
+        for (int i = 0; i < kShortLead; ++i) {
+            mark[i] = filled;
+            nops[i] = 0;
+        }
+        floatx16 acc[NB];
+        uint32_t ridx = 0;
+        const uint32_t abase = (uint32_t)(pp * kRingLD);
+        auto short_block = [&](int beta, float (*kuse)[NB]) {
+            const int g = g_of(beta), b = nblk == 2 ? beta & 1 : 0;
+            if (b == 0) {
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) acc[nb][v] = 0.f;
+                ridx = (uint32_t)(g * kRRows * p.srow + ii * p.srow + kofs) & (kRingLen - 1);
+            }
+            const int before = filled;
+            int ops = 0;
+            // the oldest block of the history whose fills reach this block's
+            // chunks: everything issued after it may stay in flight
+            int n = -1, later = 0;
+#pragma unroll
+            for (int i = kShortLead - 1; i >= 0; --i) {
+                if (hi_b(beta) <= mark[i]) n = later;
+                later += nops[i];
+            }
+            if (n >= 0) {
+                wait_vm_at_most(n);
+            } else {  // not issued yet: the ring could not take it that far ahead
+                fill_upto(hi_b(beta));
+                asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            }
+            {
+                const int want = hi_b(beta + kShortLead < nbeta - 1 ? beta + kShortLead : nbeta - 1);
+                const int cap = lo_b(beta) + kRingChunks - 1;
+                fill_upto(want < cap ? want : cap);
+            }
+            ops += kRPairs * (filled - before);
+            float a[BS];
+#pragma unroll
+            for (int u = 0; u < BS; ++u) a[u] = ring[abase + ((ridx + 2 * u) & (kRingLen - 1))];
+            const int t = b * BS;
+            if (2 * (t + BS) > p.KR) {
+#pragma unroll
+                for (int u = 0; u < BS; ++u)
+                    if (2 * (t + u) + kofs >= p.KR) a[u] = 0.f;
+            }
+            ridx = (ridx + 2 * BS) & (kRingLen - 1);
+#pragma unroll
+            for (int u = 0; u < BS; ++u)
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb)
+                    acc[nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[u], kuse[u][nb], acc[nb], 0, 0, 0);
+            if (b + 1 == nblk) {
+#pragma unroll
+                for (int r = 0; r < kRRows; ++r) {
+                    const int64_t h = (int64_t)g * kRRows + r;
+                    if (h >= p.o_h) break;
+                    const int32_t soff = __builtin_amdgcn_readfirstlane((int32_t)(h * p.o_w * p.k_c * 4));
+#pragma unroll
+                    for (int q4 = 0; q4 < 4; ++q4)
+#pragma unroll
+                        for (int nb = 0; nb < NB; ++nb) {
+                            const float v = acc[nb][r * 4 + q4];
+                            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), orsrc,
+                                                                  (int32_t)ooff[q4][nb], soff, kStoreNT);
+                        }
+                    ops += 4 * NB;
+                }
+            }
+#pragma unroll
+            for (int i = 0; i + 1 < kShortLead; ++i) {
+                mark[i] = mark[i + 1];
+                nops[i] = nops[i + 1];
+            }
+            mark[kShortLead - 1] = filled;
+            nops[kShortLead - 1] = ops;
+        };
+        for (int beta = 0; beta < nbeta; beta += 2) {
+            short_block(beta, kb0);
+            if (beta + 1 < nbeta) short_block(beta + 1, kb1);
+        }
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        return;
+    }
+
     // first group: everything its first two blocks read
     filled = blk_lo(g_begin, 0) - 1;
     fill_upto(blk_hi(g_begin, nblk > 1 ? 1 : 0) < blk_lo(g_begin, 0) + kRingChunks - 1
@@ -303,7 +442,7 @@ __device__ __forceinline__ void ring_item(const RingParams& p, float* ring, int6
 // block: when the whole items leave a last, partial round on the wave slots,
 // its items would otherwise run alone at the end while the other slots idle
 // (alexnet_conv1: 12320 one-group items on 2048 slots leave 32).
-template <int NB, bool FUSED, int BS>
+template <int NB, bool FUSED, int BS, bool SHORT>
 __global__ __launch_bounds__(64) void slab_gemm_f32_ring_kernel(RingParams p) {
     __shared__ __align__(16) float ring[kRPairs * kRingLD];
     if (blockIdx.x < p.nfull) {
@@ -311,7 +450,7 @@ __global__ __launch_bounds__(64) void slab_gemm_f32_ring_kernel(RingParams p) {
         const uint32_t unit = t / (uint32_t)p.n_tiles;
         const int g_begin = (int)(unit % (uint32_t)p.items_pg) * p.gpi;
         const int g_end = g_begin + p.gpi < p.ngroups ? g_begin + p.gpi : p.ngroups;
-        ring_item<NB, FUSED, BS>(p, ring, (int64_t)(unit / (uint32_t)p.items_pg) * kRPairs, g_begin, g_end,
+        ring_item<NB, FUSED, BS, SHORT>(p, ring, (int64_t)(unit / (uint32_t)p.items_pg) * kRPairs, g_begin, g_end,
                              (int)(t % (uint32_t)p.n_tiles) * 32 * NB);
     } else {
         // one channel tile (n_tiles == 1): piece = (item, group of the item, channel block)
@@ -320,7 +459,7 @@ __global__ __launch_bounds__(64) void slab_gemm_f32_ring_kernel(RingParams p) {
         const uint32_t unit = p.nfull + piece / per, sub = piece % per;
         const int g = (int)(unit % (uint32_t)p.items_pg) * p.gpi + (int)(sub / NB);
         if (g < p.ngroups)
-            ring_item<1, FUSED, BS>(p, ring, (int64_t)(unit / (uint32_t)p.items_pg) * kRPairs, g, g + 1,
+            ring_item<1, FUSED, BS, SHORT>(p, ring, (int64_t)(unit / (uint32_t)p.items_pg) * kRPairs, g, g + 1,
                                 (int)(sub % NB) * 32);
     }
 }
@@ -415,6 +554,12 @@ bool gemm_ring_usable(const Shape& s, int dtype) {
     return true;
 }
 
+bool gemm_ring_short(const Shape& s) {
+    const int64_t KR = s.k_h * s.R;
+    const int bs = ring_block_steps(KR);
+    return ring_nks(KR, bs) <= 2 * bs;
+}
+
 hipError_t launch_gemm_ring(const Shape& s, const void* A, const void* K, float* O, bool fused,
                             hipStream_t stream) {
     RingParams p{};
@@ -454,19 +599,26 @@ hipError_t launch_gemm_ring(const Shape& s, const void* A, const void* K, float*
     p.nfull = (uint32_t)plan.nfull;
     const int64_t nfull = plan.nfull, npieces = plan.npieces;
     const dim3 grid((uint32_t)(nfull + npieces)), block(64);
-#define MEC_RING(NB_, BS_)                                                                        \
-    if (nb == NB_ && bs == BS_) {                                                                 \
+    const bool short_win = gemm_ring_short(s);  // K fits two blocks: held for the whole item
+#define MEC_RING(NB_, BS_, SHORT_)                                                                \
+    if (nb == NB_ && bs == BS_ && short_win == SHORT_) {                                          \
         if (fused)                                                                                \
-            hipLaunchKernelGGL((slab_gemm_f32_ring_kernel<NB_, true, BS_>), grid, block, 0, stream, p); \
+            hipLaunchKernelGGL((slab_gemm_f32_ring_kernel<NB_, true, BS_, SHORT_>), grid, block, 0, stream, p); \
         else                                                                                      \
-            hipLaunchKernelGGL((slab_gemm_f32_ring_kernel<NB_, false, BS_>), grid, block, 0, stream, p); \
+            hipLaunchKernelGGL((slab_gemm_f32_ring_kernel<NB_, false, BS_, SHORT_>), grid, block, 0, stream, p); \
     }
-    MEC_RING(1, 7)
-    MEC_RING(2, 7)
-    MEC_RING(3, 7)
-    MEC_RING(1, 8)
-    MEC_RING(2, 8)
-    MEC_RING(3, 8)
+    MEC_RING(1, 7, false)
+    MEC_RING(2, 7, false)
+    MEC_RING(3, 7, false)
+    MEC_RING(1, 8, false)
+    MEC_RING(2, 8, false)
+    MEC_RING(3, 8, false)
+    MEC_RING(1, 7, true)
+    MEC_RING(2, 7, true)
+    MEC_RING(3, 7, true)
+    MEC_RING(1, 8, true)
+    MEC_RING(2, 8, true)
+    MEC_RING(3, 8, true)
 #undef MEC_RING
     return hipGetLastError();
 }

@@ -119,6 +119,9 @@ hipError_t launch_gemm_fixed(const Shape& s, const void* A, const void* K, float
 // (mec_gemm_ring.hip): whether its ring of LDS holds the shape's windows, and
 // the launch (dense n-h-w-c O).
 bool gemm_ring_usable(const Shape& s, int dtype);
+// the window takes at most two blocks of k-steps: K stays in registers for an
+// item and fills run several blocks ahead
+bool gemm_ring_short(const Shape& s);
 hipError_t launch_gemm_ring(const Shape& s, const void* A, const void* K, float* O, bool fused,
                             hipStream_t stream);
 

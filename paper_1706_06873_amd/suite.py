@@ -22,11 +22,12 @@ on the same im2col matrix, for context: im2col + vendor GEMM.
 For every layer it times MEC from L (compact lowering + slab products), MEC
 fused, and the im2col baseline (im2col lowering + one product through the
 same kernels), each kernel between HIP events on its stream, on seeded
-synthetic inputs already in device memory (buffer sets rotating so that one
-rotation spans at least 1 GiB, after untimed launches that let the clocks
-settle, as the benchmark does), and prints one JSON line with the
-times, the effective TFLOP/s (2 x MAC / time) and the workspace of MEC
-against im2col. Parity of every one of these shapes with the CPU oracle is
+synthetic inputs already in device memory (every operand a kernel reads
+rotating over at least 512 MB of buffer sets, twice the last-level cache, and
+O over sets that make the fused form's operands span 1 GiB, after untimed
+launches that let the clocks settle, as the benchmark does), and prints one
+JSON line with the times, the effective TFLOP/s (2 x MAC / time) and the
+workspace of MEC against im2col. Parity of every one of these shapes with the CPU oracle is
 checked by the GPU tests, not here.
 """
 import argparse
@@ -42,16 +43,23 @@ from paper_1706_06873_amd import workloads as wl
 from paper_1706_06873_amd.timing import HipEvent
 
 
-MIN_ROTATION_BYTES = 1 << 30  # per rotation: beyond the 256 MB last-level cache
-MAX_SETS = 64
+MIN_ROTATION_BYTES = 1 << 30   # I, K and O of the fused form, together
+READ_ROTATION_BYTES = 1 << 29  # each operand a kernel reads, on its own
+MAX_SETS = 256
 
 
 def _auto_sets(I0, K0, o_elems):
-    """Buffer sets so that one rotation through them spans at least 1 GiB
-    even for the fused form (I, K and O only): no launch finds its operands
-    in the last-level cache from an earlier one."""
+    """Sets of O: one rotation through I, K and O of the fused form spans at
+    least 1 GiB (between 2 and MAX_SETS)."""
     foot = I0.numel() * I0.element_size() + K0.numel() * K0.element_size() + 4 * o_elems
     return max(2, min(MAX_SETS, -(-MIN_ROTATION_BYTES // foot)))
+
+
+def _read_sets(nbytes):
+    """Sets of an operand that a kernel reads (I, K, L or M): one rotation
+    through them spans at least 512 MB, twice the 256 MB last-level cache, so
+    no launch finds it there from an earlier one (between 2 and MAX_SETS)."""
+    return max(2, min(MAX_SETS, -(-READ_ROTATION_BYTES // max(1, nbytes))))
 
 
 def _time_layer(layer, reps, warmup, sets, yardstick=False, settle=0.2):
@@ -62,20 +70,37 @@ def _time_layer(layer, reps, warmup, sets, yardstick=False, settle=0.2):
     P = k_h * k_w * i_c
     dev = torch.device("cuda:0")
     I0, K0 = wl.make_inputs(layer)
-    if sets <= 0:
-        sets = _auto_sets(I0, K0, i_n * o_h * o_w * k_c)
-    bufs = [dict(I=I0.to(dev) if j == 0 else I0.to(dev).clone(), K=K0.to(dev),
-                 O=torch.empty((i_n, o_h, o_w, k_c), dtype=torch.float32, device=dev))
-            for j in range(sets)]
+    es = I0.element_size()
+    if sets > 0:  # one count for every operand
+        n_I = n_K = n_O = n_L = n_M = sets
+    else:
+        n_I, n_K = _read_sets(I0.numel() * es), _read_sets(K0.numel() * es)
+        n_O = _auto_sets(I0, K0, i_n * o_h * o_w * k_c)
+        n_L, n_M = _read_sets(i_n * o_w * i_h * k_w * i_c * es), _read_sets(i_n * o_w * o_h * P * es)
+    Is = [I0.to(dev) if j == 0 else I0.to(dev).clone() for j in range(n_I)]
+    Ks = [K0.to(dev) for _ in range(n_K)]
+    Os = [torch.empty((i_n, o_h, o_w, k_c), dtype=torch.float32, device=dev) for _ in range(n_O)]
+    nsets = {"I": n_I, "K": n_K, "O": n_O}
+    launch = [0]  # launch k takes entry k of each list modulo its length
+
+    def next_bufs(Ws):
+        k = launch[0]
+        launch[0] += 1
+        b = dict(I=Is[k % n_I], K=Ks[k % n_K], O=Os[k % n_O])
+        if Ws:
+            b["W"] = Ws[k % len(Ws)]
+        return b
+
     stream = torch.cuda.Stream(device=dev)
     res = {}
     for algo in ("lowered", "fused", "im2col"):
+        Ws = None
         if algo == "lowered":
-            for b in bufs:
-                b["W"] = torch.empty((i_n, o_w, i_h, k_w, i_c), dtype=I0.dtype, device=dev)
+            Ws = [torch.empty((i_n, o_w, i_h, k_w, i_c), dtype=I0.dtype, device=dev) for _ in range(n_L)]
+            nsets["L"] = n_L
         elif algo == "im2col":
-            for b in bufs:
-                b["W"] = torch.empty((i_n, o_w, o_h, k_h, k_w, i_c), dtype=I0.dtype, device=dev)
+            Ws = [torch.empty((i_n, o_w, o_h, k_h, k_w, i_c), dtype=I0.dtype, device=dev) for _ in range(n_M)]
+            nsets["M"] = n_M
 
         def run(b, ev=None):
             rec = (lambda i: ev[i].record(stream)) if ev else (lambda i: None)
@@ -102,16 +127,17 @@ def _time_layer(layer, reps, warmup, sets, yardstick=False, settle=0.2):
             t0 = time.time()
             k = 0
             while time.time() - t0 < settle:
-                run(bufs[k % sets])
+                run(next_bufs(Ws))
                 k += 1
-                if k % sets == 0:
+                if k % 16 == 0:
                     torch.cuda.synchronize()
             for w in range(warmup):
-                run(bufs[w % sets])
+                run(next_bufs(Ws))
             torch.cuda.synchronize()
             evs = [[HipEvent() for _ in range(3)] for _ in range(reps)]
+            bufs = [next_bufs(Ws) for _ in range(reps)]
             for r in range(reps):
-                run(bufs[r % sets], evs[r])
+                run(bufs[r], evs[r])
             torch.cuda.synchronize()
         tot = sorted(e[0].elapsed_time(e[2]) * 1e3 for e in evs)
         low = sorted(e[0].elapsed_time(e[1]) * 1e3 for e in evs)
@@ -138,13 +164,12 @@ def _time_layer(layer, reps, warmup, sets, yardstick=False, settle=0.2):
             g = med(sorted(e[0].elapsed_time(e[1]) * 1e3 for e in gev))
             res["im2col"]["vendor_gemm_us"] = round(g, 2)
             res["im2col"]["im2col_plus_vendor_gemm_us"] = round(med(low) + g, 2)
-        for b in bufs:
-            b.pop("W", None)
+        del Ws, bufs
         torch.cuda.empty_cache()
     ws_mec = mec.workspace_bytes(*layer.dims, dtype=dt, algo=mec.LOWERED)
     ws_im2col = mec.im2col_bytes(*layer.dims, dtype=dt)
     return {"layer": layer.name, "dims": list(layer.dims), "o": [o_h, o_w], "dtype": layer.dtype,
-            "gflop": round(2.0 * macs / 1e9, 3), "sets": sets, "workspace_mec": ws_mec,
+            "gflop": round(2.0 * macs / 1e9, 3), "sets": nsets, "workspace_mec": ws_mec,
             "workspace_im2col": ws_im2col, "im2col_over_mec": round(ws_im2col / ws_mec, 3),
             "timings": res,
             "mec_speedup_vs_im2col": round(res["im2col"]["us"] / min(res["lowered"]["us"],
@@ -232,7 +257,7 @@ def main(argv=None):
     ap.add_argument("--reps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--sets", type=int, default=0,
-                    help="rotating buffer sets (0: enough that a rotation spans 1 GiB, at most %d)"
+                    help="rotating buffer sets of every operand (0: enough that each operand read spans 512 MB and O with I and K 1 GiB, at most %d)"
                          % MAX_SETS)
     ap.add_argument("--settle", type=float, default=0.2,
                     help="seconds of untimed launches per layer and algorithm before the warm-up")

@@ -384,6 +384,65 @@ def test_ring_products(orc, dims, algo):
     assert rel_l2(run_conv(I, K, s_h, s_w, algo), orc.conv2d_direct(host(I), host(K), s_h, s_w)) <= TOL_F32
 
 
+# Windows of at most two blocks of k-steps (3x3 over 1 to 3 channels, 5x5 over
+# one, and the like): K held in registers for the whole item, fills issued
+# three blocks ahead of their reads, and waits counted per block. The cases
+# reach 1, 2 and 3 channel blocks, two channel tiles, blocks of 8 steps (one
+# and two of them), a 5x5 stride-2 kernel (also from L), and, at stride 8
+# down, blocks whose chunks the ring could not take that far ahead (those wait
+# for everything in flight).
+SHORT_RING_CASES = [
+    (2, 18, 20, 3, 3, 3, 96, 1, 1),       # three channel blocks
+    (1, 19, 21, 3, 3, 3, 130, 1, 1),      # two channel tiles, the second 34 wide
+    (2, 20, 24, 1, 3, 5, 40, 1, 1),       # 15 elements: one block of 8 steps
+    (2, 21, 22, 2, 4, 4, 33, 1, 1),       # 32 elements: two blocks of 8 steps
+    (2, 23, 25, 1, 5, 5, 40, 2, 2),       # 5x5 stride 2 over one channel
+    (3, 58, 10, 3, 3, 3, 40, 8, 1),       # stride 8 down: lead cut short by the ring
+    (2, 58, 12, 2, 3, 5, 70, 8, 2),       # the same with three channel blocks, stride 8 x 2
+]
+
+
+@pytest.mark.parametrize("dims", SHORT_RING_CASES)
+@pytest.mark.parametrize("algo", ["lowered", "fused"])
+def test_ring_short_windows(orc, dims, algo):
+    say("ring short", algo, dims)
+    s_h, s_w = dims[7], dims[8]
+    Ii, Ki = case(79 + sum(dims), dims, dist="int")
+    refi = orc.conv2d_direct(host(Ii), host(Ki), s_h, s_w)
+    assert np.abs(refi).max() < 2 ** 24
+    assert np.array_equal(run_conv(Ii, Ki, s_h, s_w, algo), refi.astype(np.float32))
+    I, K = case(81 + sum(dims), dims)
+    assert rel_l2(run_conv(I, K, s_h, s_w, algo), orc.conv2d_direct(host(I), host(K), s_h, s_w)) <= TOL_F32
+
+
+# Short windows whose launch splits the items of its last partial round:
+# one-group items of 3x3 over 3 channels at 64 channels (16 pieces), and
+# two-group items at 40 channels (32 pieces), on 2048 wave slots.
+SHORT_SPLIT_CASES = [
+    ((257, 6, 66, 3, 3, 3, 64, 1, 1), (1, 2048, 16)),
+    ((257, 10, 66, 3, 3, 3, 40, 1, 1), (2, 2048, 32)),
+]
+
+
+@pytest.mark.parametrize("dims,plan", SHORT_SPLIT_CASES)
+def test_ring_short_split_tail(orc, dims, plan):
+    n, i_h, i_w, i_c, k_h, k_w, k_c, s_h, s_w = dims
+    KR = k_h * k_w * i_c
+    bs = ring_block_steps(KR)
+    nb = 3 if k_c > 64 else 2 if k_c > 32 else 1
+    o_h, o_w = i_h - k_h + 1, i_w - k_w + 1
+    slots = 8 * torch.cuda.get_device_properties(0).multi_processor_count
+    got = ring_plan(-(-n * o_w // 8), -(-o_h // 4), -(-k_c // (32 * nb)), nb, slots,
+                    -(-((KR + 1) // 2) // bs) * bs)
+    say("ring short split", dims, "plan", got)
+    if slots == 2048:
+        assert got == plan
+    I, K = case(87 + sum(dims), dims, dist="int")
+    ref = orc.conv2d_direct(host(I), host(K), s_h, s_w)
+    assert np.abs(ref).max() < 2 ** 24
+    assert np.array_equal(run_conv(I, K, s_h, s_w, "fused"), ref.astype(np.float32))
+
+
 def ring_block_steps(KR):
     """k-steps per block of the ring kernel: 7 where whole blocks of 7 pad the
     window's ceil(KR / 2) steps less than blocks of 8."""
@@ -944,9 +1003,12 @@ def test_layer_full_size_sampled(orc, name):
     g1 = O1.cpu().numpy()
     assert rel_l2(g1[tuple(idx.T)], ref) <= TOL_F32
     i_n, i_h, i_w, i_c, k_h, k_w, k_c, _, _ = layer.dims
-    if layer.dtype == "f32" and 3 <= k_h < 9 and s_h == 1 and k_w * i_c <= 10:
-        # rows of at most 10 elements: fused through the ring kernel, from L
-        # through the streaming kernel -- the same sums in another order
+    KR = k_h * k_w * i_c
+    short = -(-((KR + 1) // 2) // ring_block_steps(KR)) <= 2
+    if layer.dtype == "f32" and 3 <= k_h < 9 and s_h == 1 and k_w * i_c <= 10 and not short:
+        # rows of at most 10 elements and windows longer than two blocks:
+        # fused through the ring kernel, from L through the streaming kernel --
+        # the same sums in another order
         assert rel_l2(O2.cpu().numpy(), g1) <= TOL_F32
     else:
         assert torch.equal(O1, O2)

@@ -68,3 +68,16 @@ def test_auto_sets_span_the_last_level_cache():
         assert 2 <= sets <= suite.MAX_SETS
         assert sets * foot >= suite.MIN_ROTATION_BYTES or sets == suite.MAX_SETS
         assert sets == 2 or (sets - 1) * foot < suite.MIN_ROTATION_BYTES
+
+
+def test_read_sets_span_twice_the_last_level_cache():
+    """Sets of an operand a kernel reads: a rotation through them spans at
+    least 512 MB (twice the 256 MB last-level cache), and one set fewer would
+    not, between 2 and the cap (vgg_first's 9.8 MB input: 55 sets)."""
+    assert suite.READ_ROTATION_BYTES >= 2 * 256 * 10 ** 6
+    for nbytes in [1, 196, 3_211_264, 9_806_208, 19_267_584, 79_149_312, 211_312_640, 2_190_000_000]:
+        n = suite._read_sets(nbytes)
+        assert 2 <= n <= suite.MAX_SETS
+        assert n * nbytes >= suite.READ_ROTATION_BYTES or n == suite.MAX_SETS
+        assert n == 2 or (n - 1) * nbytes < suite.READ_ROTATION_BYTES
+    assert suite._read_sets(16 * 226 * 226 * 3 * 4) == 55
