@@ -691,14 +691,17 @@ def test_flat_window_products_bf16(orc, dims):
 
 
 @pytest.mark.parametrize("shift", [1, 3])
-def test_ring_unaligned_and_guarded(orc, shift):
+@pytest.mark.parametrize("which", ["long", "short"])
+def test_ring_unaligned_and_guarded(orc, shift, which):
     """I, K, L and O one or three elements off their 16-byte boundaries, O
     inside a guard band: element loads and stores only, nothing written
-    outside O."""
-    dims = RING_CASES[2]
-    say("ring unaligned", shift, dims)
+    outside O. An 11x11 stride-4 window, and a short one (3x3 over 3
+    channels, three channel blocks)."""
+    dims = RING_CASES[2] if which == "long" else SHORT_RING_CASES[0]
+    s_h, s_w = dims[7], dims[8]
+    say("ring unaligned", which, shift, dims)
     I, K = case(79 + shift, dims, dist="int")
-    ref = orc.conv2d_direct(host(I), host(K), 4, 4).astype(np.float32)
+    ref = orc.conv2d_direct(host(I), host(K), s_h, s_w).astype(np.float32)
 
     def offset_copy(t):
         buf = torch.zeros(t.numel() + 8, dtype=t.dtype, device=DEV)
@@ -712,7 +715,7 @@ def test_ring_unaligned_and_guarded(orc, shift):
     ws = torch.zeros(mec.workspace_bytes(*dims) + 64, dtype=torch.uint8, device=DEV)[4 * shift:]
     for algo in ("lowered", "fused"):
         buf.fill_(7.0)
-        mec.conv2d(Id, Kd, 4, 4, algo=algo, O=Od, workspace=ws)
+        mec.conv2d(Id, Kd, s_h, s_w, algo=algo, O=Od, workspace=ws)
         torch.cuda.synchronize()
         b = buf.cpu().numpy()
         assert np.all(b[:32 + shift] == 7.0) and np.all(b[32 + shift + ref.size:] == 7.0), algo
