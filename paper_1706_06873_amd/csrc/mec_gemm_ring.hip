@@ -19,11 +19,13 @@
 // v_mfma_f32_32x32x2_f32), padded with zeros to whole blocks of 7 or 8 steps
 // (363 -> 364): no per-row padding of R to a staging width. The wave streams
 // its 8 pairs' rows of L (or, fused, the same elements of I) through a ring in
-// LDS, 512 elements per pair, filled
-// 64 elements at a time by direct-to-LDS loads one block of k-steps ahead of
-// use; every element of the rows it covers is loaded once per item, the
-// overlap between output rows is read from the ring. Waves share nothing, so
-// there is no barrier: several waves per SIMD hide each other's load latency.
+// LDS, 512 elements per pair, filled 64 elements at a time by direct-to-LDS
+// loads one block of k-steps ahead of use, or, where the window takes at most
+// two blocks (3x3 over 1 to 3 channels: K then stays in registers for the
+// whole item), five blocks ahead with waits counted per block. Every element
+// of the rows it covers is loaded once per item, the overlap between output
+// rows is read from the ring. Waves share nothing, so there is no barrier:
+// several waves per SIMD hide each other's load latency.
 #include "mec_mfma.h"
 
 namespace mec {
