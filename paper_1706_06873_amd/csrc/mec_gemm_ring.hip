@@ -170,7 +170,7 @@ __device__ __forceinline__ void ring_item(const RingParams& p, float* ring, int6
         } else {
             rel = (uint32_t)o;
         }
-        const uint32_t slot = (uint32_t)(c % kRingChunks) * kChunk;
+        const uint32_t slot = ((uint32_t)c % kRingChunks) * kChunk;
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 #pragma unroll
         for (int q = 0; q < kRPairs; ++q)
@@ -181,11 +181,15 @@ __device__ __forceinline__ void ring_item(const RingParams& p, float* ring, int6
         for (int c = filled + 1; c <= target; ++c) fill(c);
         if (target > filled) filled = target;
     };
-    // chunks read by block b of group g: [lo, hi]
+    // chunks read by block b of group g: [lo, hi] (the element offsets are
+    // never negative: divided as unsigned, one shift each instead of the
+    // signed division's four scalar instructions; with the ring slot's
+    // unsigned remainder and K's 32-bit resource offset below, 1.5-2.5%
+    // faster on alexnet_conv1, cv1 and cv3)
     const int rspan = (kRRows - 1) * p.srow;
-    auto blk_lo = [&](int g, int b) { return (g * kRRows * p.srow + 2 * BS * b) / kChunk; };
+    auto blk_lo = [&](int g, int b) { return (int)((uint32_t)(g * kRRows * p.srow + 2 * BS * b) / kChunk); };
     auto blk_hi = [&](int g, int b) {
-        return (g * kRRows * p.srow + rspan + 2 * BS * b + 2 * BS - 1) / kChunk;
+        return (int)((uint32_t)(g * kRRows * p.srow + rspan + 2 * BS * b + 2 * BS - 1) / kChunk);
     };
     const int nblk = (p.nks + BS - 1) / BS;
 
@@ -213,7 +217,7 @@ __device__ __forceinline__ void ring_item(const RingParams& p, float* ring, int6
         // padding is less than one block), so the range is not empty
         const uint32_t kfirst = (uint32_t)kt * kstep;
         const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc(
-            const_cast<float*>(p.K) + (int64_t)kt * 2 * p.k_c, (short)0, (int)(kbytes - kfirst), 0x00020000);
+            reinterpret_cast<char*>(const_cast<float*>(p.K)) + kfirst, (short)0, (int)(kbytes - kfirst), 0x00020000);
 #pragma unroll
         for (int u = 0; u < BS; ++u)
 #pragma unroll
