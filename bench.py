@@ -123,6 +123,13 @@ def load_traffic(dtype, layer_name, algo, digest):
     return out
 
 
+def rotation_sets(nbytes, nsets):
+    """Buffer sets for an operand of `nbytes` that a kernel reads: enough that
+    one rotation through them spans READ_ROTATION_BYTES, at least `nsets`, at
+    most 256."""
+    return min(max(nsets, -(-READ_ROTATION_BYTES // max(nbytes, 1))), 256)
+
+
 class Config:
     """One layer and algorithm: sizes, algorithmic work, buffers and launches."""
 
@@ -153,8 +160,7 @@ class Config:
         # (Over 5 sets, vgg_first's 9.8 MB I stayed in that cache while 1 GiB
         # of O went through it: its fused products took 44 us there against
         # 62 us with I read from HBM.)
-        def read_sets(nbytes):
-            return min(max(nsets, -(-READ_ROTATION_BYTES // max(nbytes, 1))), 256)
+        read_sets = lambda nbytes: rotation_sets(nbytes, nsets)
         src = self.size_I if algo == "fused" else self.size_W
         prod_foot = es * (src + self.size_K) + 4 * self.size_O
         n_o = min(max(nsets, -(-MIN_ROTATION_BYTES // prod_foot)), 256)

@@ -81,3 +81,20 @@ def test_read_sets_span_twice_the_last_level_cache():
         assert n * nbytes >= suite.READ_ROTATION_BYTES or n == suite.MAX_SETS
         assert n == 2 or (n - 1) * nbytes < suite.READ_ROTATION_BYTES
     assert suite._read_sets(16 * 226 * 226 * 3 * 4) == 55
+
+
+def test_bench_rotation_sets():
+    """The benchmark's sets per read operand: a rotation spans at least
+    512 MB (twice the 256 MB last-level cache), never fewer than asked for,
+    at most 256 (vgg_first's 9.8 MB input: 55 sets; alexnet_conv1's 211 MB
+    lowered tensor: 4 at the default of 4)."""
+    import bench
+    assert bench.READ_ROTATION_BYTES >= 2 * 256 * 10 ** 6
+    assert bench.rotation_sets(16 * 226 * 226 * 3 * 4, 4) == 55
+    assert bench.rotation_sets(210_946_560, 4) == 4
+    assert bench.rotation_sets(210_946_560, 1) == 3
+    assert bench.rotation_sets(196, 4) == 256
+    for nbytes in [1, 3_211_264, 29_159_424, 79_149_312, 2_190_000_000]:
+        n = bench.rotation_sets(nbytes, 1)
+        assert n * nbytes >= bench.READ_ROTATION_BYTES or n == 256
+        assert n == 1 or (n - 1) * nbytes < bench.READ_ROTATION_BYTES
